@@ -1,0 +1,19 @@
+"""fp64 CPU oracle for the FlipFlop Hessian estimate.
+
+TEST INFRASTRUCTURE ONLY.  This package is the slow, plain reference that the
+GPU path is checked against.  Only the test-suite, the smoke check and the
+benchmark's CPU-baseline leg may import it; the product path (the HIP
+library and its Python binding) never does, and shares no code with it.
+
+Every function cites the passage of the paper it follows.  Where the paper
+leaves a choice open, the reading taken is stated in the docstring.
+"""
+from .flipflop import (FlipFlopResult, NotSPDError, as_f64_samples, half_step_B,
+                       half_step_A, normalise, damp, flipflop, loglik)
+from .metrics import kron_rel_error, kron_rel_error_scale_free, trace_identity
+from .kron import kron_apply, mismatch_factor
+
+__all__ = ["FlipFlopResult", "NotSPDError", "as_f64_samples", "half_step_B",
+           "half_step_A", "normalise", "damp", "flipflop", "loglik",
+           "kron_rel_error", "kron_rel_error_scale_free", "trace_identity",
+           "kron_apply", "mismatch_factor"]

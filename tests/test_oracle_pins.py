@@ -1,0 +1,346 @@
+"""Pins of the fp64 oracle against what the paper and the mathematics fix.
+
+None of these re-types the oracle's own formula: each checks it against an
+independent route (a library routine, the explicit mn x mn Kronecker form,
+a closed form, a brute-force optimisation, or an invariance of the method),
+chosen so that a dropped term, a wrong scale, a transposed operand or a
+swapped side fails at least one of them.
+"""
+import numpy as np
+import pytest
+import scipy.linalg as sla
+import scipy.optimize as sopt
+from scipy.stats import multivariate_normal
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.filterwarnings("ignore::RuntimeWarning")
+
+
+# ----------------------------------------------------------------- helpers
+
+def rand_spd(dim, rng, cond=10.0):
+    Q = synth.haar_orthogonal(dim, rng)
+    lam = np.geomspace(1.0, 1.0 / cond, dim)
+    return (Q * lam) @ Q.T
+
+
+def matrix_normal(N, A, B, rng):
+    """Samples with Cov(vec G) = A (x) B (column-major vec)."""
+    m, n = B.shape[0], A.shape[0]
+    SA = np.linalg.cholesky(A)
+    SB = np.linalg.cholesky(B)
+    Z = rng.standard_normal((N, m, n))
+    return SB[None] @ Z @ SA.T[None]
+
+
+def vec_cm(G):
+    """Column-major vec of each sample: (N, m n)."""
+    return np.stack([g.reshape(-1, order="F") for g in G])
+
+
+def explicit_H(G):
+    V = vec_cm(G)
+    return V.T @ V / G.shape[0]
+
+
+def explicit_loglik(G, A, B):
+    """Gaussian log-likelihood with the explicit mn x mn covariance A (x) B."""
+    K = np.kron(A, B)
+    return float(np.sum(multivariate_normal(mean=np.zeros(K.shape[0]), cov=K).logpdf(vec_cm(G))))
+
+
+def normalised(A, B):
+    c = np.trace(A) / A.shape[0]
+    return A / c, B * c
+
+
+# -------------------------------------------------- p1: textbook reduction
+
+def test_first_half_step_is_uncentred_second_moment():
+    """With A = I the B update is the second moment of the N n columns
+    (Table 1 'Marginal'/'Input' factors; Appendix B start from I)."""
+    rng = np.random.default_rng(1)
+    N, m, n = 7, 5, 9
+    G = rng.standard_normal((N, m, n))
+    cols = G.transpose(1, 0, 2).reshape(m, N * n)          # every column g of every sample
+    mom = np.cov(cols, bias=True) + np.outer(cols.mean(1), cols.mean(1))
+    B1 = oracle.half_step_B(G, np.eye(n))
+    np.testing.assert_allclose(B1, mom, rtol=1e-13, atol=1e-14)
+    rows = G.reshape(N * m, n)                               # every row of every sample
+    momA = np.cov(rows.T, bias=True) + np.outer(rows.mean(0), rows.mean(0))
+    A1 = oracle.half_step_A(G, np.eye(m))
+    np.testing.assert_allclose(A1, momA, rtol=1e-13, atol=1e-14)
+
+
+def test_damping_adds_mean_diagonal():
+    """Appendix B damping: X + kappa * mean(diag X) * I."""
+    rng = np.random.default_rng(2)
+    G = rng.standard_normal((6, 4, 5))
+    r = oracle.flipflop(G, 1, damping=0.1, keep_half_steps=True)
+    _, _, B1 = r.half_steps[0]
+    cols = G.transpose(1, 0, 2).reshape(4, -1)
+    mom = cols @ cols.T / cols.shape[1]
+    np.testing.assert_allclose(B1, mom + 0.1 * np.mean(np.diag(mom)) * np.eye(4), rtol=1e-13)
+
+
+# ------------------------------------------- p2: orthogonal design, exact
+
+@pytest.mark.parametrize("m,n", [(5, 7), (4, 3), (1, 6), (6, 1)])
+def test_orthogonal_design_recovers_truth_in_one_iteration(m, n):
+    """N = m n samples sqrt(mn) S_B e_k e_l^T S_A^T make the sample H exactly
+    A (x) B, so one iteration must return (A, B) up to the trace scale."""
+    rng = np.random.default_rng(3 + m + n)
+    A = rand_spd(n, rng, 30.0)
+    B = rand_spd(m, rng, 20.0)
+    SA = np.linalg.cholesky(A)
+    SB = np.linalg.cholesky(B)
+    G = []
+    for k in range(m):
+        for l in range(n):
+            Z = np.zeros((m, n))
+            Z[k, l] = np.sqrt(m * n)
+            G.append(SB @ Z @ SA.T)
+    G = np.array(G)
+    np.testing.assert_allclose(explicit_H(G), np.kron(A, B), atol=1e-12)
+    r = oracle.flipflop(G, 1)
+    At, Bt = normalised(A, B)
+    assert oracle.kron_rel_error(r.A, r.B, At, Bt) < 1e-13
+    np.testing.assert_allclose(r.A, At, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(r.B, Bt, rtol=1e-12, atol=1e-13)
+
+
+# -------------------------------------------------- p3: trace identity
+
+@pytest.mark.parametrize("order", ["B_FIRST", "A_FIRST"])
+def test_trace_identity_after_every_half_step(order):
+    """(1/mn) tr(H (A(x)B)^-1) = 1 after each maximum-likelihood half step,
+    with H and the Kronecker inverse formed explicitly (Section 5)."""
+    rng = np.random.default_rng(4)
+    N, m, n = 30, 3, 4
+    G = matrix_normal(N, rand_spd(n, rng), rand_spd(m, rng), rng)
+    H = explicit_H(G)
+    r = oracle.flipflop(G, 4, order=order, keep_half_steps=True)
+    assert len(r.half_steps) == 8
+    for _, A, B in r.half_steps:
+        t = np.trace(H @ np.linalg.inv(np.kron(A, B))) / (m * n)
+        assert abs(t - 1.0) < 1e-12
+        assert abs(oracle.trace_identity(G, A, B) - 1.0) < 1e-12
+
+
+# ------------------------------------------- p4: monotone log-likelihood
+
+def test_loglik_matches_explicit_gaussian_and_is_monotone():
+    rng = np.random.default_rng(5)
+    N, m, n = 25, 3, 4
+    G = matrix_normal(N, rand_spd(n, rng, 50), rand_spd(m, rng, 50), rng)
+    G += 0.3 * rng.standard_normal(G.shape)                  # not exactly Kronecker
+    r = oracle.flipflop(G, 6, keep_half_steps=True)
+    prev = explicit_loglik(G, np.eye(n), np.eye(m))
+    for _, A, B in r.half_steps:
+        ll = explicit_loglik(G, A, B)
+        assert abs(ll - oracle.loglik(G, A, B)) < 1e-9 * abs(ll)
+        assert ll >= prev - 1e-9 * abs(prev)
+        prev = ll
+    # the normalisation leaves the likelihood unchanged
+    A, B = r.half_steps[-1][1], r.half_steps[-1][2]
+    assert abs(explicit_loglik(G, 3.0 * A, B / 3.0) - explicit_loglik(G, A, B)) < 1e-9 * abs(prev)
+
+
+# ----------------------------------------------------- p5: brute force
+
+def test_fixed_point_matches_brute_force_mle():
+    """Maximise the explicit mn x mn Gaussian likelihood over Cholesky
+    parameters of A and B with BFGS; the flip-flop fixed point must agree."""
+    rng = np.random.default_rng(6)
+    N, m, n = 40, 2, 3
+    G = matrix_normal(N, rand_spd(n, rng, 8), rand_spd(m, rng, 8), rng)
+    G += 0.2 * rng.standard_normal(G.shape)
+    V = vec_cm(G)
+    S = V.T @ V
+
+    il_n = np.tril_indices(n)
+    il_m = np.tril_indices(m)
+
+    def unpack(th):
+        LA = np.zeros((n, n))
+        LA[il_n] = th[:len(il_n[0])]
+        LB = np.zeros((m, m))
+        LB[il_m] = th[len(il_n[0]):]
+        return LA @ LA.T, LB @ LB.T
+
+    def nll(th):
+        A, B = unpack(th)
+        K = np.kron(A, B)
+        sign, logdet = np.linalg.slogdet(K)
+        if sign <= 0:
+            return 1e30
+        return 0.5 * N * logdet + 0.5 * np.trace(np.linalg.solve(K, S))
+
+    th0 = np.concatenate([np.eye(n)[il_n], np.eye(m)[il_m]])
+    best = sopt.minimize(nll, th0, method="BFGS", options={"gtol": 1e-10, "maxiter": 10000})
+    Ab, Bb = normalised(*unpack(best.x))
+    r = oracle.flipflop(G, 300)
+    assert oracle.kron_rel_error(r.A, r.B, Ab, Bb) < 1e-5
+
+
+# ------------------------------------------------- p6: order independence
+
+def test_fixed_point_independent_of_update_order():
+    rng = np.random.default_rng(7)
+    N, m, n = 50, 6, 8
+    G = matrix_normal(N, rand_spd(n, rng, 20), rand_spd(m, rng, 20), rng)
+    G += 0.3 * rng.standard_normal(G.shape)
+    rb = oracle.flipflop(G, 400, order="B_FIRST")
+    ra = oracle.flipflop(G, 400, order="A_FIRST")
+    assert oracle.kron_rel_error(rb.A, rb.B, ra.A, ra.B) < 1e-9
+    # ... but a few iterations in, the two orders are different iterates
+    rb2 = oracle.flipflop(G, 2, order="B_FIRST")
+    ra2 = oracle.flipflop(G, 2, order="A_FIRST")
+    assert oracle.kron_rel_error(rb2.A, rb2.B, ra2.A, ra2.B) > 1e-6
+
+
+# ------------------------------------------------------ p7: consistency
+
+def test_recovers_truth_at_rate_n_to_minus_half():
+    """Noise-free matrix-normal samples: the error of A (x) B against the
+    true factors falls like N^-1/2 (the iteration is the MLE)."""
+    w = synth.Workload("consistency", 6, 5, 0, 30, 1.0, 1.0, "normal", 0, 0.0, "f32", 0)
+    Ns = [50, 200, 800, 3200]
+    errs = []
+    for N in Ns:
+        e = []
+        for s in range(6):
+            d = synth.generate(w.scaled(N=N), seed=1000 + s, threads=1)
+            r = oracle.flipflop(d.G, 30)
+            e.append(oracle.kron_rel_error(r.A, r.B, *normalised(d.A_true, d.B_true)))
+        errs.append(np.mean(e))
+    slope = np.polyfit(np.log(Ns), np.log(errs), 1)[0]
+    assert -0.65 < slope < -0.35, (slope, errs)
+    assert errs[-1] < 0.05
+
+
+# ------------------------------------------------------ p8: equivariance
+
+def test_equivariance_rotations_scale_permutation():
+    rng = np.random.default_rng(8)
+    N, m, n = 20, 5, 7
+    G = matrix_normal(N, rand_spd(n, rng, 10), rand_spd(m, rng, 10), rng)
+    G += 0.2 * rng.standard_normal(G.shape)
+    base = oracle.flipflop(G, 5)
+    U = synth.haar_orthogonal(m, rng)
+    V = synth.haar_orthogonal(n, rng)
+    rot = oracle.flipflop(U[None] @ G @ V.T[None], 5)
+    np.testing.assert_allclose(rot.A, V @ base.A @ V.T, rtol=1e-9, atol=1e-10)
+    np.testing.assert_allclose(rot.B, U @ base.B @ U.T, rtol=1e-9, atol=1e-10)
+    sc = oracle.flipflop(3.0 * G, 5)
+    np.testing.assert_allclose(sc.A, base.A, rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(sc.B, 9.0 * base.B, rtol=1e-11, atol=1e-12)
+    perm = oracle.flipflop(G[rng.permutation(N)], 5)
+    np.testing.assert_allclose(perm.A, base.A, rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(perm.B, base.B, rtol=1e-11, atol=1e-12)
+
+
+# ------------------------------------------------- p10: degenerate shapes
+
+def test_single_row_and_single_column_layers():
+    """m = 1: B is a scalar b; A b is the second moment S of the rows after
+    one iteration and stays there.  n = 1 is the mirror image."""
+    rng = np.random.default_rng(9)
+    N, n = 40, 6
+    G = rng.standard_normal((N, 1, n)) @ np.diag(np.linspace(0.5, 2.0, n))
+    rows = G[:, 0, :]
+    S = rows.T @ rows / N
+    for it in (1, 2, 5):
+        r = oracle.flipflop(G, it)
+        np.testing.assert_allclose(r.A, n * S / np.trace(S), rtol=1e-12)
+        np.testing.assert_allclose(r.B, [[np.trace(S) / n]], rtol=1e-12)
+    Gt = np.transpose(G, (0, 2, 1))                            # n = 1, m = 6
+    r = oracle.flipflop(Gt, 3)
+    np.testing.assert_allclose(r.A * r.B, S, rtol=1e-12)
+    assert r.A.shape == (1, 1) and abs(r.A[0, 0] - 1.0) < 1e-15
+
+
+# ---------------------------------------------- failures (Section 2 convention)
+
+def test_rank_deficient_samples_raise_not_spd():
+    rng = np.random.default_rng(10)
+    G = rng.standard_normal((2, 3, 9))        # N m = 6 < n = 9: A-update singular
+    with pytest.raises(oracle.NotSPDError) as ei:
+        oracle.flipflop(G, 3)
+    assert ei.value.iteration == 2             # A_1 is singular, B_2 needs A_1^-1
+    r = oracle.flipflop(G, 3, damping=0.1)     # damping makes it well posed
+    assert np.all(np.linalg.eigvalsh(r.A) > 0)
+    Gn = rng.standard_normal((4, 3, 3))
+    Gn[1, 0, 0] = np.nan
+    with pytest.raises(oracle.NotSPDError):
+        oracle.flipflop(Gn, 1)
+
+
+# ---------------------------------------------------- metric and apply pins
+
+def test_kron_rel_error_matches_explicit_kronecker():
+    rng = np.random.default_rng(11)
+    A, Ar = rand_spd(4, rng), rand_spd(4, rng)
+    B, Br = rand_spd(3, rng), rand_spd(3, rng)
+    ref = np.linalg.norm(np.kron(A, B) - np.kron(Ar, Br)) / np.linalg.norm(np.kron(Ar, Br))
+    assert abs(oracle.kron_rel_error(A, B, Ar, Br) - ref) < 1e-14
+    # tiny perturbations: the stable form keeps digits the expanded form loses
+    dA = 1e-9 * rng.standard_normal((4, 4))
+    e = oracle.kron_rel_error(Ar + dA, Br, Ar, Br)
+    assert abs(e - np.linalg.norm(dA) / np.linalg.norm(Ar)) < 1e-6 * e
+
+
+def test_kron_apply_matches_explicit_kronecker():
+    rng = np.random.default_rng(12)
+    m, n = 3, 5
+    A, B = rand_spd(n, rng), rand_spd(m, rng)
+    X = rng.standard_normal((2, m, n))
+    Y = oracle.kron_apply(A, B, X)
+    K = np.kron(A, B)
+    for b in range(2):
+        np.testing.assert_allclose(Y[b].reshape(-1, order="F"), K @ X[b].reshape(-1, order="F"),
+                                   rtol=1e-12)
+    Yi = oracle.kron_apply(A, B, X, inverse=True)
+    for b in range(2):
+        np.testing.assert_allclose(Yi[b].reshape(-1, order="F"),
+                                   np.linalg.solve(K, X[b].reshape(-1, order="F")), rtol=1e-10)
+
+
+# ------------------------------------------------- p9: mismatch factor
+
+def test_mismatch_factor_identities():
+    """Section 4: Phi >= 1 with equality iff H is proportional to A (x) B;
+    eq. (6) ties log Phi to the KL divergence minimised over a scale; and
+    since each half step minimises Phi over one factor, Phi never rises."""
+    rng = np.random.default_rng(13)
+    m, n = 2, 3
+    N = 60                                      # N >= mn: H nonsingular
+    G = matrix_normal(N, rand_spd(n, rng, 5), rand_spd(m, rng, 5), rng)
+    G += 0.5 * rng.standard_normal(G.shape)
+    H = explicit_H(G)
+    A, B = rand_spd(n, rng), rand_spd(m, rng)
+    assert abs(oracle.mismatch_factor(7.0 * np.kron(A, B), A, B) - 1.0) < 1e-12
+    phi = oracle.mismatch_factor(H, A, B)
+    assert phi > 1.0
+    K = np.kron(A, B)
+    d = m * n
+
+    def kl(s):   # KL(N(0,H) || N(0, sK))
+        Ks = s * K
+        return 0.5 * (np.trace(np.linalg.solve(Ks, H)) - d
+                      + np.linalg.slogdet(Ks)[1] - np.linalg.slogdet(H)[1])
+
+    best = sopt.minimize_scalar(lambda t: kl(np.exp(t)), bracket=(-5, 5), tol=1e-12)
+    assert abs(np.log(phi) - 2.0 / d * best.fun) < 1e-9
+    r = oracle.flipflop(G, 5, keep_half_steps=True)
+    prev = oracle.mismatch_factor(H, np.eye(n), np.eye(m))
+    for kind, A, B in r.half_steps:
+        phi = oracle.mismatch_factor(H, A, B)
+        assert phi <= prev * (1 + 1e-12)
+        prev = phi
+        if kind == "A":    # trace identity: Phi |H|^(1/mn) = |A|^(1/n) |B|^(1/m)
+            lhs = np.log(phi) + np.linalg.slogdet(H)[1] / d
+            rhs = np.linalg.slogdet(A)[1] / n + np.linalg.slogdet(B)[1] / m
+            assert abs(lhs - rhs) < 1e-10
