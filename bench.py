@@ -1,0 +1,175 @@
+"""Benchmark of the FlipFlop Hessian engine on one MI355X.
+
+A step is one flip-flop iteration (Section 5): both whitening passes, both
+symmetric products and reductions, both Cholesky + inverse factorisations,
+the trace normalisation and the log-likelihood.  The timed region is one
+whole job: ff_init on the device-resident samples (internal transposed copy)
+followed by ff_iterate over `--steps` iterations, bracketed by stream
+synchronisation; the value is iterations per second of that job.
+
+Prints one JSON line.  The per-kernel durations come from HIP events
+recorded by the library on its stream inside the timed region; the CPU
+baseline times the fp64 oracle on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "flip-flop iter/s + TFLOP/s (% bf16 MFMA peak), m=n=4096, N=128"
+PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+
+
+def cpu_baseline(G, w, budget_s: float):
+    """Oracle time of one iteration, from a bounded number of samples.
+
+    Both half steps are timed on the first k samples (k grows until the
+    budget is used), each against a fixed SPD factor (the per-sample cost of
+    a Cholesky solve does not depend on its values); an iteration over all N
+    samples costs N/k times that, the two Cholesky factorisations being
+    negligible next to the per-sample solves and products.
+    """
+    import numpy as np
+    import torch
+    from threadpoolctl import threadpool_info
+
+    import oracle
+
+    In = np.eye(w.n)
+    Im = np.eye(w.m)
+    t_total = 0.0
+    k = 0
+    host = []
+    while k < w.N and (t_total < budget_s or k < 1):
+        Gi = G[k:k + 1]
+        if Gi.dtype == torch.bfloat16:
+            host.append(Gi.view(torch.int16).cpu().numpy().view(np.uint16))
+        else:
+            host.append(Gi.cpu().numpy())
+        Gs = np.concatenate(host)
+        t0 = time.perf_counter()
+        Gk = oracle.as_f64_samples(Gs[-1:])
+        oracle.half_step_B(Gk, In)
+        oracle.half_step_A(Gk, Im)
+        t_total += time.perf_counter() - t0
+        k += 1
+    per_iter = t_total / k * w.N
+    threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"]
+                  or [1])
+    return {"value": 1.0 / per_iter, "unit": "iter/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"both fp64 half steps (direct cho_solve + dgemm form) on {k} of {w.N} samples "
+                      f"of {w.name}, {t_total:.1f} s, scaled to a full iteration ({per_iter:.1f} s)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10, help="timed flip-flop iterations")
+    ap.add_argument("--warmup", type=int, default=2, help="untimed iterations on a separate handle")
+    ap.add_argument("--workload", default="attn",
+                    help="tiny | attn | mlp_up | mlp_down | mlp_large")
+    ap.add_argument("--seed", type=int, default=None)
+    ap.add_argument("--whiten-split", type=int, default=1)
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: the FlipFlop engine is a single-GPU build "
+              "(sharding over samples is described in the design notes, not built).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import synth
+    import paper_2609_14706_amd as ffe
+
+    dev = torch.device("cuda:0")
+    w = synth.workload(args.workload)
+    t0 = time.perf_counter()
+    G = synth.generate_device(w, seed=args.seed, device=dev)
+    torch.cuda.synchronize()
+    print(f"[bench] generated {w.name} ({G.numel() * G.element_size() / 1e9:.2f} GB) in "
+          f"{time.perf_counter() - t0:.1f} s", file=sys.stderr, flush=True)
+    nbytes = ffe.FlipFlop.workspace_bytes(w.m, w.n, w.N, w.dtype, args.whiten_split)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    if args.warmup > 0:
+        f = ffe.FlipFlop(G, whiten_split=args.whiten_split, workspace=ws, stream=stream)
+        f.iterate(args.warmup)
+        f.close()
+    torch.cuda.synchronize()
+    print(f"[bench] warmup done ({args.warmup} iterations)", file=sys.stderr, flush=True)
+
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    f = ffe.FlipFlop(G, whiten_split=args.whiten_split, workspace=ws, stream=stream)
+    f.set_timing(True)
+    ll = f.iterate(args.steps)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms_total = ev0.elapsed_time(ev1)
+    kern = {k: f.kernel_timing(k) for k in ("whiten", "syrk", "reduce", "cholinv")}
+    f.close()
+    ms_per_step = ms_total / args.steps
+    iters_per_s = 1000.0 / ms_per_step
+    flop_iter = w.flop_per_iter
+    tflops = flop_iter / (ms_per_step * 1e-3) / 1e12
+    peak = PEAK_TFLOPS[w.dtype]
+    print(f"[bench] {args.steps} iterations in {ms_total:.2f} ms; kernels: " +
+          ", ".join(f"{k}: {n} x {ms / max(n, 1):.3f} ms" for k, (n, ms, _) in kern.items()),
+          file=sys.stderr, flush=True)
+
+    dom = max(("whiten", "syrk"), key=lambda k: kern[k][1])
+    n_l, ms_l, fl_l = kern[dom]
+    achieved = fl_l / (ms_l * 1e-3) / 1e12 if ms_l > 0 else 0.0
+    roofline = {"bound": "mfma", "kernel": {"whiten": "k_whiten_bf16", "syrk": "k_syrk_bf16"}[dom]
+                if w.dtype == "bf16" else "k_gemm_f32",
+                "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 4), "traffic": None,
+                "launches": n_l, "avg_launch_ms": round(ms_l / max(n_l, 1), 4),
+                "alg_flop_per_launch": fl_l / max(n_l, 1)}
+
+    out = {
+        "metric": METRIC,
+        "value": round(iters_per_s, 4),
+        "unit": "iter/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "m": w.m, "n": w.n, "N": w.N,
+                   "timed_job": f"ff_init + {args.steps} iterations",
+                   "whiten_split": args.whiten_split},
+        "tflops": round(tflops, 2),
+        "pct_peak": round(100.0 * tflops / peak, 2),
+        "alg_flop_per_iter": flop_iter,
+        "loglik_last": ll[-1] if ll else None,
+        "kernels_ms": {k: round(ms, 3) for k, (n, ms, _) in kern.items()},
+        "roofline": roofline,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the fp64 oracle on host cores", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(G, w, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,165 @@
+/*
+ * ff.h -- C ABI of the FlipFlop Hessian engine for AMD MI355X (gfx950).
+ *
+ * The engine estimates the Kronecker-factored Hessian H ~ A (x) B of one
+ * linear layer W (m x n) from N samples G_i (m x n), with
+ * H = E[vec(G) vec(G)^T] and column-major vec (paper, Section 2 notation and
+ * Section 5).  A (n x n) is the input-side factor, B (m x m) the output-side
+ * factor.  The estimate is the flip-flop iteration of Section 5, i.e. the
+ * matrix-normal maximum-likelihood iteration:
+ *
+ *     B <- (1/(N n)) sum_i G_i A^-1 G_i^T          (update of B for fixed A)
+ *     A <- (1/(N m)) sum_i G_i^T B^-1 G_i          (update of A for fixed B)
+ *     c = tr(A)/n;  A <- A/c;  B <- B c            (scale fixed: tr(A) = n)
+ *
+ * started from A = I_n with B updated first (Appendix B convention; one
+ * iteration = one update of B and one of A).  Optional damping (Appendix B)
+ * adds kappa * tr(X)/dim * I to each factor right after its update.
+ *
+ * Conventions shared by every entry point
+ *  - Every call returns an ff_status; no C++ exception crosses this ABI.
+ *    On error, out-parameters are left untouched (except *iters_done, which
+ *    ff_iterate always writes).  ff_last_error() gives a message for the
+ *    most recent failure on the calling thread.
+ *  - The library never allocates device memory.  G, the workspace, A0/B0,
+ *    X/Y and the output buffers are owned by the caller.  Host memory for
+ *    the handle itself is allocated by ff_init and freed by ff_destroy.
+ *  - Device pointers must be 256-byte aligned where stated, otherwise
+ *    16-byte aligned.  All matrices are dense row-major.
+ *  - Work is enqueued on cfg.stream (a hipStream_t; NULL = default stream).
+ *    ff_iterate, ff_factors(on_host=1) and ff_kron_apply synchronise that
+ *    stream once before returning; the others return without waiting.
+ *  - A handle is not thread-safe; distinct handles are independent.  The
+ *    device that is current at ff_init must be current for every later
+ *    call on the handle.
+ */
+#ifndef FF_H
+#define FF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ff_handle_s* ff_handle;
+
+typedef enum {
+  FF_OK = 0,
+  FF_ERR_INVALID_ARG = 1, /* bad shape, dtype, pointer, alignment or option */
+  FF_ERR_NOT_SPD = 2,     /* a factor to be inverted had a pivot <= 0 or NaN */
+  FF_ERR_WORKSPACE = 3,   /* workspace missing, too small or misaligned */
+  FF_ERR_HIP = 4,         /* a HIP runtime call failed */
+  FF_ERR_STATE = 5        /* call not valid in the handle's state */
+} ff_status;
+
+/* Element type of the samples G.  The factors are always fp32.
+ * FF_F32: every product runs in fp32 (fp32 matrix cores, fp32 accumulate).
+ * FF_BF16: G is bf16; the whitening operand L^-1 and the whitened samples
+ * are rounded to bf16 (round to nearest even) and all products accumulate
+ * in fp32 on the bf16 matrix cores; factorisations stay in fp32. */
+typedef enum { FF_F32 = 0, FF_BF16 = 1 } ff_dtype;
+
+/* Update order.  B_FIRST (default; Appendix B): start from A0 (I_n if NULL),
+ * each iteration updates B then A.  A_FIRST (Section 5 indexing): start from
+ * B0 (I_m if NULL), each iteration updates A then B.  Both end each
+ * iteration with the trace normalisation tr(A) = n and share the same fixed
+ * point; their iterates differ. */
+typedef enum { FF_ORDER_B_FIRST = 0, FF_ORDER_A_FIRST = 1 } ff_order;
+
+/* ff_kron_apply modes: (A (x) B) vec(X) = vec(B X A) (A symmetric), and
+ * its inverse vec(B^-1 X A^-1). */
+typedef enum { FF_APPLY = 0, FF_APPLY_INV = 1 } ff_apply_mode;
+
+typedef struct {
+  int64_t m, n, N;        /* G is [N][m][n], row-major, contiguous; all >= 1 */
+  ff_dtype dtype;         /* element type of G */
+  const void* G;          /* DEVICE pointer, 16-byte aligned, BORROWED: must
+                             stay valid and unmodified until ff_destroy */
+  void* stream;           /* hipStream_t for all work of this handle */
+  ff_order order;
+  double damping;         /* kappa >= 0 (0 for the plain iteration) */
+  const float* A0;        /* optional DEVICE n x n SPD start for A (B_FIRST);
+                             NULL = I_n.  Copied at ff_init */
+  const float* B0;        /* optional DEVICE m x m SPD start for B (A_FIRST);
+                             NULL = I_m.  Copied at ff_init */
+  int whiten_split;       /* FF_BF16 only: 1 = L^-1 rounded to bf16 once;
+                             2 = L^-1 split as hi + lo bf16 parts (two passes,
+                             smaller whitening error).  Ignored for FF_F32 */
+  void* workspace;        /* DEVICE scratch, 256-byte aligned, owned by the
+                             caller, >= ff_workspace_size() bytes; must stay
+                             valid until ff_destroy */
+  size_t workspace_bytes;
+} ff_config;
+
+/* Bytes of device workspace ff_init needs for cfg (only the shape, dtype and
+ * whiten_split fields are read).  Errors: FF_ERR_INVALID_ARG. */
+ff_status ff_workspace_size(const ff_config* cfg, size_t* bytes);
+
+/* Validate cfg, lay out the workspace and enqueue the set-up on cfg->stream:
+ * the starting factor (A0/B0 or identity) and the internal copies of G
+ * (a transposed copy used by the A update; a zero-padded copy when m or n is
+ * not a multiple of the tile size).  Does not wait for the stream.
+ * Errors: FF_ERR_INVALID_ARG, FF_ERR_WORKSPACE, FF_ERR_HIP. */
+ff_status ff_init(const ff_config* cfg, ff_handle* out);
+
+/* Run up to `iters` (>= 0) flip-flop iterations (Section 5) continuing from
+ * the handle's current factors, then synchronise the stream.
+ * *iters_done receives the number of iterations completed by this call.
+ * loglik (host array of `iters` doubles, may be NULL) receives, per completed
+ * iteration, the matrix-normal log-likelihood of the samples under the new
+ * A (x) B, evaluated as -(N/2)(m log|A| + n log|B|) - (N m n/2)(1 + log 2 pi),
+ * which is exact when damping == 0 (the trace term equals N m n after a
+ * maximum-likelihood half step, Section 5 trace identity).
+ * FF_ERR_NOT_SPD: a factor to be inverted was not positive definite (the
+ * paper assumes invertibility, Section 2; use damping > 0).  The handle then
+ * keeps the factors of the last completed iteration and stays usable.  An
+ * iteration whose new factor is singular still completes (its log-likelihood
+ * entry is NaN); the next iteration, which must invert it, fails.
+ * Errors: FF_ERR_INVALID_ARG, FF_ERR_NOT_SPD, FF_ERR_HIP. */
+ff_status ff_iterate(ff_handle h, int iters, int* iters_done, double* loglik);
+
+/* Copy the current factors: A (n x n) and B (m x m), fp32 row-major,
+ * normalised to tr(A) = n.  on_host = 0: A and B are device pointers and the
+ * copy is enqueued on the stream; on_host = 1: host pointers, the call waits.
+ * Either pointer may be NULL to skip that factor.
+ * Errors: FF_ERR_INVALID_ARG, FF_ERR_HIP. */
+ff_status ff_factors(ff_handle h, float* A, float* B, int on_host);
+
+/* Apply the current Kronecker factors to `batch` matrices X_b (m x n):
+ * FF_APPLY: Y_b = B X_b A  (= (A (x) B) vec(X_b), column-major vec);
+ * FF_APPLY_INV: Y_b = B^-1 X_b A^-1.  X and Y are DEVICE fp32 [batch][m][n],
+ * 16-byte aligned and must not overlap.  Computed in fp32.
+ * Errors: FF_ERR_INVALID_ARG, FF_ERR_NOT_SPD (INV with a singular factor),
+ * FF_ERR_HIP. */
+ff_status ff_kron_apply(ff_handle h, const float* X, float* Y, int64_t batch,
+                        ff_apply_mode mode);
+
+/* Release the handle (host memory only; waits for the handle's stream).
+ * NULL is accepted. */
+ff_status ff_destroy(ff_handle h);
+
+/* Measurement hook (not needed for estimation).  With timing enabled,
+ * ff_iterate brackets each launch of the main kernels with HIP events on the
+ * handle's stream and accumulates their durations and algorithmic flop
+ * counts; enabling resets the counters.  Kernel ids: 0 = whitening
+ * (N m n^2 or N m^2 n flop per launch), 1 = symmetric product over the
+ * stacked samples (N n m^2 or N m n^2), 2 = reduction of its partial sums
+ * (0 flop), 3 = Cholesky + inverse of one factor (dim^3 / 3 flop).
+ * Errors: FF_ERR_INVALID_ARG, FF_ERR_HIP. */
+ff_status ff_set_timing(ff_handle h, int enable);
+ff_status ff_kernel_timing(ff_handle h, int kernel, int64_t* launches, double* total_ms,
+                           double* alg_flop);
+
+/* Static description of a status code. */
+const char* ff_status_string(ff_status s);
+
+/* Message of the most recent failing call on this thread ("" if none). */
+const char* ff_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FF_H */

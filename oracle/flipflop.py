@@ -108,6 +108,27 @@ def half_step_A(G, B, *, iteration=0):
     return 0.5 * (A + A.T)
 
 
+def half_step_B_rows(G, A, rows):
+    """Rows ``rows`` of the B update (1/(N n)) sum_i G_i A^-1 G_i^T.
+
+    For large layers: the samples are converted to fp64 one at a time
+    (uint16 = bf16 bit patterns), so only one sample is held in fp64.
+    """
+    G = np.asarray(G)
+    N, m, n = G.shape
+    rows = np.asarray(rows)
+    identity = A is None
+    cA = None if identity else _chol(np.asarray(A, np.float64), "A", 0)
+    out = np.zeros((len(rows), m))
+    for i in range(N):
+        Gi = as_f64_samples(G[i:i + 1])[0]
+        R = Gi[rows]                                    # (r, n)
+        if not identity:
+            R = sla.cho_solve(cA, R.T, check_finite=False).T
+        out += R @ Gi.T
+    return out / (N * n)
+
+
 def damp(X, kappa):
     """X + kappa * (tr X / dim) I  (Appendix B: damping by the mean diagonal)."""
     if kappa == 0.0:

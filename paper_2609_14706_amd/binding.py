@@ -1,0 +1,268 @@
+"""ctypes binding of libff.so (include/ff.h): argument marshalling only.
+
+Every step of the estimate runs in the HIP library; torch supplies device
+memory (the samples, the workspace, outputs) and the stream.  If the library
+is not built this module raises at first use: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libff.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "ff.h")
+
+FF_OK, FF_ERR_INVALID_ARG, FF_ERR_NOT_SPD, FF_ERR_WORKSPACE, FF_ERR_HIP, FF_ERR_STATE = range(6)
+FF_F32, FF_BF16 = 0, 1
+FF_ORDER_B_FIRST, FF_ORDER_A_FIRST = 0, 1
+FF_APPLY, FF_APPLY_INV = 0, 1
+KERNEL_IDS = {"whiten": 0, "syrk": 1, "reduce": 2, "cholinv": 3}
+
+
+class ff_config(ctypes.Structure):
+    _fields_ = [
+        ("m", ctypes.c_int64),
+        ("n", ctypes.c_int64),
+        ("N", ctypes.c_int64),
+        ("dtype", ctypes.c_int),
+        ("G", ctypes.c_void_p),
+        ("stream", ctypes.c_void_p),
+        ("order", ctypes.c_int),
+        ("damping", ctypes.c_double),
+        ("A0", ctypes.c_void_p),
+        ("B0", ctypes.c_void_p),
+        ("whiten_split", ctypes.c_int),
+        ("workspace", ctypes.c_void_p),
+        ("workspace_bytes", ctypes.c_size_t),
+    ]
+
+
+_LIB = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libff.so once and declare the signatures of ff.h."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2609_14706_amd.build`"
+                           " (the FlipFlop engine has no fallback path)")
+    lib = ctypes.CDLL(path)
+    H = ctypes.c_void_p
+    st = ctypes.c_int
+    sig = {
+        "ff_workspace_size": (st, [ctypes.POINTER(ff_config), ctypes.POINTER(ctypes.c_size_t)]),
+        "ff_init": (st, [ctypes.POINTER(ff_config), ctypes.POINTER(H)]),
+        "ff_iterate": (st, [H, ctypes.c_int, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_double)]),
+        "ff_factors": (st, [H, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int]),
+        "ff_kron_apply": (st, [H, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int]),
+        "ff_destroy": (st, [H]),
+        "ff_set_timing": (st, [H, ctypes.c_int]),
+        "ff_kernel_timing": (st, [H, ctypes.c_int, ctypes.POINTER(ctypes.c_int64),
+                                  ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
+        "ff_status_string": (ctypes.c_char_p, [st]),
+        "ff_last_error": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    _LIB = lib
+    return lib
+
+
+def header_functions(path: str = HEADER) -> list[str]:
+    """Names of the functions ff.h declares."""
+    text = open(path).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ff_\w+)\s*\(", text)))
+
+
+class FlipFlopError(RuntimeError):
+    def __init__(self, code: int, msg: str, iters_done: int = 0):
+        super().__init__(f"{ff_status_string(code)}: {msg}")
+        self.code = code
+        self.iters_done = iters_done
+
+
+def ff_status_string(code: int) -> str:
+    return load_library().ff_status_string(code).decode()
+
+
+def ff_last_error() -> str:
+    return load_library().ff_last_error().decode()
+
+
+def _check(code: int, iters_done: int = 0):
+    if code != FF_OK:
+        raise FlipFlopError(code, ff_last_error(), iters_done)
+
+
+# ------------------------------------------------------------ thin wrappers
+def ff_workspace_size(cfg: ff_config) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load_library().ff_workspace_size(ctypes.byref(cfg), ctypes.byref(out)))
+    return out.value
+
+
+def ff_init(cfg: ff_config) -> ctypes.c_void_p:
+    h = ctypes.c_void_p()
+    _check(load_library().ff_init(ctypes.byref(cfg), ctypes.byref(h)))
+    return h
+
+
+def ff_iterate(h, iters: int, want_loglik: bool = True):
+    done = ctypes.c_int(0)
+    ll = (ctypes.c_double * max(iters, 1))() if want_loglik else None
+    code = load_library().ff_iterate(h, iters, ctypes.byref(done), ll)
+    lls = list(ll[:done.value]) if ll is not None else []
+    if code != FF_OK:
+        err = FlipFlopError(code, ff_last_error(), done.value)
+        err.loglik = lls
+        raise err
+    return done.value, lls
+
+
+def ff_factors(h, A_ptr: int, B_ptr: int, on_host: int):
+    _check(load_library().ff_factors(h, A_ptr, B_ptr, on_host))
+
+
+def ff_kron_apply(h, X_ptr: int, Y_ptr: int, batch: int, mode: int):
+    _check(load_library().ff_kron_apply(h, X_ptr, Y_ptr, batch, mode))
+
+
+def ff_destroy(h):
+    _check(load_library().ff_destroy(h))
+
+
+def ff_set_timing(h, enable: bool):
+    _check(load_library().ff_set_timing(h, 1 if enable else 0))
+
+
+def ff_kernel_timing(h, kernel: int):
+    n = ctypes.c_int64(0)
+    ms = ctypes.c_double(0)
+    fl = ctypes.c_double(0)
+    _check(load_library().ff_kernel_timing(h, kernel, ctypes.byref(n), ctypes.byref(ms), ctypes.byref(fl)))
+    return n.value, ms.value, fl.value
+
+
+# --------------------------------------------------------------- torch API
+class FlipFlop:
+    """FlipFlop Hessian estimate A (x) B of samples G (N, m, n) on the GPU.
+
+    G: contiguous CUDA tensor, float32 or bfloat16.  The handle borrows G
+    and keeps it alive; the workspace is a torch uint8 tensor on G's device.
+    """
+
+    def __init__(self, G, *, order: str = "B_FIRST", damping: float = 0.0, A0=None, B0=None,
+                 whiten_split: int = 1, stream=None, workspace=None):
+        import torch
+        if not isinstance(G, torch.Tensor) or not G.is_cuda:
+            raise TypeError("G must be a CUDA tensor")
+        if G.dim() != 3 or not G.is_contiguous():
+            raise ValueError("G must be a contiguous (N, m, n) tensor")
+        if G.dtype == torch.bfloat16:
+            dt = FF_BF16
+        elif G.dtype == torch.float32:
+            dt = FF_F32
+        else:
+            raise TypeError("G must be float32 or bfloat16")
+        N, m, n = G.shape
+        self.device = G.device
+        self.stream = stream if stream is not None else torch.cuda.current_stream(G.device)
+        self.m, self.n, self.N = int(m), int(n), int(N)
+        self._keep = [G]
+        cfg = ff_config()
+        cfg.m, cfg.n, cfg.N = self.m, self.n, self.N
+        cfg.dtype = dt
+        cfg.G = G.data_ptr()
+        cfg.stream = self.stream.cuda_stream
+        cfg.order = {"B_FIRST": FF_ORDER_B_FIRST, "A_FIRST": FF_ORDER_A_FIRST}[order]
+        cfg.damping = float(damping)
+        for name, T, dim in (("A0", A0, self.n), ("B0", B0, self.m)):
+            if T is not None:
+                T = T.to(device=G.device, dtype=torch.float32).contiguous()
+                if T.shape != (dim, dim):
+                    raise ValueError(f"{name} must be {dim} x {dim}")
+                self._keep.append(T)
+                setattr(cfg, name, T.data_ptr())
+        cfg.whiten_split = int(whiten_split)
+        nbytes = ff_workspace_size(cfg)
+        if workspace is not None:
+            if (workspace.device != G.device or workspace.dtype != torch.uint8
+                    or workspace.numel() < nbytes + 256):
+                raise ValueError(f"workspace must be a uint8 tensor of >= {nbytes + 256} bytes on {G.device}")
+            self.workspace = workspace
+        else:
+            with torch.cuda.device(G.device):
+                self.workspace = torch.empty(nbytes + 256, dtype=torch.uint8, device=G.device)
+        base = self.workspace.data_ptr()
+        cfg.workspace = (base + 255) // 256 * 256
+        cfg.workspace_bytes = nbytes
+        self.cfg = cfg
+        self.h = ff_init(cfg)
+        self.iters_done = 0
+
+    @staticmethod
+    def workspace_bytes(m: int, n: int, N: int, dtype: str = "bf16", whiten_split: int = 1) -> int:
+        """Bytes a caller-provided workspace tensor needs (alignment slack included)."""
+        cfg = ff_config()
+        cfg.m, cfg.n, cfg.N = m, n, N
+        cfg.dtype = FF_BF16 if dtype == "bf16" else FF_F32
+        cfg.whiten_split = whiten_split
+        return ff_workspace_size(cfg) + 256
+
+    def iterate(self, iters: int):
+        """Run `iters` iterations; returns the per-iteration log-likelihoods."""
+        try:
+            done, ll = ff_iterate(self.h, int(iters))
+        except FlipFlopError as e:
+            self.iters_done += e.iters_done
+            raise
+        self.iters_done += done
+        return ll
+
+    def factors(self):
+        """(A, B) as new fp32 CUDA tensors, tr(A) = n."""
+        import torch
+        A = torch.empty((self.n, self.n), dtype=torch.float32, device=self.device)
+        B = torch.empty((self.m, self.m), dtype=torch.float32, device=self.device)
+        ff_factors(self.h, A.data_ptr(), B.data_ptr(), 0)
+        self.stream.synchronize()
+        return A, B
+
+    def kron_apply(self, X, inverse: bool = False):
+        """Y_b = B X_b A (or B^-1 X_b A^-1) for X of shape (batch, m, n)."""
+        import torch
+        X = X.to(device=self.device, dtype=torch.float32).contiguous()
+        squeeze = X.dim() == 2
+        if squeeze:
+            X = X[None]
+        if tuple(X.shape[1:]) != (self.m, self.n):
+            raise ValueError("X must be (batch, m, n)")
+        Y = torch.empty_like(X)
+        ff_kron_apply(self.h, X.data_ptr(), Y.data_ptr(), X.shape[0],
+                      FF_APPLY_INV if inverse else FF_APPLY)
+        return Y[0] if squeeze else Y
+
+    def set_timing(self, enable: bool = True):
+        ff_set_timing(self.h, enable)
+
+    def kernel_timing(self, kernel: str):
+        """(launches, total ms, algorithmic flop) recorded since timing was enabled."""
+        return ff_kernel_timing(self.h, KERNEL_IDS[kernel])
+
+    def close(self):
+        if getattr(self, "h", None):
+            ff_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

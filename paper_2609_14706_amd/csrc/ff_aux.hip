@@ -1,0 +1,237 @@
+// Bandwidth-bound helper kernels of the flip-flop iteration: sample packing
+// (zero-padded copy / transpose), inverse conversion for the whitening
+// operand, trace + damping, the trace normalisation, the per-iteration
+// log-likelihood, and plain fills and copies.
+#include <math.h>
+
+#include "ff_common.hpp"
+#include "ff_kernels.hpp"
+
+namespace ff {
+namespace {
+
+// ------------------------------------------------------------------ packing
+// out[s][r][c], r < rows_p, c < cols_p.  transpose = 0: G[s][r][c] when
+// r < m, c < n.  transpose = 1: G[s][c][r] when r < n, c < m.  64 x 64 tiles
+// through LDS so that both the read and the write are coalesced.
+template <typename T>
+__global__ __launch_bounds__(256) void k_pack(const T* __restrict__ G, T* __restrict__ out,
+                                              int64_t m, int64_t n, int64_t rows_p, int64_t cols_p,
+                                              int transpose) {
+  __shared__ T tile[64][65];
+  const int64_t s = blockIdx.z;
+  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+  const T* g = G + s * m * n;
+  T* o = out + s * rows_p * cols_p;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  if (!transpose) {
+    for (int y = ty; y < 64; y += 4) {
+      const int64_t r = r0 + y, c = c0 + tx;
+      if (r < rows_p && c < cols_p) o[r * cols_p + c] = (r < m && c < n) ? g[r * n + c] : T(0);
+    }
+    return;
+  }
+  // tile of the source: source rows c0.. (m side), source cols r0.. (n side)
+  for (int y = ty; y < 64; y += 4) {
+    const int64_t sr = c0 + y, sc = r0 + tx;
+    tile[y][tx] = (sr < m && sc < n) ? g[sr * n + sc] : T(0);
+  }
+  __syncthreads();
+  for (int y = ty; y < 64; y += 4) {
+    const int64_t r = r0 + y, c = c0 + tx;
+    if (r < rows_p && c < cols_p) o[r * cols_p + c] = tile[tx][y];
+  }
+}
+
+// --------------------------------------------------------- inverse convert
+template <typename T>
+__global__ __launch_bounds__(256) void k_convert_inverse(const float* __restrict__ Li, int64_t dim,
+                                                         T* __restrict__ Lw, T* __restrict__ Lw2,
+                                                         int64_t dim_p, const int* st) {
+  if (ff_halted(st)) return;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= dim_p * dim_p) return;
+  const int64_t i = idx / dim_p, j = idx % dim_p;
+  const float v = (i < dim && j <= i) ? Li[i * dim + j] : 0.0f;
+  const T hi = Elem<T>::from_f32(v);
+  Lw[idx] = hi;
+  if (Lw2 != nullptr) Lw2[idx] = Elem<T>::from_f32(v - Elem<T>::to_f32(hi));
+}
+
+// ---------------------------------------------------------- trace, damping
+__device__ double block_sum_256(double v, double* red) {
+  const int tid = threadIdx.x;
+  red[tid] = v;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (tid < w) red[tid] += red[tid + w];
+    __syncthreads();
+  }
+  const double r = red[0];
+  __syncthreads();
+  return r;
+}
+
+__global__ __launch_bounds__(256) void k_trace_damp(float* F, int64_t dim, double kappa,
+                                                    double* tr_out, const int* st) {
+  if (ff_halted(st)) return;
+  __shared__ double red[256];
+  double s = 0.0;
+  for (int64_t i = threadIdx.x; i < dim; i += 256) s += (double)F[i * dim + i];
+  double tr = block_sum_256(s, red);
+  if (kappa > 0.0) {
+    const float add = (float)(kappa * tr / (double)dim);
+    s = 0.0;
+    for (int64_t i = threadIdx.x; i < dim; i += 256) {
+      const float v = F[i * dim + i] + add;
+      F[i * dim + i] = v;
+      s += (double)v;
+    }
+    tr = block_sum_256(s, red);
+  }
+  if (threadIdx.x == 0) *tr_out = tr;
+}
+
+__global__ __launch_bounds__(256) void k_normalise(float* __restrict__ FA, int64_t nA,
+                                                   float* __restrict__ FB, int64_t nB,
+                                                   const double* trA, int64_t n, double* c_out,
+                                                   const int* st) {
+  if (ff_halted(st)) return;
+  const double c = *trA / (double)n;
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < nA; i += stride)
+    FA[i] = (float)((double)FA[i] / c);
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < nB; i += stride)
+    FB[i] = (float)((double)FB[i] * c);
+  if (blockIdx.x == 0 && threadIdx.x == 0) *c_out = c;
+}
+
+__global__ __launch_bounds__(256) void k_loglik(const double* slotsA, int nA, const double* slotsB,
+                                                int nB, const double* cptr, int first_is_B,
+                                                double m, double n, double N, double* ll_out,
+                                                const int* st) {
+  if (ff_halted(st)) return;
+  if (threadIdx.x != 0) return;
+  double la = 0.0, lb = 0.0;
+  for (int i = 0; i < nA; ++i) la += slotsA[i];
+  for (int i = 0; i < nB; ++i) lb += slotsB[i];
+  la *= 2.0;
+  lb *= 2.0;
+  const double logc = log(*cptr);
+  // The side updated first was factorised before the normalisation
+  // (B <- c B, or A <- A / c in the A-first order).
+  if (first_is_B) lb += m * logc;
+  else la -= n * logc;
+  const double log2pi = 1.8378770664093454835606594728112;
+  *ll_out = -0.5 * N * (m * la + n * lb) - 0.5 * N * m * n * (1.0 + log2pi);
+}
+
+__global__ __launch_bounds__(256) void k_copy_f32(const float* __restrict__ src,
+                                                  float* __restrict__ dst, int64_t count,
+                                                  const int* st) {
+  if (ff_halted(st)) return;
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count; i += stride) dst[i] = src[i];
+}
+
+__global__ __launch_bounds__(256) void k_fill_f32(float* dst, int64_t count, float v) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count; i += stride) dst[i] = v;
+}
+
+__global__ __launch_bounds__(256) void k_identity_f32(float* dst, int64_t dim) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < dim * dim; i += stride)
+    dst[i] = (i / dim == i % dim) ? 1.0f : 0.0f;
+}
+
+__global__ void k_set_int(int* dst, int64_t count, int v) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < count) dst[i] = v;
+}
+
+uint32_t grid_for(int64_t count) {
+  int64_t b = (count + 255) / 256;
+  if (b > 8192) b = 8192;
+  if (b < 1) b = 1;
+  return (uint32_t)b;
+}
+
+}  // namespace
+
+hipError_t launch_pack(const void* G, void* out, int64_t N, int64_t m, int64_t n, int64_t rows_p,
+                       int64_t cols_p, int transpose, int elem_bytes, hipStream_t s) {
+  if (N < 1 || N > 65535 || rows_p < 1 || cols_p < 1) return hipErrorInvalidValue;
+  if (transpose ? (rows_p < n || cols_p < m) : (rows_p < m || cols_p < n))
+    return hipErrorInvalidValue;
+  dim3 grid((uint32_t)((cols_p + 63) / 64), (uint32_t)((rows_p + 63) / 64), (uint32_t)N);
+  if (elem_bytes == 2)
+    hipLaunchKernelGGL(k_pack<bf16_t>, grid, dim3(256), 0, s, (const bf16_t*)G, (bf16_t*)out, m, n,
+                       rows_p, cols_p, transpose);
+  else if (elem_bytes == 4)
+    hipLaunchKernelGGL(k_pack<float>, grid, dim3(256), 0, s, (const float*)G, (float*)out, m, n,
+                       rows_p, cols_p, transpose);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_convert_inverse(const float* Li, int64_t dim, void* Lw, void* Lw2, int64_t dim_p,
+                                  int elem_bytes, const int* st, hipStream_t s) {
+  if (dim < 1 || dim_p < dim) return hipErrorInvalidValue;
+  const uint32_t blocks = (uint32_t)((dim_p * dim_p + 255) / 256);
+  if (elem_bytes == 2)
+    hipLaunchKernelGGL(k_convert_inverse<bf16_t>, dim3(blocks), dim3(256), 0, s, Li, dim,
+                       (bf16_t*)Lw, (bf16_t*)Lw2, dim_p, st);
+  else if (elem_bytes == 4)
+    hipLaunchKernelGGL(k_convert_inverse<float>, dim3(blocks), dim3(256), 0, s, Li, dim, (float*)Lw,
+                       (float*)Lw2, dim_p, st);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_trace_damp(float* F, int64_t dim, double kappa, double* tr, const int* st,
+                             hipStream_t s) {
+  hipLaunchKernelGGL(k_trace_damp, dim3(1), dim3(256), 0, s, F, dim, kappa, tr, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_normalise(float* FA, int64_t n, float* FB, int64_t m, const double* trA,
+                            double* c_out, const int* st, hipStream_t s) {
+  hipLaunchKernelGGL(k_normalise, dim3(grid_for(n * n > m * m ? n * n : m * m)), dim3(256), 0, s,
+                     FA, n * n, FB, m * m, trA, n, c_out, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_loglik(const double* slotsA, int nA, const double* slotsB, int nB,
+                         const double* c, int first_is_B, double m, double n, double N,
+                         double* ll_out, const int* st, hipStream_t s) {
+  hipLaunchKernelGGL(k_loglik, dim3(1), dim3(64), 0, s, slotsA, nA, slotsB, nB, c, first_is_B, m,
+                     n, N, ll_out, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_f32(const float* src, float* dst, int64_t count, const int* st,
+                           hipStream_t s) {
+  hipLaunchKernelGGL(k_copy_f32, dim3(grid_for(count)), dim3(256), 0, s, src, dst, count, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_f32(float* dst, int64_t count, float v, hipStream_t s) {
+  hipLaunchKernelGGL(k_fill_f32, dim3(grid_for(count)), dim3(256), 0, s, dst, count, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_identity_f32(float* dst, int64_t dim, hipStream_t s) {
+  hipLaunchKernelGGL(k_identity_f32, dim3(grid_for(dim * dim)), dim3(256), 0, s, dst, dim);
+  return hipGetLastError();
+}
+
+hipError_t launch_set_int(int* dst, int64_t count, int v, hipStream_t s) {
+  hipLaunchKernelGGL(k_set_int, dim3((uint32_t)((count + 255) / 256)), dim3(256), 0, s, dst, count,
+                     v);
+  return hipGetLastError();
+}
+
+}  // namespace ff

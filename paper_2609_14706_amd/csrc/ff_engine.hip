@@ -1,0 +1,669 @@
+// Host runtime of the FlipFlop engine: workspace layout, the stream-ordered
+// iteration pipeline and the C ABI declared in ff.h.
+//
+// One flip-flop iteration (Section 5; Appendix B order: B first, from A = I):
+//   whiten   W_i = G_i L_A^-T            (L_A^-1 from the previous step)
+//   symmetric product, reduce            B = (1/(N n)) sum_i W_i W_i^T   [+ damping]
+//   Cholesky + inverse of B              L_B^-1
+//   whiten   V_i = G_i^T L_B^-T          (on the transposed sample copy)
+//   symmetric product, reduce            A = (1/(N m)) sum_i V_i V_i^T   [+ damping]
+//   normalise                            c = tr(A)/n, A /= c, B *= c
+//   Cholesky + inverse of A              L_A^-1 for the next iteration, log|A|
+// All of it is enqueued on the caller's stream without host round trips; the
+// stream is synchronised once at the end of ff_iterate.
+#include <math.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <algorithm>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "ff.h"
+#include "ff_kernels.hpp"
+
+using namespace ff;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+ff_status fail(ff_status s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+#define FF_HIP(call)                                                                     \
+  do {                                                                                   \
+    hipError_t e_ = (call);                                                              \
+    if (e_ != hipSuccess)                                                                \
+      return fail(FF_ERR_HIP, std::string(#call) + ": " + hipGetErrorString(e_));        \
+  } while (0)
+
+constexpr size_t kAlign = 256;
+constexpr int kLLCap = 1024;      // log-likelihood values per device ring
+constexpr int kTimedKernels = 4;  // whiten, symmetric product, reduction, factorisation
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+int64_t round_up(int64_t x, int64_t g) { return (x + g - 1) / g * g; }
+
+struct Side {
+  int64_t dim = 0, dim_p = 0;
+  float* F[2] = {nullptr, nullptr};  // the factor, double buffered by iteration parity
+  float* L = nullptr;                // Cholesky work copy
+  float* Li = nullptr;               // L^-1 (fp32, lower)
+  void* Lw = nullptr;                // whitening operand (elem, dim_p x dim_p)
+  void* Lw2 = nullptr;               // its low bf16 part (whiten_split = 2)
+  double* slots = nullptr;           // per-leaf sum log L_jj
+  int nslots = 0;
+  double* tr = nullptr;              // trace after the last update
+  int splits = 1;                    // k-splits of the symmetric product producing this side
+  size_t partial_floats = 0;
+  bool lw_valid = false;             // Lw holds the inverse factor of F[cur]
+  int code = 0;                      // 1 = A, 2 = B
+};
+
+struct Layout {
+  int64_t m_p, n_p;
+  bool own_gx;
+  size_t off_small, off_ll, off_slotsA, off_slotsB, off_gx, off_gt, off_w, off_p;
+  size_t off_A[6], off_B[6];  // F0, F1, L, Li, Lw, Lw2
+  size_t total;
+  int splitsA, splitsB;
+  size_t partialA, partialB;
+};
+
+bool is_bf16(const ff_config* c) { return c->dtype == FF_BF16; }
+int elem_bytes(const ff_config* c) { return is_bf16(c) ? 2 : 4; }
+int granule(const ff_config* c) { return is_bf16(c) ? kTileBF16 : 64; }
+
+// Splits of the bf16 symmetric product: minimise (rounds of 256 workgroups) x
+// (k slices per workgroup) plus the cost of writing and re-reading partials.
+int choose_splits_bf16(int64_t dim_p, int64_t kslices) {
+  const int64_t T = dim_p / kTileBF16, tiles = T * (T + 1) / 2;
+  double best = 1e300;
+  int bestS = 1;
+  const int64_t maxS = std::min<int64_t>(128, kslices);
+  for (int64_t S = 1; S <= maxS; ++S) {
+    const double rounds = (double)((tiles * S + 255) / 256);
+    const double t = rounds * (double)((kslices + S - 1) / S) * 1.7e-6 +
+                     (double)(tiles * S) * 0.5e6 / 4.0e12;
+    if (t < best * (1.0 - 1e-9)) {
+      best = t;
+      bestS = (int)S;
+    }
+  }
+  return bestS;
+}
+
+int choose_splits_f32(int64_t dim_p, int64_t K) {
+  const int64_t T = (dim_p + 127) / 128, tiles = T * (T + 1) / 2;
+  int64_t S = std::max<int64_t>(1, 512 / tiles);
+  S = std::min<int64_t>(S, std::max<int64_t>(1, K / 256));
+  return (int)std::min<int64_t>(S, 256);
+}
+
+ff_status validate_shape(const ff_config* c) {
+  if (c == nullptr) return fail(FF_ERR_INVALID_ARG, "config is NULL");
+  if (c->m < 1 || c->n < 1 || c->N < 1)
+    return fail(FF_ERR_INVALID_ARG, "m, n and N must be >= 1");
+  if (c->dtype != FF_F32 && c->dtype != FF_BF16) return fail(FF_ERR_INVALID_ARG, "unknown dtype");
+  if (c->N > 65535) return fail(FF_ERR_INVALID_ARG, "N must be <= 65535");
+  if (c->m > (1 << 20) || c->n > (1 << 20))
+    return fail(FF_ERR_INVALID_ARG, "m and n must be <= 1048576");
+  if (is_bf16(c) && c->whiten_split != 1 && c->whiten_split != 2)
+    return fail(FF_ERR_INVALID_ARG, "whiten_split must be 1 or 2");
+  return FF_OK;
+}
+
+Layout make_layout(const ff_config* c) {
+  Layout L{};
+  const int g = granule(c), e = elem_bytes(c);
+  const int64_t m = c->m, n = c->n, N = c->N;
+  L.m_p = round_up(m, g);
+  L.n_p = round_up(n, g);
+  L.own_gx = !(L.m_p == m && L.n_p == n);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  L.off_small = take(kAlign);  // status[4] @0, c @64, trA @128, trB @192
+  L.off_ll = take(sizeof(double) * kLLCap);
+  L.off_slotsA = take(sizeof(double) * ((n + kLeaf - 1) / kLeaf));
+  L.off_slotsB = take(sizeof(double) * ((m + kLeaf - 1) / kLeaf));
+  const size_t gbytes = (size_t)N * L.m_p * L.n_p * e;
+  L.off_gx = L.own_gx ? take(gbytes) : 0;
+  L.off_gt = take(gbytes);
+  L.off_w = take(std::max(gbytes, (size_t)m * n * sizeof(float)));
+  if (is_bf16(c)) {
+    L.splitsB = choose_splits_bf16(L.m_p, N * L.n_p / 64);
+    L.splitsA = choose_splits_bf16(L.n_p, N * L.m_p / 64);
+    const int64_t TB = L.m_p / kTileBF16, TA = L.n_p / kTileBF16;
+    L.partialB = (size_t)L.splitsB * (TB * (TB + 1) / 2) * kTileBF16 * kTileBF16;
+    L.partialA = (size_t)L.splitsA * (TA * (TA + 1) / 2) * kTileBF16 * kTileBF16;
+  } else {
+    L.splitsB = choose_splits_f32(L.m_p, N * L.n_p);
+    L.splitsA = choose_splits_f32(L.n_p, N * L.m_p);
+    L.partialB = (size_t)L.splitsB * L.m_p * L.m_p;
+    L.partialA = (size_t)L.splitsA * L.n_p * L.n_p;
+  }
+  L.off_p = take(sizeof(float) * std::max(L.partialA, L.partialB));
+  const bool split2 = is_bf16(c) && c->whiten_split == 2;
+  auto side = [&](size_t* o, int64_t dim, int64_t dim_p) {
+    const size_t fb = (size_t)dim * dim * sizeof(float);
+    o[0] = take(fb);
+    o[1] = take(fb);
+    o[2] = take(fb);
+    o[3] = take(fb);
+    o[4] = take((size_t)dim_p * dim_p * e);
+    o[5] = split2 ? take((size_t)dim_p * dim_p * 2) : 0;
+  };
+  side(L.off_A, n, L.n_p);
+  side(L.off_B, m, L.m_p);
+  L.total = off;
+  return L;
+}
+
+}  // namespace
+
+struct ff_handle_s {
+  ff_config cfg{};
+  hipStream_t stream = nullptr;
+  int device = 0;
+  int64_t m = 0, n = 0, N = 0;
+  bool bf16 = false;
+  int elem = 4;
+  Layout lay{};
+  const void* Gx = nullptr;
+  void* Gt = nullptr;
+  void* W = nullptr;
+  float* P = nullptr;
+  Side A, B;
+  int* st = nullptr;
+  double* c = nullptr;
+  double* ll = nullptr;
+  int64_t iters_total = 0;
+  int cur = 0;
+  // measurement hook
+  bool timing = false;
+  std::vector<hipEvent_t> events;
+  size_t ev_used = 0;
+  struct Pending { int kernel; size_t ev; double flop; };
+  std::vector<Pending> pending;
+  int64_t t_launches[kTimedKernels] = {0, 0, 0, 0};
+  double t_ms[kTimedKernels] = {0, 0, 0, 0};
+  double t_flop[kTimedKernels] = {0, 0, 0, 0};
+};
+
+namespace {
+
+// ------------------------------------------------------------------ timing
+struct Timed {
+  ff_handle_s* h;
+  int kernel;
+  double flop;
+  size_t ev = SIZE_MAX;
+  Timed(ff_handle_s* hh, int k, double f) : h(hh), kernel(k), flop(f) {
+    if (h->timing && h->ev_used + 2 <= h->events.size()) {
+      ev = h->ev_used;
+      h->ev_used += 2;
+      hipEventRecord(h->events[ev], h->stream);
+    }
+  }
+  ~Timed() {
+    if (ev != SIZE_MAX) {
+      hipEventRecord(h->events[ev + 1], h->stream);
+      h->pending.push_back({kernel, ev, flop});
+    }
+  }
+};
+
+void collect_timing(ff_handle_s* h) {
+  for (const auto& p : h->pending) {
+    float ms = 0.0f;
+    if (hipEventElapsedTime(&ms, h->events[p.ev], h->events[p.ev + 1]) == hipSuccess) {
+      h->t_launches[p.kernel] += 1;
+      h->t_ms[p.kernel] += ms;
+      h->t_flop[p.kernel] += p.flop;
+    }
+  }
+  h->pending.clear();
+  h->ev_used = 0;
+}
+
+// ------------------------------------------------------- factorisation
+ff_status cholinv_rec(ff_handle_s* h, Side& s, int64_t o, int64_t sz, int iteration) {
+  const int64_t d = s.dim;
+  if (sz <= kLeaf) {
+    FF_HIP(launch_chol_leaf(s.L + o * d + o, s.Li + o * d + o, d, (int)sz, o, s.slots,
+                            (int)(o / kLeaf), iteration, s.code, h->st, h->stream));
+    return FF_OK;
+  }
+  const int64_t nl = (sz + kLeaf - 1) / kLeaf;
+  const int64_t hh = (nl + 1) / 2 * kLeaf, r = sz - hh;
+  ff_status rc = cholinv_rec(h, s, o, hh, iteration);
+  if (rc != FF_OK) return rc;
+  float* L21 = s.L + (o + hh) * d + o;
+  float* L22 = s.L + (o + hh) * d + (o + hh);
+  float* Li11 = s.Li + o * d + o;
+  float* Li21 = s.Li + (o + hh) * d + o;
+  float* Li22 = s.Li + (o + hh) * d + (o + hh);
+  GemmF32 g{};
+  g.lda = g.ldb = g.ldc = d;
+  g.kseg = INT64_MAX / 4;
+  g.ksplit = 1;
+  g.st = h->st;
+  // Li21 <- A21 Li11^T  (the panel of L, parked in the Li21 block)
+  g.A = L21; g.B = Li11; g.C = Li21; g.M = r; g.N = hh; g.K = hh;
+  g.transA = 0; g.transB = 1; g.alpha = 1.f; g.beta = 0.f; g.flags = kKHiCol;
+  FF_HIP(launch_gemm_f32(g, 1, h->stream));
+  // A22 <- A22 - L21 L21^T  (lower triangle)
+  g.A = Li21; g.B = Li21; g.C = L22; g.M = r; g.N = r; g.K = hh;
+  g.transA = 0; g.transB = 1; g.alpha = -1.f; g.beta = 1.f; g.flags = kCLower;
+  FF_HIP(launch_gemm_f32(g, 1, h->stream));
+  rc = cholinv_rec(h, s, o + hh, r, iteration);
+  if (rc != FF_OK) return rc;
+  // X <- L21 Li11  (into the A21 block, no longer needed)
+  g.A = Li21; g.B = Li11; g.C = L21; g.M = r; g.N = hh; g.K = hh;
+  g.transA = 0; g.transB = 0; g.alpha = 1.f; g.beta = 0.f; g.flags = kKLoCol;
+  FF_HIP(launch_gemm_f32(g, 1, h->stream));
+  // Li21 <- -Li22 X
+  g.A = Li22; g.B = L21; g.C = Li21; g.M = r; g.N = hh; g.K = r;
+  g.transA = 0; g.transB = 0; g.alpha = -1.f; g.beta = 0.f; g.flags = kKHiRow;
+  FF_HIP(launch_gemm_f32(g, 1, h->stream));
+  return FF_OK;
+}
+
+// L^-1 of s.F[slot] into s.Li and the whitening operand s.Lw.
+ff_status cholinv(ff_handle_s* h, Side& s, int slot, int iteration) {
+  Timed t(h, 3, (double)s.dim * s.dim * s.dim / 3.0);
+  FF_HIP(launch_copy_f32(s.F[slot], s.L, s.dim * s.dim, h->st, h->stream));
+  ff_status rc = cholinv_rec(h, s, 0, s.dim, iteration);
+  if (rc != FF_OK) return rc;
+  FF_HIP(launch_convert_inverse(s.Li, s.dim, s.Lw, s.Lw2, s.dim_p, h->elem, h->st, h->stream));
+  return FF_OK;
+}
+
+// s.F[slot] = (1/(N p.dim)) sum_i X_i Li_p^T Li_p X_i^T  (+ damping), trace into s.tr.
+ff_status update(ff_handle_s* h, Side& s, Side& p, int slot) {
+  const void* X = (&s == &h->B) ? h->Gx : h->Gt;
+  const int64_t N = h->N, rows = N * s.dim_p, Kp = p.dim_p;
+  const double scale = 1.0 / ((double)N * (double)p.dim);
+  const double wflop = (double)N * s.dim * p.dim * p.dim;
+  const double sflop = (double)N * p.dim * s.dim * s.dim;
+  if (h->bf16) {
+    {
+      Timed t(h, 0, wflop);
+      FF_HIP(launch_whiten_bf16((const bf16_t*)X, (const bf16_t*)p.Lw, (const bf16_t*)p.Lw2,
+                                (bf16_t*)h->W, rows, Kp, h->st, h->stream));
+    }
+    {
+      Timed t(h, 1, sflop);
+      FF_HIP(launch_syrk_bf16((const bf16_t*)h->W, s.dim_p, Kp, s.dim_p * Kp, N, s.splits, h->P,
+                              h->st, h->stream));
+    }
+    {
+      Timed t(h, 2, 0.0);
+      FF_HIP(launch_reduce_frag(h->P, s.splits, s.dim_p, s.F[slot], s.dim, scale, h->st,
+                                h->stream));
+    }
+  } else {
+    GemmF32 g{};
+    g.st = h->st;
+    g.ksplit = 1;
+    {
+      Timed t(h, 0, wflop);
+      g.A = (const float*)X; g.lda = Kp; g.transA = 0;
+      g.B = (const float*)p.Lw; g.ldb = Kp; g.transB = 1;
+      g.C = (float*)h->W; g.ldc = Kp;
+      g.M = rows; g.N = Kp; g.K = Kp; g.kseg = Kp;
+      g.alpha = 1.f; g.beta = 0.f; g.flags = kKHiCol;
+      FF_HIP(launch_gemm_f32(g, 1, h->stream));
+    }
+    {
+      Timed t(h, 1, sflop);
+      GemmF32 q{};
+      q.st = h->st;
+      q.A = (const float*)h->W; q.lda = Kp; q.transA = 0;
+      q.B = (const float*)h->W; q.ldb = Kp; q.transB = 1;
+      q.C = h->P; q.ldc = s.dim_p; q.sC = s.dim_p * s.dim_p;
+      q.M = s.dim_p; q.N = s.dim_p; q.K = N * Kp;
+      q.kseg = Kp; q.segA = q.segB = s.dim_p * Kp;
+      q.alpha = 1.f; q.beta = 0.f; q.flags = kCLower; q.ksplit = s.splits;
+      FF_HIP(launch_gemm_f32(q, 1, h->stream));
+    }
+    {
+      Timed t(h, 2, 0.0);
+      FF_HIP(launch_reduce_rowmajor(h->P, s.splits, s.dim_p, s.F[slot], s.dim, scale, h->st,
+                                    h->stream));
+    }
+  }
+  FF_HIP(launch_trace_damp(s.F[slot], s.dim, h->cfg.damping, s.tr, h->st, h->stream));
+  return FF_OK;
+}
+
+ff_status read_status(ff_handle_s* h, int st[4]) {
+  FF_HIP(hipMemcpyAsync(st, h->st, 4 * sizeof(int), hipMemcpyDeviceToHost, h->stream));
+  FF_HIP(hipStreamSynchronize(h->stream));
+  return FF_OK;
+}
+
+ff_status clear_status(ff_handle_s* h) {
+  FF_HIP(launch_set_int(h->st, 4, 0, h->stream));
+  return FF_OK;
+}
+
+// Up to kLLCap iterations; synchronises once.
+//
+// The factorisation of the second-updated factor that closes iteration g is
+// the one iteration g + 1 needs, so its failure is attributed to g + 1:
+// iteration g is complete (the oracle also returns such a singular factor),
+// and only a later iteration that would invert it fails.
+ff_status iterate_chunk(ff_handle_s* h, int iters, int* done, double* loglik) {
+  *done = 0;
+  const bool bfirst = h->cfg.order == FF_ORDER_B_FIRST;
+  Side& first = bfirst ? h->B : h->A;
+  Side& second = bfirst ? h->A : h->B;
+  const int64_t base = h->iters_total;
+  ff_status rc;
+  if (!second.lw_valid) {
+    rc = cholinv(h, second, h->cur, (int)(base + 1));
+    if (rc != FF_OK) return rc;
+  }
+  for (int k = 1; k <= iters; ++k) {
+    const int64_t g = base + k;
+    const int slot = (int)(g & 1);
+    if ((rc = update(h, first, second, slot)) != FF_OK) return rc;
+    if ((rc = cholinv(h, first, slot, (int)g)) != FF_OK) return rc;
+    if ((rc = update(h, second, first, slot)) != FF_OK) return rc;
+    FF_HIP(launch_normalise(h->A.F[slot], h->n, h->B.F[slot], h->m, h->A.tr, h->c, h->st,
+                            h->stream));
+    if ((rc = cholinv(h, second, slot, (int)(g + 1))) != FF_OK) return rc;
+    FF_HIP(launch_loglik(h->A.slots, h->A.nslots, h->B.slots, h->B.nslots, h->c, bfirst ? 1 : 0,
+                         (double)h->m, (double)h->n, (double)h->N, h->ll + (k - 1), h->st,
+                         h->stream));
+  }
+  int st[4];
+  if ((rc = read_status(h, st)) != FF_OK) return rc;
+  if (h->timing) collect_timing(h);
+  int completed = iters;
+  if (st[0] != 0) completed = (int)std::max<int64_t>(0, std::min<int64_t>(iters, st[0] - 1 - base));
+  if (loglik != nullptr && completed > 0) {
+    FF_HIP(hipMemcpy(loglik, h->ll, sizeof(double) * completed, hipMemcpyDeviceToHost));
+    if (st[0] != 0) loglik[completed - 1] = NAN;  // its closing factorisation failed
+  }
+  h->iters_total = base + completed;
+  h->cur = (int)(h->iters_total & 1);
+  *done = completed;
+  if (st[0] != 0) {
+    second.lw_valid = false;
+    first.lw_valid = false;
+    if ((rc = clear_status(h)) != FF_OK) return rc;
+    FF_HIP(hipStreamSynchronize(h->stream));
+    if (st[0] == base + iters + 1) return FF_OK;  // only the look-ahead failed
+    char msg[160];
+    snprintf(msg, sizeof msg, "factor %s not positive definite at iteration %d (pivot %d)",
+             st[1] == 1 ? "A" : "B", st[0], st[2]);
+    return fail(FF_ERR_NOT_SPD, msg);
+  }
+  second.lw_valid = true;
+  return FF_OK;
+}
+
+}  // namespace
+
+// ====================================================================== ABI
+extern "C" {
+
+const char* ff_status_string(ff_status s) {
+  switch (s) {
+    case FF_OK: return "ok";
+    case FF_ERR_INVALID_ARG: return "invalid argument";
+    case FF_ERR_NOT_SPD: return "factor not positive definite";
+    case FF_ERR_WORKSPACE: return "workspace missing, too small or misaligned";
+    case FF_ERR_HIP: return "HIP runtime error";
+    case FF_ERR_STATE: return "invalid handle state";
+  }
+  return "unknown status";
+}
+
+const char* ff_last_error(void) { return g_last_error.c_str(); }
+
+ff_status ff_workspace_size(const ff_config* cfg, size_t* bytes) {
+  ff_status rc = validate_shape(cfg);
+  if (rc != FF_OK) return rc;
+  if (bytes == nullptr) return fail(FF_ERR_INVALID_ARG, "bytes is NULL");
+  *bytes = make_layout(cfg).total;
+  return FF_OK;
+}
+
+ff_status ff_init(const ff_config* cfg, ff_handle* out) {
+  ff_status rc = validate_shape(cfg);
+  if (rc != FF_OK) return rc;
+  if (out == nullptr) return fail(FF_ERR_INVALID_ARG, "out is NULL");
+  if (cfg->G == nullptr || ((uintptr_t)cfg->G % 16) != 0)
+    return fail(FF_ERR_INVALID_ARG, "G must be a non-NULL 16-byte aligned device pointer");
+  if (cfg->order != FF_ORDER_B_FIRST && cfg->order != FF_ORDER_A_FIRST)
+    return fail(FF_ERR_INVALID_ARG, "unknown order");
+  if (!(cfg->damping >= 0.0) || !isfinite(cfg->damping))
+    return fail(FF_ERR_INVALID_ARG, "damping must be finite and >= 0");
+  if (((uintptr_t)cfg->A0 % 16) != 0 || ((uintptr_t)cfg->B0 % 16) != 0)
+    return fail(FF_ERR_INVALID_ARG, "A0/B0 must be 16-byte aligned");
+  const Layout lay = make_layout(cfg);
+  if (cfg->workspace == nullptr || ((uintptr_t)cfg->workspace % kAlign) != 0)
+    return fail(FF_ERR_WORKSPACE, "workspace must be a non-NULL 256-byte aligned device pointer");
+  if (cfg->workspace_bytes < lay.total) {
+    char msg[128];
+    snprintf(msg, sizeof msg, "workspace too small: %zu < %zu bytes", cfg->workspace_bytes,
+             lay.total);
+    return fail(FF_ERR_WORKSPACE, msg);
+  }
+  ff_handle_s* h = new (std::nothrow) ff_handle_s();
+  if (h == nullptr) return fail(FF_ERR_INVALID_ARG, "host allocation of the handle failed");
+  h->cfg = *cfg;
+  if (!is_bf16(cfg)) h->cfg.whiten_split = 1;
+  h->stream = (hipStream_t)cfg->stream;
+  h->m = cfg->m;
+  h->n = cfg->n;
+  h->N = cfg->N;
+  h->bf16 = is_bf16(cfg);
+  h->elem = elem_bytes(cfg);
+  h->lay = lay;
+  if (hipGetDevice(&h->device) != hipSuccess) {
+    delete h;
+    return fail(FF_ERR_HIP, "hipGetDevice failed");
+  }
+  char* ws = (char*)cfg->workspace;
+  h->st = (int*)(ws + lay.off_small);
+  h->c = (double*)(ws + lay.off_small + 64);
+  h->A.tr = (double*)(ws + lay.off_small + 128);
+  h->B.tr = (double*)(ws + lay.off_small + 192);
+  h->ll = (double*)(ws + lay.off_ll);
+  h->A.slots = (double*)(ws + lay.off_slotsA);
+  h->B.slots = (double*)(ws + lay.off_slotsB);
+  h->A.nslots = (int)((h->n + kLeaf - 1) / kLeaf);
+  h->B.nslots = (int)((h->m + kLeaf - 1) / kLeaf);
+  h->Gx = lay.own_gx ? (const void*)(ws + lay.off_gx) : cfg->G;
+  h->Gt = ws + lay.off_gt;
+  h->W = ws + lay.off_w;
+  h->P = (float*)(ws + lay.off_p);
+  auto side = [&](Side& s, const size_t* o, int64_t dim, int64_t dim_p, int splits, int code) {
+    s.dim = dim;
+    s.dim_p = dim_p;
+    s.F[0] = (float*)(ws + o[0]);
+    s.F[1] = (float*)(ws + o[1]);
+    s.L = (float*)(ws + o[2]);
+    s.Li = (float*)(ws + o[3]);
+    s.Lw = ws + o[4];
+    s.Lw2 = h->cfg.whiten_split == 2 ? (void*)(ws + o[5]) : nullptr;
+    s.splits = splits;
+    s.code = code;
+  };
+  side(h->A, lay.off_A, h->n, lay.n_p, lay.splitsA, 1);
+  side(h->B, lay.off_B, h->m, lay.m_p, lay.splitsB, 2);
+
+  auto setup = [&]() -> ff_status {
+    FF_HIP(launch_set_int(h->st, 4, 0, h->stream));
+    const int64_t N = h->N, m = h->m, n = h->n;
+    if (lay.own_gx)
+      FF_HIP(launch_pack(cfg->G, (void*)h->Gx, N, m, n, lay.m_p, lay.n_p, 0, h->elem, h->stream));
+    FF_HIP(launch_pack(cfg->G, h->Gt, N, m, n, lay.n_p, lay.m_p, 1, h->elem, h->stream));
+    // Upper blocks of L^-1 are never written by the factorisation: zero once.
+    FF_HIP(launch_fill_f32(h->A.Li, n * n, 0.0f, h->stream));
+    FF_HIP(launch_fill_f32(h->B.Li, m * m, 0.0f, h->stream));
+    if (cfg->A0 != nullptr)
+      FF_HIP(hipMemcpyAsync(h->A.F[0], cfg->A0, n * n * sizeof(float), hipMemcpyDeviceToDevice,
+                            h->stream));
+    else
+      FF_HIP(launch_identity_f32(h->A.F[0], n, h->stream));
+    if (cfg->B0 != nullptr)
+      FF_HIP(hipMemcpyAsync(h->B.F[0], cfg->B0, m * m * sizeof(float), hipMemcpyDeviceToDevice,
+                            h->stream));
+    else
+      FF_HIP(launch_identity_f32(h->B.F[0], m, h->stream));
+    return FF_OK;
+  };
+  rc = setup();
+  if (rc != FF_OK) {
+    delete h;
+    return rc;
+  }
+  *out = h;
+  return FF_OK;
+}
+
+ff_status ff_iterate(ff_handle h, int iters, int* iters_done, double* loglik) {
+  if (iters_done != nullptr) *iters_done = 0;
+  if (h == nullptr) return fail(FF_ERR_INVALID_ARG, "handle is NULL");
+  if (iters < 0) return fail(FF_ERR_INVALID_ARG, "iters must be >= 0");
+  if (h->iters_total + (int64_t)iters > 0x7fffffffLL)
+    return fail(FF_ERR_STATE, "iteration counter overflow");
+  int total = 0;
+  const int cap = h->timing ? 32 : kLLCap;
+  while (total < iters) {
+    const int chunk = std::min(cap, iters - total);
+    int done = 0;
+    ff_status rc = iterate_chunk(h, chunk, &done, loglik ? loglik + total : nullptr);
+    total += done;
+    if (iters_done != nullptr) *iters_done = total;
+    if (rc != FF_OK) return rc;
+  }
+  return FF_OK;
+}
+
+ff_status ff_factors(ff_handle h, float* A, float* B, int on_host) {
+  if (h == nullptr) return fail(FF_ERR_INVALID_ARG, "handle is NULL");
+  const hipMemcpyKind kind = on_host ? hipMemcpyDeviceToHost : hipMemcpyDeviceToDevice;
+  if (A != nullptr)
+    FF_HIP(hipMemcpyAsync(A, h->A.F[h->cur], h->n * h->n * sizeof(float), kind, h->stream));
+  if (B != nullptr)
+    FF_HIP(hipMemcpyAsync(B, h->B.F[h->cur], h->m * h->m * sizeof(float), kind, h->stream));
+  if (on_host) FF_HIP(hipStreamSynchronize(h->stream));
+  return FF_OK;
+}
+
+ff_status ff_kron_apply(ff_handle h, const float* X, float* Y, int64_t batch, ff_apply_mode mode) {
+  if (h == nullptr) return fail(FF_ERR_INVALID_ARG, "handle is NULL");
+  if (batch < 0) return fail(FF_ERR_INVALID_ARG, "batch must be >= 0");
+  if (mode != FF_APPLY && mode != FF_APPLY_INV) return fail(FF_ERR_INVALID_ARG, "unknown mode");
+  if (batch == 0) return FF_OK;
+  if (X == nullptr || Y == nullptr || ((uintptr_t)X % 16) || ((uintptr_t)Y % 16))
+    return fail(FF_ERR_INVALID_ARG, "X and Y must be non-NULL 16-byte aligned device pointers");
+  const int64_t m = h->m, n = h->n, mn = m * n;
+  const char* xb = (const char*)X;
+  const char* yb = (const char*)Y;
+  if (xb < yb + batch * mn * 4 && yb < xb + batch * mn * 4)
+    return fail(FF_ERR_INVALID_ARG, "X and Y overlap");
+  const int cur = h->cur;
+  ff_status rc;
+  if (mode == FF_APPLY_INV) {
+    // Fresh factorisations of the current factors (label 0 marks them).
+    if ((rc = cholinv(h, h->A, cur, -1)) != FF_OK) return rc;
+    if ((rc = cholinv(h, h->B, cur, -1)) != FF_OK) return rc;
+  }
+  float* T = (float*)h->W;
+  const size_t tcap = std::max((size_t)h->N * h->lay.m_p * h->lay.n_p * h->elem,
+                               (size_t)mn * sizeof(float)) / sizeof(float);
+  const int64_t chunk = std::max<int64_t>(1, (int64_t)(tcap / (size_t)mn));
+  for (int64_t b0 = 0; b0 < batch; b0 += chunk) {
+    const int bc = (int)std::min<int64_t>(chunk, batch - b0);
+    const float* Xc = X + b0 * mn;
+    float* Yc = Y + b0 * mn;
+    GemmF32 g{};
+    g.st = h->st;
+    g.kseg = INT64_MAX / 4;
+    g.ksplit = 1;
+    g.alpha = 1.f;
+    g.beta = 0.f;
+    auto gemm = [&](const float* Aop, int64_t lda, int64_t sA, int tA, const float* Bop,
+                    int64_t ldb, int64_t sB, int tB, float* C, int64_t M, int64_t Nn, int64_t K,
+                    int flags) -> ff_status {
+      g.A = Aop; g.lda = lda; g.sA = sA; g.transA = tA;
+      g.B = Bop; g.ldb = ldb; g.sB = sB; g.transB = tB;
+      g.C = C; g.ldc = Nn; g.sC = mn;
+      g.M = M; g.N = Nn; g.K = K; g.flags = flags;
+      FF_HIP(launch_gemm_f32(g, bc, h->stream));
+      return FF_OK;
+    };
+    if (mode == FF_APPLY) {
+      // T = B X ; Y = T A
+      if ((rc = gemm(h->B.F[cur], m, 0, 0, Xc, n, mn, 0, T, m, n, m, 0)) != FF_OK) return rc;
+      if ((rc = gemm(T, n, mn, 0, h->A.F[cur], n, 0, 0, Yc, m, n, n, 0)) != FF_OK) return rc;
+    } else {
+      // B^-1 X A^-1 = Li_B^T Li_B X Li_A^T Li_A
+      if ((rc = gemm(h->B.Li, m, 0, 0, Xc, n, mn, 0, T, m, n, m, kKHiRow)) != FF_OK) return rc;
+      if ((rc = gemm(h->B.Li, m, 0, 1, T, n, mn, 0, Yc, m, n, m, kKLoRow)) != FF_OK) return rc;
+      if ((rc = gemm(Yc, n, mn, 0, h->A.Li, n, 0, 1, T, m, n, n, kKHiCol)) != FF_OK) return rc;
+      if ((rc = gemm(T, n, mn, 0, h->A.Li, n, 0, 0, Yc, m, n, n, kKLoCol)) != FF_OK) return rc;
+    }
+  }
+  int st[4];
+  if ((rc = read_status(h, st)) != FF_OK) return rc;
+  if (st[0] != 0) {
+    if ((rc = clear_status(h)) != FF_OK) return rc;
+    FF_HIP(hipStreamSynchronize(h->stream));
+    h->A.lw_valid = h->B.lw_valid = false;
+    return fail(FF_ERR_NOT_SPD, std::string("factor ") + (st[1] == 1 ? "A" : "B") +
+                                    " not positive definite in ff_kron_apply");
+  }
+  return FF_OK;
+}
+
+ff_status ff_destroy(ff_handle h) {
+  if (h == nullptr) return FF_OK;
+  hipStreamSynchronize(h->stream);
+  for (hipEvent_t e : h->events) hipEventDestroy(e);
+  delete h;
+  return FF_OK;
+}
+
+ff_status ff_set_timing(ff_handle h, int enable) {
+  if (h == nullptr) return fail(FF_ERR_INVALID_ARG, "handle is NULL");
+  if (enable && h->events.empty()) {
+    h->events.resize(2 * 10 * 32 + 16);
+    for (auto& e : h->events) FF_HIP(hipEventCreate(&e));
+  }
+  h->timing = enable != 0;
+  for (int k = 0; k < kTimedKernels; ++k) {
+    h->t_launches[k] = 0;
+    h->t_ms[k] = 0;
+    h->t_flop[k] = 0;
+  }
+  return FF_OK;
+}
+
+ff_status ff_kernel_timing(ff_handle h, int kernel, int64_t* launches, double* total_ms,
+                           double* alg_flop) {
+  if (h == nullptr) return fail(FF_ERR_INVALID_ARG, "handle is NULL");
+  if (kernel < 0 || kernel >= kTimedKernels) return fail(FF_ERR_INVALID_ARG, "unknown kernel id");
+  if (launches) *launches = h->t_launches[kernel];
+  if (total_ms) *total_ms = h->t_ms[kernel];
+  if (alg_flop) *alg_flop = h->t_flop[kernel];
+  return FF_OK;
+}
+
+}  // extern "C"

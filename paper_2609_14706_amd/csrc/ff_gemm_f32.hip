@@ -1,0 +1,222 @@
+// General fp32 product on the fp32 matrix cores (v_mfma_f32_32x32x2_f32).
+//
+// Used wherever the iteration needs fp32 products: the blocked Cholesky and
+// triangular inverse of the factors, the whole fp32 sample path (whitening
+// and symmetric product), and the Kronecker application.  128 x 128 output
+// tiles, four waves of 64 x 64 (2 x 2 matrix-core tiles), 16-wide k slices
+// staged through double-buffered LDS.  Any shape and either operand
+// transpose; k ranges can be clipped to the non-zero triangle of a
+// triangular operand, k can run over segments (the stacked samples), and k
+// can be split over the grid into partial outputs.  When every operand is
+// 16-byte aligned with leading dimensions divisible by 4, global loads are
+// 16-byte vectors (edge vectors fall back to element loads).
+#include "ff_common.hpp"
+#include "ff_kernels.hpp"
+
+namespace ff {
+namespace {
+
+constexpr int BT = 128;  // tile rows / cols
+constexpr int BK = 16;   // k per slice
+constexpr int LDP = BT + 4;
+
+__device__ __forceinline__ int64_t seg_off(int64_t k, int64_t kseg, int64_t seg) {
+  return (k / kseg) * seg + (k % kseg);
+}
+
+// One operand slice: 128 "outer" indices (rows of op(A) or columns of op(B))
+// x 16 k.  kmajor: the operand is contiguous along k (element (o, k) at
+// P[o * ld + koff(k)]); otherwise contiguous along o (at P[koff(k) * ld + o]).
+// Each thread fetches two 4-element vectors; slice[k][o] is written to LDS.
+template <bool VEC>
+struct SliceLoader {
+  f32x4 v[2];
+  __device__ __forceinline__ void load(const float* P, int64_t ld, bool kmajor, int64_t o0,
+                                       int64_t olim, int64_t k0, int64_t khi, int64_t kseg,
+                                       int64_t seg, int tid) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int idx = tid + 256 * q;
+      int o, k;
+      if (kmajor) { o = idx >> 2; k = (idx & 3) * 4; }
+      else { k = idx >> 5; o = (idx & 31) * 4; }
+      const int64_t go = o0 + o, gk = k0 + k;
+      f32x4 r = {0.f, 0.f, 0.f, 0.f};
+      bool full;
+      if (kmajor) full = go < olim && gk + 3 < khi;
+      else full = gk < khi && go + 3 < olim;
+      if (VEC && full) {
+        const int64_t ko = seg_off(gk, kseg, seg);
+        r = kmajor ? *reinterpret_cast<const f32x4*>(P + go * ld + ko)
+                   : *reinterpret_cast<const f32x4*>(P + ko * ld + go);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int64_t eo = kmajor ? go : go + e, ek = kmajor ? gk + e : gk;
+          if (eo < olim && ek < khi) {
+            const int64_t ko = seg_off(ek, kseg, seg);
+            r[e] = kmajor ? P[eo * ld + ko] : P[ko * ld + eo];
+          }
+        }
+      }
+      v[q] = r;
+    }
+  }
+  __device__ __forceinline__ void store(float (*S)[LDP], bool kmajor, int tid) const {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int idx = tid + 256 * q;
+      if (kmajor) {
+        const int o = idx >> 2, k = (idx & 3) * 4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) S[k + e][o] = v[q][e];
+      } else {
+        const int k = idx >> 5, o = (idx & 31) * 4;
+        *reinterpret_cast<f32x4*>(&S[k][o]) = v[q];
+      }
+    }
+  }
+};
+
+template <bool VEC>
+__global__ __launch_bounds__(256) void k_gemm_f32(GemmF32 p) {
+  if (ff_halted(p.st)) return;
+  const int64_t i0 = (int64_t)blockIdx.x * BT, j0 = (int64_t)blockIdx.y * BT;
+  if ((p.flags & kCLower) && j0 > i0 + BT - 1) return;
+  const float* A = p.A;
+  const float* B = p.B;
+  float* C = p.C;
+  int64_t klo = 0, khi = p.K;
+  if (p.flags & kKHiRow) khi = min(khi, i0 + BT);
+  if (p.flags & kKLoRow) klo = max(klo, i0);
+  if (p.flags & kKHiCol) khi = min(khi, j0 + BT);
+  if (p.flags & kKLoCol) klo = max(klo, j0);
+  if (p.ksplit > 1) {
+    const int64_t span = khi > klo ? khi - klo : 0;
+    const int64_t chunk = ((span + p.ksplit - 1) / p.ksplit + BK - 1) / BK * BK;
+    klo = klo + (int64_t)blockIdx.z * chunk;
+    khi = min(khi, klo + chunk);
+    C += (int64_t)blockIdx.z * p.sC;
+  } else {
+    A += (int64_t)blockIdx.z * p.sA;
+    B += (int64_t)blockIdx.z * p.sB;
+    C += (int64_t)blockIdx.z * p.sC;
+  }
+
+  __shared__ __align__(16) float As[2][BK][LDP];
+  __shared__ __align__(16) float Bs[2][BK][LDP];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int wm = wave >> 1, wn = wave & 1;
+  const bool amaj = p.transA == 0, bmaj = p.transB != 0;
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
+
+  if (klo < khi) {
+    SliceLoader<VEC> la, lb;
+    la.load(A, p.lda, amaj, i0, p.M, klo, khi, p.kseg, p.segA, tid);
+    lb.load(B, p.ldb, bmaj, j0, p.N, klo, khi, p.kseg, p.segB, tid);
+    la.store(As[0], amaj, tid);
+    lb.store(Bs[0], bmaj, tid);
+    __syncthreads();
+    int cur = 0;
+    for (int64_t k0 = klo; k0 < khi; k0 += BK) {
+      const bool more = k0 + BK < khi;
+      if (more) {
+        la.load(A, p.lda, amaj, i0, p.M, k0 + BK, khi, p.kseg, p.segA, tid);
+        lb.load(B, p.ldb, bmaj, j0, p.N, k0 + BK, khi, p.kseg, p.segB, tid);
+      }
+#pragma unroll
+      for (int s = 0; s < BK / 2; ++s) {
+        const int kr = 2 * s + (lane >> 5);
+        float fa[2], fb[2];
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          fa[t] = As[cur][kr][wm * 64 + t * 32 + (lane & 31)];
+          fb[t] = Bs[cur][kr][wn * 64 + t * 32 + (lane & 31)];
+        }
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+          for (int b = 0; b < 2; ++b)
+            acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[a], fb[b], acc[a][b], 0, 0, 0);
+      }
+      if (more) {
+        la.store(As[cur ^ 1], amaj, tid);
+        lb.store(Bs[cur ^ 1], bmaj, tid);
+      }
+      __syncthreads();
+      cur ^= 1;
+    }
+  }
+
+  const bool lower = (p.flags & kCLower) != 0;
+  const bool use_beta = p.ksplit <= 1 && p.beta != 0.0f;
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t i = i0 + wm * 64 + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        const int64_t j = j0 + wn * 64 + b * 32 + (lane & 31);
+        if (i < p.M && j < p.N && (!lower || i >= j)) {
+          float v = p.alpha * acc[a][b][r];
+          if (use_beta) v += p.beta * C[i * p.ldc + j];
+          C[i * p.ldc + j] = v;
+        }
+      }
+}
+
+__global__ __launch_bounds__(256) void k_reduce_rowmajor(const float* __restrict__ P, int splits,
+                                                         int64_t dim_p, float* __restrict__ F,
+                                                         int64_t dim, float scale, const int* st) {
+  if (ff_halted(st)) return;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= dim * dim) return;
+  const int64_t i = idx / dim, j = idx % dim;
+  if (j > i) return;
+  float s = 0.0f;
+  for (int z = 0; z < splits; ++z) s += P[(int64_t)z * dim_p * dim_p + i * dim_p + j];
+  s *= scale;
+  F[i * dim + j] = s;
+  F[j * dim + i] = s;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+}  // namespace
+
+hipError_t launch_gemm_f32(const GemmF32& p, int batch, hipStream_t s) {
+  if (p.M < 0 || p.N < 0 || p.K < 0 || batch < 1 || p.kseg < 1) return hipErrorInvalidValue;
+  if (p.ksplit > 1 && batch != 1) return hipErrorInvalidValue;
+  if (p.M == 0 || p.N == 0) return hipSuccess;
+  const int64_t gx = (p.M + BT - 1) / BT, gy = (p.N + BT - 1) / BT;
+  const int gz = p.ksplit > 1 ? p.ksplit : batch;
+  if (gx > 0x7fffffff || gy > 65535 || gz > 65535) return hipErrorInvalidValue;
+  const bool segmented = p.kseg < p.K;
+  const bool vec = aligned16(p.A) && aligned16(p.B) && p.lda % 4 == 0 && p.ldb % 4 == 0 &&
+                   (batch == 1 || (p.sA % 4 == 0 && p.sB % 4 == 0)) &&
+                   (!segmented || (p.kseg % 4 == 0 && p.segA % 4 == 0 && p.segB % 4 == 0));
+  const dim3 grid((uint32_t)gx, (uint32_t)gy, (uint32_t)gz);
+  if (vec)
+    hipLaunchKernelGGL(k_gemm_f32<true>, grid, dim3(256), 0, s, p);
+  else
+    hipLaunchKernelGGL(k_gemm_f32<false>, grid, dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_rowmajor(const float* P, int splits, int64_t dim_p, float* F,
+                                  int64_t dim, double scale, const int* st, hipStream_t s) {
+  if (dim <= 0 || dim > dim_p || splits < 1) return hipErrorInvalidValue;
+  const int64_t blocks = (dim * dim + 255) / 256;
+  hipLaunchKernelGGL(k_reduce_rowmajor, dim3((uint32_t)blocks), dim3(256), 0, s, P, splits, dim_p,
+                     F, dim, (float)scale, st);
+  return hipGetLastError();
+}
+
+}  // namespace ff

@@ -1,0 +1,115 @@
+// Host-side launchers of the FlipFlop kernels.  Every launcher enqueues on
+// the given stream, checks its shape preconditions on the host and returns
+// the launch status; none allocates memory.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ff {
+
+typedef uint16_t bf16_t;
+
+// ---------------------------------------------------------------- bf16 path
+// Tile of the bf16 matrix-core kernels; every padded dimension is a multiple.
+constexpr int kTileBF16 = 256;
+
+// Whitening (triangular product, bf16 matrix cores, fp32 accumulation):
+//   C[r][c] = sum_{k <= c} X[r][k] * Y[c][k]  (+ same with Y2 when non-null)
+// X: rows x Kp, Y/Y2: Kp x Kp lower triangular, C: rows x Kp, all row-major
+// bf16 with leading dimension Kp.  rows and Kp are multiples of 256.
+hipError_t launch_whiten_bf16(const bf16_t* X, const bf16_t* Y, const bf16_t* Y2, bf16_t* C,
+                              int64_t rows, int64_t Kp, const int* st, hipStream_t s);
+
+// Symmetric rank-k product over segmented rows, split over k:
+//   P[z][tile] = partial sums of X X^T for upper tiles (ti <= tj),
+// where row r of X is the concatenation over segments s < nseg of
+// X[s * seg_stride + r * ld .. + ld).  dim_p (rows) and ld are multiples of
+// 256 and 64.  P holds splits * T(T+1)/2 tiles of 256 x 256 fp32 in the
+// matrix-core fragment order (decoded by launch_reduce_frag).
+hipError_t launch_syrk_bf16(const bf16_t* X, int64_t dim_p, int64_t ld, int64_t seg_stride,
+                            int64_t nseg, int splits, float* P, const int* st, hipStream_t s);
+
+// F (dim x dim, fp32, row-major) = scale * sum_z P[z]  (upper tiles mirrored).
+hipError_t launch_reduce_frag(const float* P, int splits, int64_t dim_p, float* F, int64_t dim,
+                              double scale, const int* st, hipStream_t s);
+
+// ---------------------------------------------------------------- fp32 path
+enum GemmFlags : int {
+  kKHiRow = 1,   // k < i0 + 64   (left operand lower triangular)
+  kKLoRow = 2,   // k >= i0       (left operand upper triangular)
+  kKHiCol = 4,   // k < j0 + 64   (right operand upper triangular)
+  kKLoCol = 8,   // k >= j0       (right operand lower triangular)
+  kCLower = 16,  // write only C[i][j] with i >= j
+};
+
+struct GemmF32 {
+  const float* A;
+  const float* B;
+  float* C;
+  int64_t lda, ldb, ldc;
+  int64_t sA, sB, sC;  // batch strides (grid z = batch when ksplit == 1)
+  int64_t M, N, K;
+  int transA;          // 0: A(i,k) = A[i*lda + k]; 1: A(i,k) = A[k*lda + i]
+  int transB;          // 0: B(k,j) = B[k*ldb + j]; 1: B(k,j) = B[j*ldb + k]
+  float alpha, beta;
+  int flags;
+  int64_t kseg;        // segmented k: k -> (k / kseg) * seg + k % kseg (kseg = K: plain)
+  int64_t segA, segB;
+  int ksplit;          // > 1: grid z splits k, C += z * sC, beta ignored
+  const int* st;
+};
+// C = alpha * op(A) op(B) + beta * C on the fp32 matrix cores (64 x 64 tiles).
+hipError_t launch_gemm_f32(const GemmF32& p, int batch, hipStream_t s);
+
+// F (dim x dim) = scale * sum_z P[z] with P[z] row-major dim_p x dim_p, lower
+// triangle read, mirrored.
+hipError_t launch_reduce_rowmajor(const float* P, int splits, int64_t dim_p, float* F,
+                                  int64_t dim, double scale, const int* st, hipStream_t s);
+
+// ------------------------------------------------------ factorisation / misc
+constexpr int kLeaf = 128;  // diagonal block factorised inside one workgroup
+
+// Cholesky + inverse of a diagonal block of size b <= kLeaf.  Reads the lower
+// triangle of Lblk (ld), writes Li block (lower, zeros above), writes
+// sum(log diag L) to logdet[slot]; on a non-positive/NaN pivot sets
+// st = {iteration, side, pivot_base + j}.
+hipError_t launch_chol_leaf(const float* Lblk, float* Liblk, int64_t ld, int b, int64_t pivot_base,
+                            double* logdet, int slot, int iteration, int side, int* st,
+                            hipStream_t s);
+
+// out[s][r][c] (rows_p x cols_p) from G[s] (m x n): copy (transpose = 0,
+// rows_p >= m, cols_p >= n) or transpose (transpose = 1, rows_p >= n,
+// cols_p >= m), zero padding.  elem_bytes = 2 (bf16) or 4 (fp32).
+hipError_t launch_pack(const void* G, void* out, int64_t N, int64_t m, int64_t n, int64_t rows_p,
+                       int64_t cols_p, int transpose, int elem_bytes, hipStream_t s);
+
+// Lw (dim_p x dim_p, elem) = lower(Li) rounded (bf16: hi part; Lw2: lo part
+// if non-null), zero elsewhere.  elem_bytes = 2 or 4.
+hipError_t launch_convert_inverse(const float* Li, int64_t dim, void* Lw, void* Lw2, int64_t dim_p,
+                                  int elem_bytes, const int* st, hipStream_t s);
+
+// tr = trace(F); with kappa > 0, F += kappa * tr/dim * I first and tr is the
+// trace after damping.  fp64 accumulation, one workgroup, fixed order.
+hipError_t launch_trace_damp(float* F, int64_t dim, double kappa, double* tr, const int* st,
+                             hipStream_t s);
+
+// c = trA / n; FA /= c; FB *= c; *c_out = c.
+hipError_t launch_normalise(float* FA, int64_t n, float* FB, int64_t m, const double* trA,
+                            double* c_out, const int* st, hipStream_t s);
+
+// ll = -(N/2)(m logdetA + n logdetB) - (N m n / 2)(1 + log 2 pi), with
+// logdet = 2 * sum of slots; the side factorised before the normalisation
+// gets its log-determinant corrected by -+ dim * log c.
+hipError_t launch_loglik(const double* slotsA, int nA, const double* slotsB, int nB,
+                         const double* c, int first_is_B, double m, double n, double N,
+                         double* ll_out, const int* st, hipStream_t s);
+
+hipError_t launch_copy_f32(const float* src, float* dst, int64_t count, const int* st,
+                           hipStream_t s);
+hipError_t launch_fill_f32(float* dst, int64_t count, float v, hipStream_t s);
+hipError_t launch_identity_f32(float* dst, int64_t dim, hipStream_t s);
+hipError_t launch_set_int(int* dst, int64_t count, int v, hipStream_t s);
+
+}  // namespace ff
