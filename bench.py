@@ -24,6 +24,26 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "flip-flop iter/s + TFLOP/s (% bf16 MFMA peak), m=n=4096, N=128"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_attn-4096x4096-N128.md")
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_14706_amd", "csrc", "ff_gemm_bf16.hip")
+
+
+def recorded_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` from the committed counter summary, or
+    None when it was taken for another kernel/workload or the kernel source
+    has changed since."""
+    import hashlib
+    if workload != "attn-4096x4096-N128" or not os.path.exists(TRAFFIC_FILE):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_FILE):
+        if "=" in line and line.startswith("traffic_"):
+            k, v = line.strip().split("=", 1)
+            kv[k] = v
+    src = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
+    if kv.get("traffic_kernel") != kernel or kv.get("traffic_source_sha256") != src:
+        return None
+    return int(kv["traffic_bytes_per_launch"])
 PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 
 
@@ -138,9 +158,12 @@ def main():
                 if w.dtype == "bf16" else "k_gemm_f32",
                 "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4), "traffic": None,
+                "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-scaled)",
                 "launches": n_l, "avg_launch_ms": round(ms_l / max(n_l, 1), 4),
                 "alg_flop_per_launch": fl_l / max(n_l, 1)}
 
+    if w.dtype == "bf16":
+        roofline["traffic"] = recorded_traffic(roofline["kernel"], w.name)
     out = {
         "metric": METRIC,
         "value": round(iters_per_s, 4),

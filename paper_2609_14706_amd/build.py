@@ -16,6 +16,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libff.so")
+BENCH = os.path.join(HERE, "ffbench")
 SOURCES = ["ff_gemm_bf16.hip", "ff_gemm_f32.hip", "ff_chol.hip", "ff_aux.hip", "ff_engine.hip"]
 ARCH = "gfx950"
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
@@ -53,8 +54,15 @@ def build(verbose: bool = False) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"linking libff.so failed:\n{r.stdout}\n{r.stderr}")
     os.replace(tmp, LIB)
+    # native benchmark driver of the C ABI (used for hardware-counter runs)
+    cmd = [cc, *FLAGS, os.path.join(CSRC, "ffbench.hip"), "-o", BENCH + ".tmp",
+           f"-L{HERE}", "-lff", "-Wl,-rpath,$ORIGIN"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"building ffbench failed:\n{r.stdout}\n{r.stderr}")
+    os.replace(BENCH + ".tmp", BENCH)
     if verbose:
-        print("built", LIB, flush=True)
+        print("built", LIB, "and", BENCH, flush=True)
     return LIB
 
 

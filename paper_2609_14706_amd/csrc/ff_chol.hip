@@ -57,11 +57,12 @@ __global__ __launch_bounds__(256) void k_chol_leaf(const float* __restrict__ Lbl
 
   // ---------------------------------------------------------- factorisation
   for (int p = 0; p < NT; ++p) {
-    if (tj == p) {  // the 16 lanes of block column p
+    if (tj == p) {  // the 16 lanes of block column p; (p, p) is lane (17 p) mod 64
+      const int dl = (17 * p) & 63;
       bool ok = true;
 #pragma unroll
       for (int c = 0; c < TB; ++c) {
-        const float d = __shfl(blk[c][c], p, 16);
+        const float d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(blk[c][c]), dl));
         if (!(d > 0.0f) || !(d < INFINITY)) ok = false;
         const float s = sqrtf(d), rs = 1.0f / s;
 #pragma unroll
@@ -71,40 +72,17 @@ __global__ __launch_bounds__(256) void k_chol_leaf(const float* __restrict__ Lbl
         }
 #pragma unroll
         for (int c2 = c + 1; c2 < TB; ++c2) {
-          const float lc = __shfl(blk[c2][c], p, 16);
+          const float lc =
+              __int_as_float(__builtin_amdgcn_readlane(__float_as_int(blk[c2][c]), dl));
 #pragma unroll
           for (int r = 0; r < TB; ++r) blk[r][c2] -= blk[r][c] * lc;
         }
       }
-      if (ti == p) {
-        if (!ok) {
-          // first failing column of this block: recompute pivots in order
-          int c0 = 0;
-          for (; c0 < TB; ++c0)
-            if (!(blk[c0][c0] > 0.0f) || !(blk[c0][c0] < INFINITY)) break;
-          bad = p * TB + (c0 < TB ? c0 : 0);
-        }
-        double lsum = 0.0;
-#pragma unroll
-        for (int c = 0; c < TB; ++c) lsum += log((double)blk[c][c]);
-        ldp[p] = lsum;
-        // inverse of the 8 x 8 lower diagonal block
-        float inv[TB][TB];
-#pragma unroll
-        for (int c = 0; c < TB; ++c) {
-#pragma unroll
-          for (int r = 0; r < TB; ++r) {
-            float acc = r == c ? 1.0f : 0.0f;
-#pragma unroll
-            for (int k = 0; k < TB; ++k)
-              if (k >= c && k < r) acc -= blk[r][k] * inv[k][c];
-            inv[r][c] = r >= c ? acc / blk[r][r] : 0.0f;
-          }
-        }
-#pragma unroll
-        for (int r = 0; r < TB; ++r)
-#pragma unroll
-          for (int c = 0; c < TB; ++c) Ld[p][r][c] = inv[r][c];
+      if (!ok && ti == p) {  // first failing column of this block
+        int c0 = 0;
+        for (; c0 < TB; ++c0)
+          if (!(blk[c0][c0] > 0.0f) || !(blk[c0][c0] < INFINITY)) break;
+        bad = p * TB + (c0 < TB ? c0 : 0);
       }
       if (ti >= p) {
 #pragma unroll
@@ -152,6 +130,30 @@ __global__ __launch_bounds__(256) void k_chol_leaf(const float* __restrict__ Lbl
     }
     return;
   }
+  // Diagonal blocks, in parallel: log-determinant share and 8 x 8 inverse.
+  if (ti == tj) {
+    double lsum = 0.0;
+#pragma unroll
+    for (int c = 0; c < TB; ++c) lsum += log((double)blk[c][c]);
+    ldp[ti] = lsum;
+    float inv[TB][TB];
+#pragma unroll
+    for (int c = 0; c < TB; ++c) {
+#pragma unroll
+      for (int r = 0; r < TB; ++r) {
+        float acc = r == c ? 1.0f : 0.0f;
+#pragma unroll
+        for (int k = 0; k < TB; ++k)
+          if (k >= c && k < r) acc -= blk[r][k] * inv[k][c];
+        inv[r][c] = r >= c ? acc / blk[r][r] : 0.0f;
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < TB; ++r)
+#pragma unroll
+      for (int c = 0; c < TB; ++c) Ld[ti][r][c] = inv[r][c];
+  }
+  __syncthreads();
   if (tid == 0) {
     double s = 0.0;
     for (int p = 0; p < NT; ++p) s += ldp[p];

@@ -12,9 +12,12 @@
 //    i of the Section 5 updates), upper tiles only, split over k into
 //    deterministic partial sums that a second kernel adds in fixed order.
 //
-// Operands are staged through LDS in 64-wide k slices, double buffered, with
-// an XOR swizzle of the 16-byte chunks of each 128-byte row so that the
-// matrix-core fragment reads of 32 consecutive rows hit distinct banks.
+// Operands move global -> LDS with the direct-to-LDS loads of gfx950
+// (global_load_lds_dwordx4, no register staging) in 32-wide k slices through
+// a 5-slot ring (160 KB), four slices in flight ahead of the matrix cores, which
+// covers the memory latency with one workgroup of four waves per CU.  The
+// 16-byte chunks of each 64-byte row are XOR-swizzled so that fragment
+// reads of consecutive rows hit distinct banks.
 #include "ff_common.hpp"
 #include "ff_kernels.hpp"
 
@@ -22,89 +25,161 @@ namespace ff {
 namespace {
 
 constexpr int TM = 256;       // tile rows (and columns)
-constexpr int TK = 64;        // k per LDS stage
-constexpr int CH = TK / 8;    // 16-byte chunks per tile row
+constexpr int TK = 32;        // k per LDS stage
+constexpr int NSTAGE = 5;     // LDS ring depth (four slices in flight, 160 KB)
 constexpr int NTHR = 256;     // four waves
 constexpr int TILE_FLOATS = TM * TM;
+constexpr int CHUNKS = TM * TK / 8;  // 16-byte chunks per operand per stage (1024)
 
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+typedef __attribute__((address_space(3))) void lds_void;
 
-struct __align__(16) Stage {
-  u32x4 a[TM * CH];
-  u32x4 b[TM * CH];
+// Stage layout: chunk position P = 4 row + slot; slot s of row r holds the
+// 16-byte k chunk c = s ^ ((r >> 1) & 3), so that the fragment reads of 8
+// consecutive rows fall on distinct banks.
+struct __align__(16) Ring {
+  u32x4 a[NSTAGE][CHUNKS];
+  u32x4 b[NSTAGE][CHUNKS];
 };
 
-__device__ __forceinline__ int swz(int row, int chunk) { return row * CH + (chunk ^ (row & 7)); }
+__device__ __forceinline__ int chunk_pos(int row, int c) { return row * 4 + (c ^ ((row >> 1) & 3)); }
 
-// Per-thread share of one operand slice: chunk (tid & 7) of rows
-// (tid >> 3) + 32 q, q = 0..7.
-struct Loader {
-  uint32_t off[8];
-  __device__ __forceinline__ void init(int tid, uint32_t ld) {
-#pragma unroll
-    for (int q = 0; q < 8; ++q) off[q] = (uint32_t)((tid >> 3) + 32 * q) * ld + (uint32_t)(tid & 7) * 8u;
-  }
-  __device__ __forceinline__ void load(const bf16_t* base, u32x4 (&r)[8]) const {
-#pragma unroll
-    for (int q = 0; q < 8; ++q) r[q] = *reinterpret_cast<const u32x4*>(base + off[q]);
-  }
-};
-
-__device__ __forceinline__ void stage_store(u32x4* dst, int tid, const u32x4 (&r)[8]) {
-#pragma unroll
-  for (int q = 0; q < 8; ++q) dst[swz((tid >> 3) + 32 * q, tid & 7)] = r[q];
+// vmcnt(N) with the other counters left alone (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-__device__ __forceinline__ void stage_compute(const Stage& sm, int wave, int lane,
-                                              f32x16 (&acc)[4][4]) {
-  const int wm = wave >> 1, wn = wave & 1;
-  const int lrow = lane & 31, kh = lane >> 5;
+// lgkmcnt(0) with the other counters left alone.
+__device__ __forceinline__ void wait_lds() { __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4)); }
+
+// Per-lane element offsets of the four chunks this lane moves per operand and
+// stage: instruction q of wave w fills positions (4 q + w) 64 + lane.
+__device__ __forceinline__ void chunk_offsets(int wave, int lane, uint32_t ld, uint32_t (&off)[4]) {
 #pragma unroll
-  for (int kk = 0; kk < TK / 16; ++kk) {
-    bf16x8 fa[4], fb[4];
+  for (int q = 0; q < 4; ++q) {
+    const int P = (q * 4 + wave) * 64 + lane;
+    const int row = P >> 2, slot = P & 3;
+    const int c = slot ^ ((row >> 1) & 3);
+    off[q] = (uint32_t)row * ld + (uint32_t)c * 8u;
+  }
+}
+
+// Asynchronous global -> LDS copy of one k slice of both operands.
+__device__ __forceinline__ void issue_stage(Ring& sm, int buf, const bf16_t* pa, const bf16_t* pb,
+                                            const uint32_t (&oa)[4], const uint32_t (&ob)[4],
+                                            int wave) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    __builtin_amdgcn_global_load_lds((const void*)(pa + oa[q]),
+                                     (lds_void*)&sm.a[buf][(q * 4 + wave) * 64], 16, 0, 0);
+    __builtin_amdgcn_global_load_lds((const void*)(pb + ob[q]),
+                                     (lds_void*)&sm.b[buf][(q * 4 + wave) * 64], 16, 0, 0);
+  }
+}
+
+// Matrix-core fragments of one LDS slot: for each of the two 16-wide k
+// steps, the rows (A side) and columns (B side) of this wave's 128 x 128
+// quadrant, 8 consecutive k per lane.  f[kk][0..3] = A, f[kk][4..7] = B.
+typedef bf16x8 Frags[2][8];
+
+__device__ __forceinline__ void read_frags(const Ring& sm, int buf, int wave, int lane, Frags& f) {
+  const int wm = wave >> 1, wn = wave & 1;
+  const int lrow = lane & 31;
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) {
+    const int c = kk * 2 + (lane >> 5);
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      fa[t] = __builtin_bit_cast(bf16x8, sm.a[swz(wm * 128 + t * 32 + lrow, kk * 2 + kh)]);
-      fb[t] = __builtin_bit_cast(bf16x8, sm.b[swz(wn * 128 + t * 32 + lrow, kk * 2 + kh)]);
+      f[kk][t] = __builtin_bit_cast(bf16x8, sm.a[buf][chunk_pos(wm * 128 + t * 32 + lrow, c)]);
+      f[kk][4 + t] = __builtin_bit_cast(bf16x8, sm.b[buf][chunk_pos(wn * 128 + t * 32 + lrow, c)]);
     }
+  }
+}
+
+__device__ __forceinline__ void mfma_slot(const Frags& f, f32x16 (&acc)[4][4]) {
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[kk][i], f[kk][4 + j], acc[i][j], 0, 0, 0);
+}
+
+// Slices requested but not yet known to have landed may number at most
+// `pending` (0..4) when this returns (eight copies per slice and lane).
+__device__ __forceinline__ void wait_pending(int pending) {
+  if (pending >= 4) wait_vmem<32>();
+  else if (pending == 3) wait_vmem<24>();
+  else if (pending == 2) wait_vmem<16>();
+  else if (pending == 1) wait_vmem<8>();
+  else wait_vmem<0>();
+}
+
+// One k slice i (not the last) of the main loop, register set CUR holding
+// its fragments: wait for slice i + 1, barrier (every wave has slice i in
+// registers, so its slot is free), request slice i + 5 into that slot, then
+// read slice i + 1 into the other register set interleaved with the 32
+// products of slice i.
+template <int CUR, class Addr>
+__device__ __forceinline__ void loop_step(Ring& sm, int i, int n, int kt0, const Addr& addr,
+                                          const uint32_t (&oa)[4], const uint32_t (&ob)[4],
+                                          int wave, int lane, Frags (&F)[2],
+                                          f32x16 (&acc)[4][4]) {
+  wait_pending(min(n, i + NSTAGE) - (i + 2));
+  wait_lds();  // this wave's reads of slice i (issued one step ago) are complete
+  __builtin_amdgcn_s_barrier();
+  if (i + NSTAGE < n) {
+    const bf16_t *pa, *pb;
+    addr(kt0 + i + NSTAGE, pa, pb);
+    issue_stage(sm, (i + NSTAGE) % NSTAGE, pa, pb, oa, ob, wave);
+  }
+  read_frags(sm, (i + 1) % NSTAGE, wave, lane, F[CUR ^ 1]);
+  mfma_slot(F[CUR], acc);
+#pragma unroll
+  for (int q = 0; q < 16; ++q) {
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // two matrix-core products
   }
 }
 
 // acc += sum over k slices [kt0, kt1) of Aslice(kt) Bslice(kt)^T, where
-// addr(kt, pa, pb) yields the slice base pointers (row 0, k = 64 kt).
+// addr(kt, pa, pb) yields the slice base pointers (row 0, k = 32 kt).
+// Slices are copied global -> LDS five slots ahead; fragments are read one
+// slice ahead into a second register set.
 template <class Addr>
-__device__ __forceinline__ void mainloop(Stage* sm, int kt0, int kt1, uint32_t lda, uint32_t ldb,
+__device__ __forceinline__ void mainloop(Ring& sm, int kt0, int kt1, uint32_t lda, uint32_t ldb,
                                          const Addr& addr, f32x16 (&acc)[4][4]) {
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  if (kt0 >= kt1) return;
-  Loader la, lb;
-  la.init(tid, lda);
-  lb.init(tid, ldb);
-  u32x4 ra[8], rb[8];
-  const bf16_t *pa, *pb;
-  addr(kt0, pa, pb);
-  la.load(pa, ra);
-  lb.load(pb, rb);
-  stage_store(sm[0].a, tid, ra);
-  stage_store(sm[0].b, tid, rb);
-  __syncthreads();
-  int cur = 0;
-  for (int kt = kt0; kt + 1 < kt1; ++kt) {
-    addr(kt + 1, pa, pb);
-    la.load(pa, ra);
-    lb.load(pb, rb);
-    stage_compute(sm[cur], wave, lane, acc);
-    stage_store(sm[cur ^ 1].a, tid, ra);
-    stage_store(sm[cur ^ 1].b, tid, rb);
-    __syncthreads();
-    cur ^= 1;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS bases in SGPRs
+  const int n = kt1 - kt0;
+  if (n <= 0) return;
+  uint32_t oa[4], ob[4];
+  chunk_offsets(wave, lane, lda, oa);
+  chunk_offsets(wave, lane, ldb, ob);
+  for (int s = 0; s < NSTAGE && s < n; ++s) {
+    const bf16_t *pa, *pb;
+    addr(kt0 + s, pa, pb);
+    issue_stage(sm, s, pa, pb, oa, ob, wave);
   }
-  stage_compute(sm[cur], wave, lane, acc);
+  wait_pending(min(n, NSTAGE) - 1);
+  __builtin_amdgcn_s_barrier();
+  Frags F[2];
+  read_frags(sm, 0, wave, lane, F[0]);
+  int i = 0;
+  for (; i + 2 < n; i += 2) {
+    loop_step<0>(sm, i, n, kt0, addr, oa, ob, wave, lane, F, acc);
+    loop_step<1>(sm, i + 1, n, kt0, addr, oa, ob, wave, lane, F, acc);
+  }
+  if (n - i == 2) {
+    loop_step<0>(sm, i, n, kt0, addr, oa, ob, wave, lane, F, acc);
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int t = 0; t < 8; ++t) F[0][kk][t] = F[1][kk][t];
+  }
+  mfma_slot(F[0], acc);
   __syncthreads();
 }
 
@@ -123,7 +198,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_whiten_bf16(const bf16_t* __restric
                                                          bf16_t* __restrict__ C, uint32_t Kp,
                                                          const int* st) {
   if (ff_halted(st)) return;
-  __shared__ Stage sm[2];
+  __shared__ Ring sm;
   const uint32_t ncol = Kp / TM;
   const uint32_t t = xcd_remap(blockIdx.x, gridDim.x);
   const uint32_t rb = t / ncol;
@@ -180,7 +255,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_syrk_bf16(const bf16_t* __restrict_
                                                        uint32_t T, uint32_t ntiles, uint32_t splits,
                                                        float* __restrict__ P, const int* st) {
   if (ff_halted(st)) return;
-  __shared__ Stage sm[2];
+  __shared__ Ring sm;
   const uint32_t t = xcd_remap(blockIdx.x, gridDim.x);
   const uint32_t z = t / ntiles, tile = t % ntiles;
   uint32_t ti, tj;

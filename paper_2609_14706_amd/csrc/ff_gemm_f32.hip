@@ -25,48 +25,45 @@ __device__ __forceinline__ int64_t seg_off(int64_t k, int64_t kseg, int64_t seg)
 }
 
 // One operand slice: 128 "outer" indices (rows of op(A) or columns of op(B))
-// x 16 k.  kmajor: the operand is contiguous along k (element (o, k) at
+// x 16 k.  KMAJ: the operand is contiguous along k (element (o, k) at
 // P[o * ld + koff(k)]); otherwise contiguous along o (at P[koff(k) * ld + o]).
-// Each thread fetches two 4-element vectors; slice[k][o] is written to LDS.
-template <bool VEC>
+// Each thread fetches two 4-element groups; slice[k][o] is written to LDS.
+// FAST: the whole slice is in bounds and 16-byte vectors can be used.
+template <bool KMAJ, bool FAST>
 struct SliceLoader {
   f32x4 v[2];
-  __device__ __forceinline__ void load(const float* P, int64_t ld, bool kmajor, int64_t o0,
-                                       int64_t olim, int64_t k0, int64_t khi, int64_t kseg,
-                                       int64_t seg, int tid) {
+  __device__ __forceinline__ void load(const float* P, int64_t ld, int64_t o0, int64_t olim,
+                                       int64_t k0, int64_t khi, int64_t kseg, int64_t seg,
+                                       int tid) {
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
       const int idx = tid + 256 * q;
-      int o, k;
-      if (kmajor) { o = idx >> 2; k = (idx & 3) * 4; }
-      else { k = idx >> 5; o = (idx & 31) * 4; }
+      const int o = KMAJ ? idx >> 2 : (idx & 31) * 4;
+      const int k = KMAJ ? (idx & 3) * 4 : idx >> 5;
       const int64_t go = o0 + o, gk = k0 + k;
-      f32x4 r = {0.f, 0.f, 0.f, 0.f};
-      bool full;
-      if (kmajor) full = go < olim && gk + 3 < khi;
-      else full = gk < khi && go + 3 < olim;
-      if (VEC && full) {
+      if (FAST) {
         const int64_t ko = seg_off(gk, kseg, seg);
-        r = kmajor ? *reinterpret_cast<const f32x4*>(P + go * ld + ko)
-                   : *reinterpret_cast<const f32x4*>(P + ko * ld + go);
+        v[q] = KMAJ ? *reinterpret_cast<const f32x4*>(P + go * ld + ko)
+                    : *reinterpret_cast<const f32x4*>(P + ko * ld + go);
       } else {
+        f32x4 r = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int64_t eo = kmajor ? go : go + e, ek = kmajor ? gk + e : gk;
+          const int64_t eo = KMAJ ? go : go + e, ek = KMAJ ? gk + e : gk;
           if (eo < olim && ek < khi) {
             const int64_t ko = seg_off(ek, kseg, seg);
-            r[e] = kmajor ? P[eo * ld + ko] : P[ko * ld + eo];
+            r[e] = KMAJ ? P[eo * ld + ko] : P[ko * ld + eo];
           }
         }
+        v[q] = r;
       }
-      v[q] = r;
     }
   }
-  __device__ __forceinline__ void store(float (*S)[LDP], bool kmajor, int tid) const {
+  __device__ __forceinline__ void store(float (*S)[LDP], int tid) const {
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
       const int idx = tid + 256 * q;
-      if (kmajor) {
+      if (KMAJ) {
         const int o = idx >> 2, k = (idx & 3) * 4;
 #pragma unroll
         for (int e = 0; e < 4; ++e) S[k + e][o] = v[q][e];
@@ -78,7 +75,59 @@ struct SliceLoader {
   }
 };
 
-template <bool VEC>
+struct TileLDS {
+  float a[2][BK][LDP];
+  float b[2][BK][LDP];
+};
+
+// acc += op(A)[i0.., klo..khi) op(B)[klo..khi), j0..) for one 128 x 128 tile.
+template <bool AK, bool BKM, bool FAST>
+__device__ __forceinline__ void tile_product(const GemmF32& p, const float* A, const float* B,
+                                             int64_t i0, int64_t j0, int64_t klo, int64_t khi,
+                                             TileLDS& sm, f32x16 (&acc)[2][2]) {
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int wm = wave >> 1, wn = wave & 1;
+  SliceLoader<AK, FAST> la;
+  SliceLoader<BKM, FAST> lb;
+  la.load(A, p.lda, i0, p.M, klo, khi, p.kseg, p.segA, tid);
+  lb.load(B, p.ldb, j0, p.N, klo, khi, p.kseg, p.segB, tid);
+  la.store(sm.a[0], tid);
+  lb.store(sm.b[0], tid);
+  __syncthreads();
+  int cur = 0;
+  for (int64_t k0 = klo; k0 < khi; k0 += BK) {
+    const bool more = k0 + BK < khi;
+    if (more) {
+      la.load(A, p.lda, i0, p.M, k0 + BK, khi, p.kseg, p.segA, tid);
+      lb.load(B, p.ldb, j0, p.N, k0 + BK, khi, p.kseg, p.segB, tid);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int s = 0; s < BK / 2; ++s) {
+      const int kr = 2 * s + (lane >> 5);
+      float fa[2], fb[2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        fa[t] = sm.a[cur][kr][wm * 64 + t * 32 + (lane & 31)];
+        fb[t] = sm.b[cur][kr][wn * 64 + t * 32 + (lane & 31)];
+      }
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[a], fb[b], acc[a][b], 0, 0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    if (more) {
+      la.store(sm.a[cur ^ 1], tid);
+      lb.store(sm.b[cur ^ 1], tid);
+    }
+    __syncthreads();
+    cur ^= 1;
+  }
+}
+
+template <int TA, int TBT, bool VEC>
 __global__ __launch_bounds__(256) void k_gemm_f32(GemmF32 p) {
   if (ff_halted(p.st)) return;
   const int64_t i0 = (int64_t)blockIdx.x * BT, j0 = (int64_t)blockIdx.y * BT;
@@ -102,12 +151,9 @@ __global__ __launch_bounds__(256) void k_gemm_f32(GemmF32 p) {
     B += (int64_t)blockIdx.z * p.sB;
     C += (int64_t)blockIdx.z * p.sC;
   }
-
-  __shared__ __align__(16) float As[2][BK][LDP];
-  __shared__ __align__(16) float Bs[2][BK][LDP];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  __shared__ __align__(16) TileLDS sm;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  const bool amaj = p.transA == 0, bmaj = p.transB != 0;
   f32x16 acc[2][2];
 #pragma unroll
   for (int a = 0; a < 2; ++a)
@@ -115,45 +161,11 @@ __global__ __launch_bounds__(256) void k_gemm_f32(GemmF32 p) {
     for (int b = 0; b < 2; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
-
   if (klo < khi) {
-    SliceLoader<VEC> la, lb;
-    la.load(A, p.lda, amaj, i0, p.M, klo, khi, p.kseg, p.segA, tid);
-    lb.load(B, p.ldb, bmaj, j0, p.N, klo, khi, p.kseg, p.segB, tid);
-    la.store(As[0], amaj, tid);
-    lb.store(Bs[0], bmaj, tid);
-    __syncthreads();
-    int cur = 0;
-    for (int64_t k0 = klo; k0 < khi; k0 += BK) {
-      const bool more = k0 + BK < khi;
-      if (more) {
-        la.load(A, p.lda, amaj, i0, p.M, k0 + BK, khi, p.kseg, p.segA, tid);
-        lb.load(B, p.ldb, bmaj, j0, p.N, k0 + BK, khi, p.kseg, p.segB, tid);
-      }
-#pragma unroll
-      for (int s = 0; s < BK / 2; ++s) {
-        const int kr = 2 * s + (lane >> 5);
-        float fa[2], fb[2];
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          fa[t] = As[cur][kr][wm * 64 + t * 32 + (lane & 31)];
-          fb[t] = Bs[cur][kr][wn * 64 + t * 32 + (lane & 31)];
-        }
-#pragma unroll
-        for (int a = 0; a < 2; ++a)
-#pragma unroll
-          for (int b = 0; b < 2; ++b)
-            acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[a], fb[b], acc[a][b], 0, 0, 0);
-      }
-      if (more) {
-        la.store(As[cur ^ 1], amaj, tid);
-        lb.store(Bs[cur ^ 1], bmaj, tid);
-      }
-      __syncthreads();
-      cur ^= 1;
-    }
+    const bool fast = VEC && i0 + BT <= p.M && j0 + BT <= p.N && (khi - klo) % BK == 0;
+    if (fast) tile_product<TA == 0, TBT != 0, VEC>(p, A, B, i0, j0, klo, khi, sm, acc);
+    else tile_product<TA == 0, TBT != 0, false>(p, A, B, i0, j0, klo, khi, sm, acc);
   }
-
   const bool lower = (p.flags & kCLower) != 0;
   const bool use_beta = p.ksplit <= 1 && p.beta != 0.0f;
 #pragma unroll
@@ -203,10 +215,17 @@ hipError_t launch_gemm_f32(const GemmF32& p, int batch, hipStream_t s) {
                    (batch == 1 || (p.sA % 4 == 0 && p.sB % 4 == 0)) &&
                    (!segmented || (p.kseg % 4 == 0 && p.segA % 4 == 0 && p.segB % 4 == 0));
   const dim3 grid((uint32_t)gx, (uint32_t)gy, (uint32_t)gz);
-  if (vec)
-    hipLaunchKernelGGL(k_gemm_f32<true>, grid, dim3(256), 0, s, p);
-  else
-    hipLaunchKernelGGL(k_gemm_f32<false>, grid, dim3(256), 0, s, p);
+  const int sel = (p.transA ? 1 : 0) | (p.transB ? 2 : 0) | (vec ? 4 : 0);
+  switch (sel) {
+    case 0: hipLaunchKernelGGL((k_gemm_f32<0, 0, false>), grid, dim3(256), 0, s, p); break;
+    case 1: hipLaunchKernelGGL((k_gemm_f32<1, 0, false>), grid, dim3(256), 0, s, p); break;
+    case 2: hipLaunchKernelGGL((k_gemm_f32<0, 1, false>), grid, dim3(256), 0, s, p); break;
+    case 3: hipLaunchKernelGGL((k_gemm_f32<1, 1, false>), grid, dim3(256), 0, s, p); break;
+    case 4: hipLaunchKernelGGL((k_gemm_f32<0, 0, true>), grid, dim3(256), 0, s, p); break;
+    case 5: hipLaunchKernelGGL((k_gemm_f32<1, 0, true>), grid, dim3(256), 0, s, p); break;
+    case 6: hipLaunchKernelGGL((k_gemm_f32<0, 1, true>), grid, dim3(256), 0, s, p); break;
+    default: hipLaunchKernelGGL((k_gemm_f32<1, 1, true>), grid, dim3(256), 0, s, p); break;
+  }
   return hipGetLastError();
 }
 
