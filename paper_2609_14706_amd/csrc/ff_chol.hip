@@ -7,14 +7,18 @@
 // handled here by one workgroup; larger factors are assembled by the host
 // recursion from these blocks and fp32 matrix-core products.
 //
-// Register-blocked: thread (ti, tj), tid = 16 tj + ti, holds the 8 x 8 block
-// (ti, tj) of the lower triangle.  The 16 threads of block column p are
-// consecutive lanes of one wave, so the panel factorisation of block column p
-// needs only lane shuffles; the panel is then published in LDS and every
-// thread applies the rank-8 update to its own block (one barrier per block
-// column).  The inverse follows right-looking by block rows from the stored
-// panels.  A ragged block (b < 128) is padded with the identity.
+// Inside the block the same recursion runs in LDS: for a block [[A11, .],
+// [A21, A22]] of size s (halves h = s/2)
+//     (L11, X11) = cholinv(A11);  L21 = A21 X11^T;  A22 -= L21 L21^T;
+//     (L22, X22) = cholinv(A22);  X21 = -X22 (L21 X11)
+// with X = L^-1.  32 x 32 base blocks are factored and inverted by one wave
+// in registers (half the lanes hold rows of L, half columns of L^-1; each new
+// column of L is broadcast through LDS); the products run on the fp32 matrix
+// cores, one output tile per wave.  A ragged block (b < 128) is padded with
+// the identity.
 #include <math.h>
+
+#include <type_traits>
 
 #include "ff_common.hpp"
 #include "ff_kernels.hpp"
@@ -22,105 +26,240 @@
 namespace ff {
 namespace {
 
-constexpr int NB = 128;  // block size
-constexpr int TB = 8;    // per-thread block
-constexpr int NT = NB / TB;
+constexpr int NB = 128;     // block size
+constexpr int BS = 32;      // base block
+constexpr int SP = NB + 1;  // LDS row pitch (conflict-free column reads)
+
+struct LeafLDS {
+  float S[NB][SP];  // A, overwritten by L (lower triangle)
+  float X[NB][SP];  // L^-1
+  float T[64][65];  // product scratch
+  float C[BS][BS];  // column j of the base block's L at pivot step j
+  double ldp[NB / BS];
+  int bad;
+};
+
+__device__ __forceinline__ float bcast(float v, int lane) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+
+// Factor and invert the 32 x 32 block at (o, o) with one wave.  Lane r < 32
+// holds row r of the block, which becomes row r of L; lane 32 + r holds
+// column r of X = L^-1 (starting from the unit vector).  Pivot step j
+// scales entry j of every lane by 1 / L[j][j] (lane j keeps L[j][j]) and
+// subtracts v[j] times column j of L from entries j+1.. of every lane: for
+// the row lanes this is the Cholesky update, for the column lanes the
+// forward substitution of L X = I.  Only entry j+1 of that update lies on
+// the path to the next pivot: its multiplier L[j+1][j] is broadcast with
+// v_readlane and applied at the start of the next step.  The rest of the
+// column goes through LDS (sm.C[j][.], read back as uniform vectors) and is
+// applied one step later, off that path.  Row-lane entries above the
+// diagonal are never read for the lower triangle and are cleared at the end.
+// Returns the block-relative failing column or -1.
+__device__ __forceinline__ int base_block(LeafLDS& sm, int o, int lane) {
+  float v[BS], col[BS], nxt[BS];
+  const int r = lane & 31;
+  const bool rowlane = lane < BS;
+#pragma unroll
+  for (int c = 0; c < BS; ++c) {
+    v[c] = rowlane ? (c <= r ? sm.S[o + r][o + c] : 0.0f) : (c == r ? 1.0f : 0.0f);
+    col[c] = 0.0f;
+    nxt[c] = 0.0f;
+  }
+  int bad = -1;
+  float diag = 1.0f;           // L[r][r] (row lanes)
+  float vp = 0.0f, lp = 0.0f;  // previous step's multiplier v[j-1] and L[j][j-1]
+#pragma unroll
+  for (int j = 0; j < BS; ++j) {
+    if (j > 0) v[j] -= vp * lp;  // last update of entry j (from step j-1)
+    const float d = bcast(v[j], j);
+    if (!(d > 0.0f) || !(d < INFINITY)) {
+      if (bad < 0) bad = j;
+    }
+    const float rs = __builtin_amdgcn_rsqf(d), s = d * rs;  // 1 / L[j][j], L[j][j]
+    if (lane == j) diag = s;
+    const float vj = lane == j ? s : v[j] * rs;
+    v[j] = vj;
+    const float ln = j + 1 < BS ? bcast(vj, j + 1) : 0.0f;  // L[j+1][j]
+    if (j + 2 < BS) {
+      if (rowlane) sm.C[j][r] = vj;
+#pragma unroll
+      for (int c = j + 2; c < BS; ++c) nxt[c] = sm.C[j][c];  // L[c][j], uniform
+    }
+    // the rest of step j-1's update
+    if (j > 0) {
+#pragma unroll
+      for (int c = j + 1; c < BS; ++c) v[c] -= vp * col[c];
+    }
+    // bounded register lifetimes: step j-1 is complete here
+#pragma unroll
+    for (int c = j + 1; c < BS; ++c) asm volatile("" : "+v"(v[c]));
+#pragma unroll
+    for (int c = j + 2; c < BS; ++c) col[c] = nxt[c];
+    if (j + 1 < BS) col[j + 1] = 0.0f;  // entry j+1 is updated through lp instead
+    vp = vj;
+    lp = ln;
+  }
+#pragma unroll
+  for (int c = 0; c < BS; ++c) {
+    if (rowlane) sm.S[o + r][o + c] = c <= r ? v[c] : 0.0f;
+    else sm.X[o + c][o + r] = v[c];
+  }
+  // log-determinant share: sum of log L_jj over the block
+  double ls = rowlane ? log((double)diag) : 0.0;
+#pragma unroll
+  for (int w = 16; w >= 1; w >>= 1) ls += __shfl_xor(ls, w, 32);
+  if (lane == 0) sm.ldp[o / BS] = ls;
+  return bad;
+}
+
+// The products of a recursion level are h x h (h = 64 or 32) with k running
+// over h; each of the four waves owns one output tile: a 32 x 32 tile
+// (v_mfma_f32_32x32x2_f32) when h = 64, a 16 x 16 tile
+// (v_mfma_f32_16x16x4_f32) when h = 32.  geta(i, k) / getb(k, j) read LDS
+// with i, j relative to the h x h output.
+template <int H>
+struct LevelTile {
+  static constexpr int T = H / 2;  // tile edge
+  typedef typename std::conditional<H == 64, f32x16, f32x4>::type Acc;
+  static constexpr int NACC = H == 64 ? 16 : 4;
+
+  template <class GA, class GB>
+  __device__ __forceinline__ static Acc product(int wave, int lane, const GA& geta, const GB& getb) {
+    const int ti = wave >> 1, tj = wave & 1;
+    Acc acc;
+#pragma unroll
+    for (int r = 0; r < NACC; ++r) acc[r] = 0.0f;
+    if constexpr (H == 64) {
+      const int li = lane & 31, lk = lane >> 5;
+#pragma unroll 8
+      for (int k = 0; k < H; k += 2)
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(geta(ti * T + li, k + lk), getb(k + lk, tj * T + li),
+                                                   acc, 0, 0, 0);
+    } else {
+      const int li = lane & 15, lk = lane >> 4;
+#pragma unroll
+      for (int k = 0; k < H; k += 4)
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(geta(ti * T + li, k + lk), getb(k + lk, tj * T + li),
+                                                   acc, 0, 0, 0);
+    }
+    return acc;
+  }
+  // Output coordinates of accumulator element r of this lane.
+  __device__ __forceinline__ static int row(int wave, int r, int lane) {
+    return (wave >> 1) * T + (H == 64 ? 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3) : 4 * (lane >> 4) + r);
+  }
+  __device__ __forceinline__ static int col(int wave, int lane) {
+    return (wave & 1) * T + (H == 64 ? (lane & 31) : (lane & 15));
+  }
+};
+
+// Base block at (o, o) by wave 0; everyone waits.  Records the first failure.
+__device__ __forceinline__ void base_step(LeafLDS& sm, int o, int wave, int lane) {
+  if (wave == 0) {
+    const int b = base_block(sm, o, lane);
+    if (lane == 0 && b >= 0 && sm.bad < 0) sm.bad = o + b;
+  }
+  __syncthreads();
+}
+
+// Recursive cholinv of the block at (o, o) of size S (64 or 128, unrolled at
+// compile time); every wave takes every barrier.  Returns the failing column
+// or -1.
+template <int S>
+__device__ __forceinline__ int cholinv_lds(LeafLDS& sm, int o, int wave, int lane) {
+  constexpr int h = S / 2;
+  typedef LevelTile<h> LT;
+  if constexpr (h == BS) base_step(sm, o, wave, lane);
+  else cholinv_lds<h>(sm, o, wave, lane);
+  if (sm.bad >= 0) return sm.bad;
+  const int o2 = o + h;
+  const int oc = LT::col(wave, lane);
+  // L21 = A21 X11^T, kept in registers until every wave has read A21
+  const typename LT::Acc l21 = LT::product(wave, lane, [&](int i, int k) { return sm.S[o2 + i][o + k]; },
+                                           [&](int k, int j) { return sm.X[o + j][o + k]; });
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < LT::NACC; ++r) sm.S[o2 + LT::row(wave, r, lane)][o + oc] = l21[r];
+  __syncthreads();
+  // A22 -= L21 L21^T
+  {
+    const typename LT::Acc u = LT::product(wave, lane, [&](int i, int k) { return sm.S[o2 + i][o + k]; },
+                                           [&](int k, int j) { return sm.S[o2 + j][o + k]; });
+#pragma unroll
+    for (int r = 0; r < LT::NACC; ++r) sm.S[o2 + LT::row(wave, r, lane)][o2 + oc] -= u[r];
+  }
+  __syncthreads();
+  if constexpr (h == BS) base_step(sm, o2, wave, lane);
+  else cholinv_lds<h>(sm, o2, wave, lane);
+  if (sm.bad >= 0) return sm.bad;
+  // Y = L21 X11 -> T;  X21 = -X22 Y
+  {
+    const typename LT::Acc y = LT::product(wave, lane, [&](int i, int k) { return sm.S[o2 + i][o + k]; },
+                                           [&](int k, int j) { return sm.X[o + k][o + j]; });
+#pragma unroll
+    for (int r = 0; r < LT::NACC; ++r) sm.T[LT::row(wave, r, lane)][oc] = y[r];
+  }
+  __syncthreads();
+  {
+    const typename LT::Acc x21 = LT::product(wave, lane, [&](int i, int k) { return sm.X[o2 + i][o2 + k]; },
+                                             [&](int k, int j) { return sm.T[k][j]; });
+#pragma unroll
+    for (int r = 0; r < LT::NACC; ++r) sm.X[o2 + LT::row(wave, r, lane)][o + oc] = -x21[r];
+  }
+  __syncthreads();
+  return -1;
+}
 
 __global__ __launch_bounds__(256) void k_chol_leaf(const float* __restrict__ Lblk,
                                                    float* __restrict__ Liblk, int64_t ld, int b,
                                                    int64_t pivot_base, double* logdet, int slot,
                                                    int iteration, int side, int* st) {
   if (ff_halted(st)) return;
-  __shared__ __align__(16) float Pn[NT][TB][NB + 4];  // panel p = block column p of L, transposed
-  __shared__ float Ld[NT][TB][TB + 1];  // inverses of the diagonal 8 x 8 blocks
-  __shared__ __align__(16) float Xr[2][TB][NB + 4];  // finished block row of L^-1
-  __shared__ double ldp[NT];
-  __shared__ int bad;
-  const int tid = threadIdx.x;
-  const int ti = tid & 15, tj = tid >> 4;
-  const bool lower = ti >= tj;
-  float blk[TB][TB];
+  __shared__ LeafLDS sm;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int j = tid & (NB - 1), i0 = tid >> 7;
+  if (b == NB && (ld & 3) == 0 && (reinterpret_cast<uintptr_t>(Lblk) & 15) == 0) {
+    // full block: thread (r, q) moves float4 q of rows r, r + 8, ...; all
+    // sixteen loads are in flight before the first is used
+    const int q = tid & 31, r = tid >> 5;
+    float4 v[NB / 8];
 #pragma unroll
-  for (int r = 0; r < TB; ++r)
+    for (int t = 0; t < NB / 8; ++t)
+      v[t] = *reinterpret_cast<const float4*>(Lblk + (int64_t)(r + 8 * t) * ld + 4 * q);
 #pragma unroll
-    for (int c = 0; c < TB; ++c) {
-      const int i = ti * TB + r, j = tj * TB + c;
-      float v = 0.0f;
-      if (lower) {
-        if (i < b && j < b) v = j <= i ? Lblk[(int64_t)i * ld + j] : 0.0f;
-        else if (i == j) v = 1.0f;
-      }
-      blk[r][c] = v;
+    for (int t = 0; t < NB / 8; ++t) {
+      const int i = r + 8 * t, c = 4 * q;
+      sm.S[i][c + 0] = c + 0 <= i ? v[t].x : 0.0f;
+      sm.S[i][c + 1] = c + 1 <= i ? v[t].y : 0.0f;
+      sm.S[i][c + 2] = c + 2 <= i ? v[t].z : 0.0f;
+      sm.S[i][c + 3] = c + 3 <= i ? v[t].w : 0.0f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sm.X[i][c + e] = 0.0f;
     }
-  if (tid == 0) bad = -1;
-  __syncthreads();
-
-  // ---------------------------------------------------------- factorisation
-  for (int p = 0; p < NT; ++p) {
-    if (tj == p) {  // the 16 lanes of block column p; (p, p) is lane (17 p) mod 64
-      const int dl = (17 * p) & 63;
-      bool ok = true;
+  } else {
+    // ragged block (b < 128), padded with the identity: thread (i0, j) moves
+    // rows i0, i0 + 2, ... of column j, from clamped (always valid) addresses
 #pragma unroll
-      for (int c = 0; c < TB; ++c) {
-        const float d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(blk[c][c]), dl));
-        if (!(d > 0.0f) || !(d < INFINITY)) ok = false;
-        const float s = sqrtf(d), rs = 1.0f / s;
+    for (int half = 0; half < 2; ++half) {
+      float v[NB / 4];
 #pragma unroll
-        for (int r = 0; r < TB; ++r) {
-          if (ti == p) blk[r][c] = r > c ? blk[r][c] * rs : (r == c ? s : 0.0f);
-          else blk[r][c] *= rs;
-        }
-#pragma unroll
-        for (int c2 = c + 1; c2 < TB; ++c2) {
-          const float lc =
-              __int_as_float(__builtin_amdgcn_readlane(__float_as_int(blk[c2][c]), dl));
-#pragma unroll
-          for (int r = 0; r < TB; ++r) blk[r][c2] -= blk[r][c] * lc;
-        }
-      }
-      if (!ok && ti == p) {  // first failing column of this block
-        int c0 = 0;
-        for (; c0 < TB; ++c0)
-          if (!(blk[c0][c0] > 0.0f) || !(blk[c0][c0] < INFINITY)) break;
-        bad = p * TB + (c0 < TB ? c0 : 0);
-      }
-      if (ti >= p) {
-#pragma unroll
-        for (int c = 0; c < TB; ++c) {
-          f32x4* dst = reinterpret_cast<f32x4*>(&Pn[p][c][ti * TB]);
-          dst[0] = f32x4{blk[0][c], blk[1][c], blk[2][c], blk[3][c]};
-          dst[1] = f32x4{blk[4][c], blk[5][c], blk[6][c], blk[7][c]};
-        }
-      }
-    }
-    __syncthreads();
-    if (bad >= 0) break;
-    if (tj > p && lower) {
-      float a[TB][TB], bb[TB][TB];  // a[r][k] = L(8 ti + r, 8 p + k), bb likewise for tj
-#pragma unroll
-      for (int k = 0; k < TB; ++k) {
-        const f32x4* sa = reinterpret_cast<const f32x4*>(&Pn[p][k][ti * TB]);
-        const f32x4* sb = reinterpret_cast<const f32x4*>(&Pn[p][k][tj * TB]);
-        const f32x4 a0 = sa[0], a1 = sa[1], b0 = sb[0], b1 = sb[1];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          a[q][k] = a0[q];
-          a[q + 4][k] = a1[q];
-          bb[q][k] = b0[q];
-          bb[q + 4][k] = b1[q];
-        }
+      for (int t = 0; t < NB / 4; ++t) {
+        const int i = i0 + 2 * (half * (NB / 4) + t);
+        const float x = Lblk[(int64_t)min(i, b - 1) * ld + min(j, b - 1)];
+        v[t] = (i < b && j <= i) ? x : (i == j ? 1.0f : 0.0f);
       }
 #pragma unroll
-      for (int r = 0; r < TB; ++r)
-#pragma unroll
-        for (int c = 0; c < TB; ++c) {
-          float acc = blk[r][c];
-#pragma unroll
-          for (int k = 0; k < TB; ++k) acc -= a[r][k] * bb[c][k];
-          blk[r][c] = acc;
-        }
+      for (int t = 0; t < NB / 4; ++t) {
+        const int i = i0 + 2 * (half * (NB / 4) + t);
+        sm.S[i][j] = v[t];
+        sm.X[i][j] = 0.0f;
+      }
     }
   }
+  if (tid == 0) sm.bad = -1;
+  __syncthreads();
+  const int bad = cholinv_lds<NB>(sm, 0, wave, lane);
   if (bad >= 0) {
     if (tid == 0) {
       st[1] = side;
@@ -130,98 +269,15 @@ __global__ __launch_bounds__(256) void k_chol_leaf(const float* __restrict__ Lbl
     }
     return;
   }
-  // Diagonal blocks, in parallel: log-determinant share and 8 x 8 inverse.
-  if (ti == tj) {
-    double lsum = 0.0;
-#pragma unroll
-    for (int c = 0; c < TB; ++c) lsum += log((double)blk[c][c]);
-    ldp[ti] = lsum;
-    float inv[TB][TB];
-#pragma unroll
-    for (int c = 0; c < TB; ++c) {
-#pragma unroll
-      for (int r = 0; r < TB; ++r) {
-        float acc = r == c ? 1.0f : 0.0f;
-#pragma unroll
-        for (int k = 0; k < TB; ++k)
-          if (k >= c && k < r) acc -= blk[r][k] * inv[k][c];
-        inv[r][c] = r >= c ? acc / blk[r][r] : 0.0f;
-      }
-    }
-#pragma unroll
-    for (int r = 0; r < TB; ++r)
-#pragma unroll
-      for (int c = 0; c < TB; ++c) Ld[ti][r][c] = inv[r][c];
-  }
-  __syncthreads();
   if (tid == 0) {
     double s = 0.0;
-    for (int p = 0; p < NT; ++p) s += ldp[p];
+    for (int p = 0; p < NB / BS; ++p) s += sm.ldp[p];
     logdet[slot] = s;
   }
-
-  // ---------------------------------------------------------------- inverse
-  // acc(ti, tj) = E - sum_{k < p} L(ti, k) X(k, tj); block row p is final at step p.
-#pragma unroll
-  for (int r = 0; r < TB; ++r)
-#pragma unroll
-    for (int c = 0; c < TB; ++c) blk[r][c] = (lower && ti == tj && r == c) ? 1.0f : 0.0f;
-  for (int p = 0; p < NT; ++p) {
-    const int buf = p & 1;
-    if (ti == p && tj <= p) {
-      float x[TB][TB];
-#pragma unroll
-      for (int r = 0; r < TB; ++r)
-#pragma unroll
-        for (int c = 0; c < TB; ++c) {
-          float acc = 0.0f;
-#pragma unroll
-          for (int k = 0; k < TB; ++k) acc += Ld[p][r][k] * blk[k][c];
-          x[r][c] = acc;
-        }
-#pragma unroll
-      for (int r = 0; r < TB; ++r) {
-#pragma unroll
-        for (int c = 0; c < TB; ++c) blk[r][c] = x[r][c];
-        f32x4* dst = reinterpret_cast<f32x4*>(&Xr[buf][r][tj * TB]);
-        dst[0] = f32x4{x[r][0], x[r][1], x[r][2], x[r][3]};
-        dst[1] = f32x4{x[r][4], x[r][5], x[r][6], x[r][7]};
-      }
-    }
-    __syncthreads();
-    if (ti > p && tj <= p) {
-      float a[TB][TB], xb[TB][TB];
-#pragma unroll
-      for (int k = 0; k < TB; ++k) {
-        const f32x4* sa = reinterpret_cast<const f32x4*>(&Pn[p][k][ti * TB]);
-        const f32x4* sx = reinterpret_cast<const f32x4*>(&Xr[buf][k][tj * TB]);
-        const f32x4 a0 = sa[0], a1 = sa[1], x0 = sx[0], x1 = sx[1];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          a[q][k] = a0[q];
-          a[q + 4][k] = a1[q];
-          xb[k][q] = x0[q];
-          xb[k][q + 4] = x1[q];
-        }
-      }
-#pragma unroll
-      for (int r = 0; r < TB; ++r)
-#pragma unroll
-        for (int c = 0; c < TB; ++c) {
-          float acc = blk[r][c];
-#pragma unroll
-          for (int k = 0; k < TB; ++k) acc -= a[r][k] * xb[k][c];
-          blk[r][c] = acc;
-        }
-    }
+  if (j < b) {
+#pragma unroll 8
+    for (int i = i0; i < b; i += 2) Liblk[(int64_t)i * ld + j] = j <= i ? sm.X[i][j] : 0.0f;
   }
-#pragma unroll
-  for (int r = 0; r < TB; ++r)
-#pragma unroll
-    for (int c = 0; c < TB; ++c) {
-      const int i = ti * TB + r, j = tj * TB + c;
-      if (i < b && j < b) Liblk[(int64_t)i * ld + j] = (lower && j <= i) ? blk[r][c] : 0.0f;
-    }
 }
 
 }  // namespace

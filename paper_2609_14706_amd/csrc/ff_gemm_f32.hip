@@ -3,8 +3,10 @@
 // Used wherever the iteration needs fp32 products: the blocked Cholesky and
 // triangular inverse of the factors, the whole fp32 sample path (whitening
 // and symmetric product), and the Kronecker application.  128 x 128 output
-// tiles, four waves of 64 x 64 (2 x 2 matrix-core tiles), 16-wide k slices
-// staged through double-buffered LDS.  Any shape and either operand
+// tiles, four waves of 64 x 64 (2 x 2 matrix-core tiles), 32-wide k slices
+// staged through double-buffered LDS; when fewer than 256 such tiles would be
+// launched, 64 x 64 tiles (one 32 x 32 matrix-core tile per wave) with 64-wide
+// k slices.  Any shape and either operand
 // transpose; k ranges can be clipped to the non-zero triangle of a
 // triangular operand, k can run over segments (the stacked samples), and k
 // can be split over the grid into partial outputs.  When every operand is
@@ -16,30 +18,38 @@
 namespace ff {
 namespace {
 
-constexpr int BT = 128;  // tile rows / cols
-constexpr int BK = 16;   // k per slice
-constexpr int LDP = BT + 4;
+constexpr int LDPMAX = 128 + 4;
 
+// k per LDS slice: 32 for 128 x 128 tiles, 64 for 64 x 64 tiles (the small
+// products of the factorisation are latency bound: fewer, larger slices).
+template <int BT>
+constexpr int slice_k() { return BT == 128 ? 32 : 64; }
+
+// Offset of k in a k axis made of segments of kseg, seg apart (kseg == 0:
+// one contiguous axis, no division).
 __device__ __forceinline__ int64_t seg_off(int64_t k, int64_t kseg, int64_t seg) {
-  return (k / kseg) * seg + (k % kseg);
+  return kseg ? (k / kseg) * seg + (k % kseg) : k;
 }
 
 // One operand slice: 128 "outer" indices (rows of op(A) or columns of op(B))
 // x 16 k.  KMAJ: the operand is contiguous along k (element (o, k) at
 // P[o * ld + koff(k)]); otherwise contiguous along o (at P[koff(k) * ld + o]).
-// Each thread fetches two 4-element groups; slice[k][o] is written to LDS.
+// Each thread fetches NQ 4-element groups; slice[k][o] is written to LDS.
 // FAST: the whole slice is in bounds and 16-byte vectors can be used.
-template <bool KMAJ, bool FAST>
+template <int BT, bool KMAJ, bool FAST>
 struct SliceLoader {
-  f32x4 v[2];
+  static constexpr int BK = slice_k<BT>();
+  static constexpr int NQ = BT * BK / 4 / 256;  // 4-element groups per thread
+  static constexpr int OQ = BT / 4;             // 4-element groups per k row (non-k-major)
+  f32x4 v[NQ];
   __device__ __forceinline__ void load(const float* P, int64_t ld, int64_t o0, int64_t olim,
                                        int64_t k0, int64_t khi, int64_t kseg, int64_t seg,
                                        int tid) {
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
+    for (int q = 0; q < NQ; ++q) {
       const int idx = tid + 256 * q;
-      const int o = KMAJ ? idx >> 2 : (idx & 31) * 4;
-      const int k = KMAJ ? (idx & 3) * 4 : idx >> 5;
+      const int o = KMAJ ? idx / (BK / 4) : (idx % OQ) * 4;
+      const int k = KMAJ ? (idx % (BK / 4)) * 4 : idx / OQ;
       const int64_t go = o0 + o, gk = k0 + k;
       if (FAST) {
         const int64_t ko = seg_off(gk, kseg, seg);
@@ -59,36 +69,39 @@ struct SliceLoader {
       }
     }
   }
-  __device__ __forceinline__ void store(float (*S)[LDP], int tid) const {
+  __device__ __forceinline__ void store(float (*S)[BT + 4], int tid) const {
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
+    for (int q = 0; q < NQ; ++q) {
       const int idx = tid + 256 * q;
       if (KMAJ) {
-        const int o = idx >> 2, k = (idx & 3) * 4;
+        const int o = idx / (BK / 4), k = (idx % (BK / 4)) * 4;
 #pragma unroll
         for (int e = 0; e < 4; ++e) S[k + e][o] = v[q][e];
       } else {
-        const int k = idx >> 5, o = (idx & 31) * 4;
+        const int k = idx / OQ, o = (idx % OQ) * 4;
         *reinterpret_cast<f32x4*>(&S[k][o]) = v[q];
       }
     }
   }
 };
 
+template <int BT>
 struct TileLDS {
-  float a[2][BK][LDP];
-  float b[2][BK][LDP];
+  float a[2][slice_k<BT>()][BT + 4];
+  float b[2][slice_k<BT>()][BT + 4];
 };
 
-// acc += op(A)[i0.., klo..khi) op(B)[klo..khi), j0..) for one 128 x 128 tile.
-template <bool AK, bool BKM, bool FAST>
+// acc += op(A)[i0.., klo..khi) op(B)[klo..khi), j0..) for one BT x BT tile
+// (each wave a (BT/2) x (BT/2) quadrant of MT x MT 32 x 32 matrix-core tiles).
+template <int BT, bool AK, bool BKM, bool FAST>
 __device__ __forceinline__ void tile_product(const GemmF32& p, const float* A, const float* B,
                                              int64_t i0, int64_t j0, int64_t klo, int64_t khi,
-                                             TileLDS& sm, f32x16 (&acc)[2][2]) {
+                                             TileLDS<BT>& sm, f32x16 (&acc)[BT / 64][BT / 64]) {
+  constexpr int MT = BT / 64, BK = slice_k<BT>();
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
-  SliceLoader<AK, FAST> la;
-  SliceLoader<BKM, FAST> lb;
+  SliceLoader<BT, AK, FAST> la;
+  SliceLoader<BT, BKM, FAST> lb;
   la.load(A, p.lda, i0, p.M, klo, khi, p.kseg, p.segA, tid);
   lb.load(B, p.ldb, j0, p.N, klo, khi, p.kseg, p.segB, tid);
   la.store(sm.a[0], tid);
@@ -105,16 +118,16 @@ __device__ __forceinline__ void tile_product(const GemmF32& p, const float* A, c
 #pragma unroll
     for (int s = 0; s < BK / 2; ++s) {
       const int kr = 2 * s + (lane >> 5);
-      float fa[2], fb[2];
+      float fa[MT], fb[MT];
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        fa[t] = sm.a[cur][kr][wm * 64 + t * 32 + (lane & 31)];
-        fb[t] = sm.b[cur][kr][wn * 64 + t * 32 + (lane & 31)];
+      for (int t = 0; t < MT; ++t) {
+        fa[t] = sm.a[cur][kr][wm * (BT / 2) + t * 32 + (lane & 31)];
+        fb[t] = sm.b[cur][kr][wn * (BT / 2) + t * 32 + (lane & 31)];
       }
 #pragma unroll
-      for (int a = 0; a < 2; ++a)
+      for (int a = 0; a < MT; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
+        for (int b = 0; b < MT; ++b)
           acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[a], fb[b], acc[a][b], 0, 0, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
@@ -127,8 +140,9 @@ __device__ __forceinline__ void tile_product(const GemmF32& p, const float* A, c
   }
 }
 
-template <int TA, int TBT, bool VEC>
+template <int BT, int TA, int TBT, bool VEC>
 __global__ __launch_bounds__(256) void k_gemm_f32(GemmF32 p) {
+  constexpr int MT = BT / 64, BK = slice_k<BT>();
   if (ff_halted(p.st)) return;
   const int64_t i0 = (int64_t)blockIdx.x * BT, j0 = (int64_t)blockIdx.y * BT;
   if ((p.flags & kCLower) && j0 > i0 + BT - 1) return;
@@ -151,31 +165,31 @@ __global__ __launch_bounds__(256) void k_gemm_f32(GemmF32 p) {
     B += (int64_t)blockIdx.z * p.sB;
     C += (int64_t)blockIdx.z * p.sC;
   }
-  __shared__ __align__(16) TileLDS sm;
+  __shared__ __align__(16) TileLDS<BT> sm;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  f32x16 acc[2][2];
+  f32x16 acc[MT][MT];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < MT; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < MT; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
   if (klo < khi) {
     const bool fast = VEC && i0 + BT <= p.M && j0 + BT <= p.N && (khi - klo) % BK == 0;
-    if (fast) tile_product<TA == 0, TBT != 0, VEC>(p, A, B, i0, j0, klo, khi, sm, acc);
-    else tile_product<TA == 0, TBT != 0, false>(p, A, B, i0, j0, klo, khi, sm, acc);
+    if (fast) tile_product<BT, TA == 0, TBT != 0, VEC>(p, A, B, i0, j0, klo, khi, sm, acc);
+    else tile_product<BT, TA == 0, TBT != 0, false>(p, A, B, i0, j0, klo, khi, sm, acc);
   }
   const bool lower = (p.flags & kCLower) != 0;
   const bool use_beta = p.ksplit <= 1 && p.beta != 0.0f;
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < MT; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < MT; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int64_t i = i0 + wm * 64 + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        const int64_t j = j0 + wn * 64 + b * 32 + (lane & 31);
+        const int64_t i = i0 + wm * (BT / 2) + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        const int64_t j = j0 + wn * (BT / 2) + b * 32 + (lane & 31);
         if (i < p.M && j < p.N && (!lower || i >= j)) {
           float v = p.alpha * acc[a][b][r];
           if (use_beta) v += p.beta * C[i * p.ldc + j];
@@ -203,30 +217,41 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 }  // namespace
 
+template <int BT>
+hipError_t launch_tiles(const GemmF32& p, int batch, bool vec, hipStream_t s) {
+  const int64_t gx = (p.M + BT - 1) / BT, gy = (p.N + BT - 1) / BT;
+  const int gz = p.ksplit > 1 ? p.ksplit : batch;
+  if (gx > 0x7fffffff || gy > 65535 || gz > 65535) return hipErrorInvalidValue;
+  const dim3 grid((uint32_t)gx, (uint32_t)gy, (uint32_t)gz);
+  const int sel = (p.transA ? 1 : 0) | (p.transB ? 2 : 0) | (vec ? 4 : 0);
+  switch (sel) {
+    case 0: hipLaunchKernelGGL((k_gemm_f32<BT, 0, 0, false>), grid, dim3(256), 0, s, p); break;
+    case 1: hipLaunchKernelGGL((k_gemm_f32<BT, 1, 0, false>), grid, dim3(256), 0, s, p); break;
+    case 2: hipLaunchKernelGGL((k_gemm_f32<BT, 0, 1, false>), grid, dim3(256), 0, s, p); break;
+    case 3: hipLaunchKernelGGL((k_gemm_f32<BT, 1, 1, false>), grid, dim3(256), 0, s, p); break;
+    case 4: hipLaunchKernelGGL((k_gemm_f32<BT, 0, 0, true>), grid, dim3(256), 0, s, p); break;
+    case 5: hipLaunchKernelGGL((k_gemm_f32<BT, 1, 0, true>), grid, dim3(256), 0, s, p); break;
+    case 6: hipLaunchKernelGGL((k_gemm_f32<BT, 0, 1, true>), grid, dim3(256), 0, s, p); break;
+    default: hipLaunchKernelGGL((k_gemm_f32<BT, 1, 1, true>), grid, dim3(256), 0, s, p); break;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm_f32(const GemmF32& p, int batch, hipStream_t s) {
   if (p.M < 0 || p.N < 0 || p.K < 0 || batch < 1 || p.kseg < 1) return hipErrorInvalidValue;
   if (p.ksplit > 1 && batch != 1) return hipErrorInvalidValue;
   if (p.M == 0 || p.N == 0) return hipSuccess;
-  const int64_t gx = (p.M + BT - 1) / BT, gy = (p.N + BT - 1) / BT;
-  const int gz = p.ksplit > 1 ? p.ksplit : batch;
-  if (gx > 0x7fffffff || gy > 65535 || gz > 65535) return hipErrorInvalidValue;
   const bool segmented = p.kseg < p.K;
   const bool vec = aligned16(p.A) && aligned16(p.B) && p.lda % 4 == 0 && p.ldb % 4 == 0 &&
                    (batch == 1 || (p.sA % 4 == 0 && p.sB % 4 == 0)) &&
                    (!segmented || (p.kseg % 4 == 0 && p.segA % 4 == 0 && p.segB % 4 == 0));
-  const dim3 grid((uint32_t)gx, (uint32_t)gy, (uint32_t)gz);
-  const int sel = (p.transA ? 1 : 0) | (p.transB ? 2 : 0) | (vec ? 4 : 0);
-  switch (sel) {
-    case 0: hipLaunchKernelGGL((k_gemm_f32<0, 0, false>), grid, dim3(256), 0, s, p); break;
-    case 1: hipLaunchKernelGGL((k_gemm_f32<1, 0, false>), grid, dim3(256), 0, s, p); break;
-    case 2: hipLaunchKernelGGL((k_gemm_f32<0, 1, false>), grid, dim3(256), 0, s, p); break;
-    case 3: hipLaunchKernelGGL((k_gemm_f32<1, 1, false>), grid, dim3(256), 0, s, p); break;
-    case 4: hipLaunchKernelGGL((k_gemm_f32<0, 0, true>), grid, dim3(256), 0, s, p); break;
-    case 5: hipLaunchKernelGGL((k_gemm_f32<1, 0, true>), grid, dim3(256), 0, s, p); break;
-    case 6: hipLaunchKernelGGL((k_gemm_f32<0, 1, true>), grid, dim3(256), 0, s, p); break;
-    default: hipLaunchKernelGGL((k_gemm_f32<1, 1, true>), grid, dim3(256), 0, s, p); break;
-  }
-  return hipGetLastError();
+  // 128 x 128 tiles when they fill the GPU, 64 x 64 (four times the workgroups) otherwise.
+  const int64_t big_tiles = ((p.M + 127) / 128) * ((p.N + 127) / 128) *
+                            (p.ksplit > 1 ? p.ksplit : batch);
+  GemmF32 q = p;
+  if (!segmented) q.kseg = 0;  // plain k axis: the kernels skip the segment arithmetic
+  if (big_tiles >= 256) return launch_tiles<128>(q, batch, vec, s);
+  return launch_tiles<64>(q, batch, vec, s);
 }
 
 hipError_t launch_reduce_rowmajor(const float* P, int splits, int64_t dim_p, float* F,
