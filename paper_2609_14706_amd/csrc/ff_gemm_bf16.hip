@@ -35,14 +35,19 @@ typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 typedef __attribute__((address_space(3))) void lds_void;
 
 // Stage layout: chunk position P = 4 row + slot; slot s of row r holds the
-// 16-byte k chunk c = s ^ ((r >> 1) & 3), so that the fragment reads of 8
-// consecutive rows fall on distinct banks.
+// 16-byte k chunk c = s ^ swz(r).  A fragment read moves one chunk of each
+// of 32 consecutive rows; the LDS serves it 16 lanes (16 rows, 256 bytes) at
+// a time across its 64 banks, so the 16 chunks must cover all 16 positions
+// modulo 16, i.e. (r mod 4, slot) must differ across 16 consecutive rows.
+// swz(r) = ((r >> 1) & 3) ^ ((r >> 3) & 1) gives that, and also keeps any 8
+// consecutive rows on distinct 128-byte bank groups.
 struct __align__(16) Ring {
   u32x4 a[NSTAGE][CHUNKS];
   u32x4 b[NSTAGE][CHUNKS];
 };
 
-__device__ __forceinline__ int chunk_pos(int row, int c) { return row * 4 + (c ^ ((row >> 1) & 3)); }
+__device__ __forceinline__ int swz(int row) { return ((row >> 1) & 3) ^ ((row >> 3) & 1); }
+__device__ __forceinline__ int chunk_pos(int row, int c) { return row * 4 + (c ^ swz(row)); }
 
 // vmcnt(N) with the other counters left alone (gfx9 encoding).
 template <int N>
@@ -60,7 +65,7 @@ __device__ __forceinline__ void chunk_offsets(int wave, int lane, uint32_t ld, u
   for (int q = 0; q < 4; ++q) {
     const int P = (q * 4 + wave) * 64 + lane;
     const int row = P >> 2, slot = P & 3;
-    const int c = slot ^ ((row >> 1) & 3);
+    const int c = slot ^ swz(row);
     off[q] = (uint32_t)row * ld + (uint32_t)c * 8u;
   }
 }
