@@ -107,6 +107,19 @@ __device__ __forceinline__ void tile_product(const GemmF32& p, const float* A, c
   la.store(sm.a[0], tid);
   lb.store(sm.b[0], tid);
   __syncthreads();
+  // Two-level accumulation: the products of up to CHUNK slices go into a
+  // fresh accumulator that is then added to acc.  Long k ranges (the
+  // stacked samples, hundreds of thousands deep) thus round each output
+  // element about CHUNK * BK / 2 + K / (CHUNK * BK) times instead of K / 2.
+  constexpr int CHUNK = 8;
+  f32x16 loc[MT][MT];
+#pragma unroll
+  for (int a = 0; a < MT; ++a)
+#pragma unroll
+    for (int b = 0; b < MT; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) loc[a][b][r] = 0.0f;
+  int cnt = 0;
   int cur = 0;
   for (int64_t k0 = klo; k0 < khi; k0 += BK) {
     const bool more = k0 + BK < khi;
@@ -128,7 +141,18 @@ __device__ __forceinline__ void tile_product(const GemmF32& p, const float* A, c
       for (int a = 0; a < MT; ++a)
 #pragma unroll
         for (int b = 0; b < MT; ++b)
-          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[a], fb[b], acc[a][b], 0, 0, 0);
+          loc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[a], fb[b], loc[a][b], 0, 0, 0);
+    }
+    if (++cnt == CHUNK || !more) {
+#pragma unroll
+      for (int a = 0; a < MT; ++a)
+#pragma unroll
+        for (int b = 0; b < MT; ++b) {
+          acc[a][b] += loc[a][b];
+#pragma unroll
+          for (int r = 0; r < 16; ++r) loc[a][b][r] = 0.0f;
+        }
+      cnt = 0;
     }
     __builtin_amdgcn_sched_barrier(0);
     if (more) {

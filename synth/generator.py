@@ -222,11 +222,16 @@ def generate_device(w: Workload, seed: int | None = None, *, device="cuda",
     tdtype = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     G = torch.empty((len(idx), w.m, w.n), dtype=tdtype, device=dev)
 
-    with ThreadPoolExecutor(max(1, threads)) as ex:
-        futs = [ex.submit(_draw_sample_randoms, w, seed, i) for i in idx]
-        for k, f in enumerate(futs):
-            Z, U, V = f.result()
-            futs[k] = None
+    nthr = max(1, threads)
+    with ThreadPoolExecutor(nthr) as ex:
+        # at most 2 * threads draws in flight: bounded host memory on large layers
+        futs = {}
+        for k in range(min(len(idx), 2 * nthr)):
+            futs[k] = ex.submit(_draw_sample_randoms, w, seed, idx[k])
+        for k in range(len(idx)):
+            Z, U, V = futs.pop(k).result()
+            if k + 2 * nthr < len(idx):
+                futs[k + 2 * nthr] = ex.submit(_draw_sample_randoms, w, seed, idx[k + 2 * nthr])
             Zd = torch.from_numpy(Z).to(dev, non_blocking=False).double()
             X = SB @ Zd @ SAt
             del Zd
