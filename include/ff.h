@@ -27,8 +27,9 @@
  *  - Device pointers must be 256-byte aligned where stated, otherwise
  *    16-byte aligned.  All matrices are dense row-major.
  *  - Work is enqueued on cfg.stream (a hipStream_t; NULL = default stream).
- *    ff_iterate, ff_factors(on_host=1) and ff_kron_apply synchronise that
- *    stream once before returning; the others return without waiting.
+ *    ff_iterate, ff_factors(on_host=1), ff_kron_apply and ff_objective
+ *    synchronise that stream once before returning; the others return
+ *    without waiting.
  *  - A handle is not thread-safe; distinct handles are independent.  The
  *    device that is current at ff_init must be current for every later
  *    call on the handle.
@@ -135,6 +136,24 @@ ff_status ff_factors(ff_handle h, float* A, float* B, int on_host);
  * FF_ERR_HIP. */
 ff_status ff_kron_apply(ff_handle h, const float* X, float* Y, int64_t batch,
                         ff_apply_mode mode);
+
+/* The Kronecker-Hessian mismatch objective of the factors A (n x n) and
+ * B (m x m), Section 4: with H = (1/N) sum_i vec(G_i) vec(G_i)^T the samples'
+ * second moment, the mismatch factor Phi(H, A (x) B) is the ratio of
+ * tr(H (A (x) B)^-1) / (m n) to |H|^(1/(m n)) |A|^(-1/n) |B|^(-1/m).  *psi
+ * receives its log without the H-only term,
+ *   psi = log( (1/(N m n)) sum_i tr(B^-1 G_i A^-1 G_i^T) ) + log|A|/n + log|B|/m
+ *       = log Phi(H, A (x) B) + log|H| / (m n),
+ * invariant under A -> c A, B -> B / c and minimised by the flip-flop fixed
+ * point (Section 5).  A and B are DEVICE fp32 row-major symmetric positive
+ * definite matrices (lower triangles read); either may be NULL to use the
+ * handle's current factor.  The trace term runs through the handle's path
+ * (bf16 whitening on a bf16 handle), the log-determinants come from its fp32
+ * Cholesky factorisations.  Synchronises the stream.  The handle's factors
+ * are untouched; the next ff_iterate refactorises them.
+ * Errors: FF_ERR_INVALID_ARG, FF_ERR_NOT_SPD (A or B not positive definite),
+ * FF_ERR_HIP. */
+ff_status ff_objective(ff_handle h, const float* A, const float* B, double* psi);
 
 /* Release the handle (host memory only; waits for the handle's stream).
  * NULL is accepted. */

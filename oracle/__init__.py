@@ -9,11 +9,11 @@ Every function cites the passage of the paper it follows.  Where the paper
 leaves a choice open, the reading taken is stated in the docstring.
 """
 from .flipflop import (FlipFlopResult, NotSPDError, as_f64_samples, half_step_B, half_step_B_rows,
-                       half_step_A, normalise, damp, flipflop, loglik)
+                       half_step_A, normalise, damp, flipflop, loglik, objective)
 from .metrics import kron_rel_error, kron_rel_error_scale_free, trace_identity
 from .kron import kron_apply, mismatch_factor
 
 __all__ = ["FlipFlopResult", "NotSPDError", "as_f64_samples", "half_step_B", "half_step_B_rows",
-           "half_step_A", "normalise", "damp", "flipflop", "loglik",
+           "half_step_A", "normalise", "damp", "flipflop", "loglik", "objective",
            "kron_rel_error", "kron_rel_error_scale_free", "trace_identity",
            "kron_apply", "mismatch_factor"]

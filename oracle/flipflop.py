@@ -169,6 +169,32 @@ def _loglik(G, A, B):
     return -0.5 * N * (m * logdetA + n * logdetB) - 0.5 * quad - 0.5 * N * m * n * LOG_2PI
 
 
+def objective(G, A, B):
+    """The mismatch objective of Section 4 without its H-only term.
+
+    With H = (1/N) sum_i vec(G_i) vec(G_i)^T, the mismatch factor is
+    Phi(H, A (x) B) = [tr(H (A (x) B)^-1) / mn] / [|H|^(1/mn) |A (x) B|^(-1/mn)];
+    tr(H (A (x) B)^-1) = (1/N) sum_i tr(B^-1 G_i A^-1 G_i^T) (column-major vec)
+    and |A (x) B|^(1/mn) = |A|^(1/n) |B|^(1/m), so this returns
+    psi = log((1/(N m n)) sum_i tr(B^-1 G_i A^-1 G_i^T)) + log|A|/n + log|B|/m
+        = log Phi + log|H| / (m n),
+    which stays finite when H is singular (N < m n).  Each sample's trace is
+    taken directly with two Cholesky solves, as in ``loglik``.
+    """
+    G = as_f64_samples(G)
+    N, m, n = G.shape
+    with blas_threads(m, n):
+        cA = _chol(A, "A", -1)
+        cB = _chol(B, "B", -1)
+        logdetA = 2.0 * np.sum(np.log(np.diag(cA[0])))
+        logdetB = 2.0 * np.sum(np.log(np.diag(cB[0])))
+        quad = 0.0
+        for Gi in G:
+            quad += np.trace(sla.cho_solve(cB, Gi @ sla.cho_solve(cA, Gi.T, check_finite=False),
+                                           check_finite=False))
+    return float(np.log(quad / (N * m * n)) + logdetA / n + logdetB / m)
+
+
 @dataclass
 class FlipFlopResult:
     A: np.ndarray

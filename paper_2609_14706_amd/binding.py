@@ -59,6 +59,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "ff_iterate": (st, [H, ctypes.c_int, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_double)]),
         "ff_factors": (st, [H, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int]),
         "ff_kron_apply": (st, [H, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int]),
+        "ff_objective": (st, [H, ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(ctypes.c_double)]),
         "ff_destroy": (st, [H]),
         "ff_set_timing": (st, [H, ctypes.c_int]),
         "ff_kernel_timing": (st, [H, ctypes.c_int, ctypes.POINTER(ctypes.c_int64),
@@ -132,6 +133,12 @@ def ff_factors(h, A_ptr: int, B_ptr: int, on_host: int):
 
 def ff_kron_apply(h, X_ptr: int, Y_ptr: int, batch: int, mode: int):
     _check(load_library().ff_kron_apply(h, X_ptr, Y_ptr, batch, mode))
+
+
+def ff_objective(h, A_ptr, B_ptr) -> float:
+    out = ctypes.c_double(0.0)
+    _check(load_library().ff_objective(h, A_ptr, B_ptr, ctypes.byref(out)))
+    return out.value
 
 
 def ff_destroy(h):
@@ -248,6 +255,24 @@ class FlipFlop:
         ff_kron_apply(self.h, X.data_ptr(), Y.data_ptr(), X.shape[0],
                       FF_APPLY_INV if inverse else FF_APPLY)
         return Y[0] if squeeze else Y
+
+    def objective(self, A=None, B=None) -> float:
+        """log Phi(H, A (x) B) + log|H| / (m n) of the given factors (default:
+        the current ones); see ff_objective."""
+        import torch
+        keep = []
+
+        def ptr(M, dim):
+            if M is None:
+                return None
+            M = M.to(device=self.device, dtype=torch.float32).contiguous()
+            if tuple(M.shape) != (dim, dim):
+                raise ValueError(f"factor must be {dim} x {dim}")
+            keep.append(M)
+            return M.data_ptr()
+        pa, pb = ptr(A, self.n), ptr(B, self.m)
+        torch.cuda.current_stream(self.device).synchronize()
+        return ff_objective(self.h, pa, pb)
 
     def set_timing(self, enable: bool = True):
         ff_set_timing(self.h, enable)

@@ -126,6 +126,42 @@ __global__ __launch_bounds__(256) void k_loglik(const double* slotsA, int nA, co
   *ll_out = -0.5 * N * (m * la + n * lb) - 0.5 * N * m * n * (1.0 + log2pi);
 }
 
+// Partial sums of a[i] * b[i] in fp64: block z sums a fixed strided subset
+// and reduces it in a fixed order, so the result does not depend on timing.
+constexpr int kDotBlocks = 512;
+__global__ __launch_bounds__(256) void k_dot_partial(const float* __restrict__ a,
+                                                     const float* __restrict__ b, int64_t count,
+                                                     double* __restrict__ part, const int* st) {
+  if (ff_halted(st)) return;
+  __shared__ double red[256];
+  double s = 0.0;
+  const int64_t stride = (int64_t)kDotBlocks * 256;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count; i += stride)
+    s += (double)a[i] * (double)b[i];
+  s = block_sum_256(s, red);
+  if (threadIdx.x == 0) part[blockIdx.x] = s;
+}
+
+// out[0] = sum of the partials, out[1] = 2 sum(slotsA), out[2] = 2 sum(slotsB).
+__global__ __launch_bounds__(256) void k_dot_final(const double* __restrict__ part,
+                                                   const double* slotsA, int nA,
+                                                   const double* slotsB, int nB, double* out,
+                                                   const int* st) {
+  if (ff_halted(st)) return;
+  __shared__ double red[256];
+  double s = 0.0;
+  for (int i = threadIdx.x; i < kDotBlocks; i += 256) s += part[i];
+  s = block_sum_256(s, red);
+  if (threadIdx.x == 0) {
+    double la = 0.0, lb = 0.0;
+    for (int i = 0; i < nA; ++i) la += slotsA[i];
+    for (int i = 0; i < nB; ++i) lb += slotsB[i];
+    out[0] = s;
+    out[1] = 2.0 * la;
+    out[2] = 2.0 * lb;
+  }
+}
+
 __global__ __launch_bounds__(256) void k_copy_f32(const float* __restrict__ src,
                                                   float* __restrict__ dst, int64_t count,
                                                   const int* st) {
@@ -209,6 +245,16 @@ hipError_t launch_loglik(const double* slotsA, int nA, const double* slotsB, int
                          double* ll_out, const int* st, hipStream_t s) {
   hipLaunchKernelGGL(k_loglik, dim3(1), dim3(64), 0, s, slotsA, nA, slotsB, nB, c, first_is_B, m,
                      n, N, ll_out, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_objective_terms(const float* a, const float* b, int64_t count,
+                                  const double* slotsA, int nA, const double* slotsB, int nB,
+                                  double* scratch, double* out, const int* st, hipStream_t s) {
+  if (count < 0 || nA < 0 || nB < 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_dot_partial, dim3(kDotBlocks), dim3(256), 0, s, a, b, count, scratch, st);
+  hipLaunchKernelGGL(k_dot_final, dim3(1), dim3(256), 0, s, scratch, slotsA, nA, slotsB, nB, out,
+                     st);
   return hipGetLastError();
 }
 

@@ -278,18 +278,24 @@ ff_status cholinv_rec(ff_handle_s* h, Side& s, int64_t o, int64_t sz, int iterat
   return FF_OK;
 }
 
-// L^-1 of s.F[slot] into s.Li and the whitening operand s.Lw.
-ff_status cholinv(ff_handle_s* h, Side& s, int slot, int iteration) {
+// L^-1 of the dim x dim factor at src into s.Li and the whitening operand
+// s.Lw; sum log L_jj per leaf into s.slots.
+ff_status cholinv_from(ff_handle_s* h, Side& s, const float* src, int iteration) {
   Timed t(h, 3, (double)s.dim * s.dim * s.dim / 3.0);
-  FF_HIP(launch_copy_f32(s.F[slot], s.L, s.dim * s.dim, h->st, h->stream));
+  FF_HIP(launch_copy_f32(src, s.L, s.dim * s.dim, h->st, h->stream));
   ff_status rc = cholinv_rec(h, s, 0, s.dim, iteration);
   if (rc != FF_OK) return rc;
   FF_HIP(launch_convert_inverse(s.Li, s.dim, s.Lw, s.Lw2, s.dim_p, h->elem, h->st, h->stream));
   return FF_OK;
 }
 
-// s.F[slot] = (1/(N p.dim)) sum_i X_i Li_p^T Li_p X_i^T  (+ damping), trace into s.tr.
-ff_status update(ff_handle_s* h, Side& s, Side& p, int slot) {
+ff_status cholinv(ff_handle_s* h, Side& s, int slot, int iteration) {
+  return cholinv_from(h, s, s.F[slot], iteration);
+}
+
+// s.F[slot] = (1/(N p.dim)) sum_i X_i Li_p^T Li_p X_i^T  (+ damping), trace into
+// s.tr; with finish = false, without damping and trace.
+ff_status update(ff_handle_s* h, Side& s, Side& p, int slot, bool finish = true) {
   const void* X = (&s == &h->B) ? h->Gx : h->Gt;
   const int64_t N = h->N, rows = N * s.dim_p, Kp = p.dim_p;
   const double scale = 1.0 / ((double)N * (double)p.dim);
@@ -342,7 +348,7 @@ ff_status update(ff_handle_s* h, Side& s, Side& p, int slot) {
                                     h->stream));
     }
   }
-  FF_HIP(launch_trace_damp(s.F[slot], s.dim, h->cfg.damping, s.tr, h->st, h->stream));
+  if (finish) FF_HIP(launch_trace_damp(s.F[slot], s.dim, h->cfg.damping, s.tr, h->st, h->stream));
   return FF_OK;
 }
 
@@ -630,6 +636,50 @@ ff_status ff_kron_apply(ff_handle h, const float* X, float* Y, int64_t batch, ff
     return fail(FF_ERR_NOT_SPD, std::string("factor ") + (st[1] == 1 ? "A" : "B") +
                                     " not positive definite in ff_kron_apply");
   }
+  return FF_OK;
+}
+
+ff_status ff_objective(ff_handle h, const float* A, const float* B, double* psi) {
+  if (h == nullptr) return fail(FF_ERR_INVALID_ARG, "handle is NULL");
+  if (psi == nullptr) return fail(FF_ERR_INVALID_ARG, "psi is NULL");
+  const int cur = h->cur, spare = cur ^ 1;
+  const float* Af = A != nullptr ? A : h->A.F[cur];
+  const float* Bf = B != nullptr ? B : h->B.F[cur];
+  // The whitening operands no longer belong to the current factors.
+  h->A.lw_valid = h->B.lw_valid = false;
+  ff_status rc;
+  if ((rc = cholinv_from(h, h->A, Af, -1)) != FF_OK) return rc;
+  if ((rc = cholinv_from(h, h->B, Bf, -1)) != FF_OK) return rc;
+  // M = (1/(N n)) sum_i G_i A^-1 G_i^T into the spare B buffer (no damping)
+  if ((rc = update(h, h->B, h->A, spare, false)) != FF_OK) return rc;
+  // Y = L_B^-1 M; tr(B^-1 M) = sum_jk Y_jk (L_B^-1)_jk
+  const int64_t m = h->m;
+  GemmF32 g{};
+  g.st = h->st;
+  g.kseg = INT64_MAX / 4;
+  g.ksplit = 1;
+  g.A = h->B.Li; g.lda = m; g.transA = 0;
+  g.B = h->B.F[spare]; g.ldb = m; g.transB = 0;
+  g.C = h->B.L; g.ldc = m;
+  g.M = m; g.N = m; g.K = m;
+  g.alpha = 1.f; g.beta = 0.f; g.flags = kKHiRow;
+  FF_HIP(launch_gemm_f32(g, 1, h->stream));
+  double* scratch = reinterpret_cast<double*>(h->P);
+  double* out = scratch + 512;
+  FF_HIP(launch_objective_terms(h->B.L, h->B.Li, m * m, h->A.slots, h->A.nslots, h->B.slots,
+                                h->B.nslots, scratch, out, h->st, h->stream));
+  double terms[3];
+  FF_HIP(hipMemcpyAsync(terms, out, sizeof terms, hipMemcpyDeviceToHost, h->stream));
+  int st[4];
+  if ((rc = read_status(h, st)) != FF_OK) return rc;
+  if (st[0] != 0) {
+    if ((rc = clear_status(h)) != FF_OK) return rc;
+    FF_HIP(hipStreamSynchronize(h->stream));
+    return fail(FF_ERR_NOT_SPD, std::string("factor ") + (st[1] == 1 ? "A" : "B") +
+                                    " not positive definite in ff_objective");
+  }
+  // (1/(N m n)) sum_i tr(B^-1 G_i A^-1 G_i^T) = tr(B^-1 M) / m
+  *psi = log(terms[0] / (double)m) + terms[1] / (double)h->n + terms[2] / (double)m;
   return FF_OK;
 }
 

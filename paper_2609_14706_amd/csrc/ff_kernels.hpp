@@ -106,6 +106,12 @@ hipError_t launch_loglik(const double* slotsA, int nA, const double* slotsB, int
                          const double* c, int first_is_B, double m, double n, double N,
                          double* ll_out, const int* st, hipStream_t s);
 
+// out[0] = sum_i a[i] b[i] (fp64, fixed order), out[1] = 2 sum(slotsA),
+// out[2] = 2 sum(slotsB).  scratch: 512 doubles.
+hipError_t launch_objective_terms(const float* a, const float* b, int64_t count,
+                                  const double* slotsA, int nA, const double* slotsB, int nB,
+                                  double* scratch, double* out, const int* st, hipStream_t s);
+
 hipError_t launch_copy_f32(const float* src, float* dst, int64_t count, const int* st,
                            hipStream_t s);
 hipError_t launch_fill_f32(float* dst, int64_t count, float v, hipStream_t s);

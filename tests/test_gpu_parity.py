@@ -227,3 +227,72 @@ def test_resume_and_bitwise_determinism(gpu):
     assert bool((A1 == A2).all()) and bool((B1 == B2).all())
     f1.close()
     f2.close()
+
+
+# ------------------------------------------------------- mismatch objective
+
+def _spd(dim, rng, cond):
+    Q = synth.haar_orthogonal(dim, rng)
+    return ((Q * np.geomspace(1.0, 1.0 / cond, dim)) @ Q.T).astype(np.float32)
+
+
+@pytest.mark.parametrize("dtype,tol", [("f32", 1e-5), ("bf16", 5e-3)])
+def test_objective_at_given_factors(gpu, dtype, tol):
+    """psi = log Phi(H, A (x) B) + log|H|/(mn) (Section 4) at factors that are
+    not a fixed point, through the handle's own path; A, B are the same fp32
+    values on both sides."""
+    import torch
+    import paper_2609_14706_amd as ffe
+    rng = np.random.default_rng(21)
+    m, n, N = (48, 80, 40) if dtype == "f32" else (600, 520, 6)
+    w = small_workload("attn", m=m, n=n, N=N)
+    d = synth.generate(w) if dtype == "bf16" else None
+    G = d.G if dtype == "bf16" else synth.generate(small_workload("tiny", m=m, n=n, N=N)).G
+    A, B = _spd(n, rng, 30.0), _spd(m, rng, 50.0)
+    f = ffe.FlipFlop(to_device(G, gpu))
+    psi = f.objective(torch.from_numpy(A), torch.from_numpy(B))
+    f.close()
+    ref = oracle.objective(G, A.astype(np.float64), B.astype(np.float64))
+    print(f"objective {dtype} {m}x{n} N={N}: device {psi:.9f} oracle {ref:.9f}")
+    assert abs(psi - ref) < tol
+
+
+def test_objective_of_current_factors_and_handle_state(gpu):
+    """Default factors are the handle's current ones; psi falls over the
+    iterations as the oracle's does; evaluating foreign factors leaves the
+    iteration itself unchanged (bitwise against an undisturbed handle); a
+    factor that is not positive definite is reported."""
+    import torch
+    import paper_2609_14706_amd as ffe
+    rng = np.random.default_rng(22)
+    d = synth.generate(small_workload("tiny", m=40, n=72, N=30))
+    G = to_device(d.G, gpu)
+    f = ffe.FlipFlop(G)
+    g = ffe.FlipFlop(G)
+    psis = []
+    for k in range(3):
+        f.iterate(1)
+        g.iterate(1)
+        psis.append(f.objective())
+        f.objective(torch.from_numpy(_spd(72, rng, 5.0)), None)   # foreign A, then keep going
+    refs = [oracle.objective(d.G, r.A, r.B) for r in
+            (oracle.flipflop(d.G, k) for k in (1, 2, 3))]
+    print("psi device", psis, "oracle", refs)
+    assert all(abs(a - b) < 1e-5 for a, b in zip(psis, refs))
+    assert psis[0] >= psis[1] >= psis[2]
+    f.iterate(2)
+    g.iterate(2)
+    A1, B1 = f.factors()
+    A2, B2 = g.factors()
+    assert bool((A1 == A2).all()) and bool((B1 == B2).all())
+    bad = -torch.eye(72)
+    with pytest.raises(ffe.FlipFlopError) as ei:
+        f.objective(bad, None)
+    assert ei.value.code == ffe.FF_ERR_NOT_SPD
+    f.iterate(1)
+    g.iterate(1)
+    A1, _ = f.factors()
+    A2, _ = g.factors()
+    assert bool((A1 == A2).all())
+    f.close()
+    g.close()

@@ -344,3 +344,36 @@ def test_mismatch_factor_identities():
             lhs = np.log(phi) + np.linalg.slogdet(H)[1] / d
             rhs = np.linalg.slogdet(A)[1] / n + np.linalg.slogdet(B)[1] / m
             assert abs(lhs - rhs) < 1e-10
+
+
+def test_objective_is_mismatch_factor_up_to_the_data_term():
+    """Section 4: psi = log Phi(H, A (x) B) + log|H| / (m n), with Phi taken
+    as the AM/GM ratio of the generalised eigenvalues of (H, A (x) B) (an
+    independent route through the explicit mn x mn matrices), at factors that
+    are not a fixed point; invariant under A -> cA, B -> B/c; never rising
+    over flip-flop half steps; and after an A half step it equals
+    -2 l / (N m n) - (1 + log 2 pi) with l the log-likelihood."""
+    rng = np.random.default_rng(17)
+    m, n = 2, 3
+    N = 40                                      # N >= mn: H nonsingular
+    G = matrix_normal(N, rand_spd(n, rng, 4), rand_spd(m, rng, 6), rng)
+    G += 0.3 * rng.standard_normal(G.shape)
+    H = explicit_H(G)
+    d = m * n
+    A, B = rand_spd(n, rng, 3), rand_spd(m, rng, 8)
+    psi = oracle.objective(G, A, B)
+    ref = np.log(oracle.mismatch_factor(H, A, B)) + np.linalg.slogdet(H)[1] / d
+    assert abs(psi - ref) < 1e-11
+    assert abs(oracle.objective(G, 3.7 * A, B / 3.7) - psi) < 1e-12
+    r = oracle.flipflop(G, 4, keep_half_steps=True)
+    prev = oracle.objective(G, np.eye(n), np.eye(m))
+    for kind, A, B in r.half_steps:
+        cur = oracle.objective(G, A, B)
+        assert cur <= prev + 1e-12
+        prev = cur
+        if kind == "A":
+            ll = oracle.loglik(G, A, B)
+            assert abs(cur - (-2.0 * ll / (N * d) - 1.0 - np.log(2 * np.pi))) < 1e-10
+    # rank-deficient H (N < mn): psi is still finite and scale-invariant
+    Gs = G[:3]
+    assert np.isfinite(oracle.objective(Gs, A, B))
