@@ -73,8 +73,18 @@ typedef enum { FF_ORDER_B_FIRST = 0, FF_ORDER_A_FIRST = 1 } ff_order;
  * its inverse vec(B^-1 X A^-1). */
 typedef enum { FF_APPLY = 0, FF_APPLY_INV = 1 } ff_apply_mode;
 
+/* How the samples are given.  FF_SAMPLES_DENSE: N matrices G_i (m x n).
+ * FF_SAMPLES_RANK1: N tokens, sample t being the rank-one matrix
+ * G_t = g_t x_t^T of an output gradient g_t (m) and an input x_t (n), the
+ * form the paper runs (Section 5 writes both half steps for it:
+ * A <- E[(g^T B^-1 g) x x^T], B <- E[(x^T A^-1 x) g g^T]; Table 1, FlipFlop
+ * row).  The iteration, scalings and outputs are those of the dense form
+ * applied to these G_t; the cost per iteration is 2 N (m^2 + n^2). */
+typedef enum { FF_SAMPLES_DENSE = 0, FF_SAMPLES_RANK1 = 1 } ff_sample_form;
+
 typedef struct {
-  int64_t m, n, N;        /* G is [N][m][n], row-major, contiguous; all >= 1 */
+  int64_t m, n, N;        /* G is [N][m][n], row-major, contiguous; all >= 1
+                             (RANK1: N = number of tokens) */
   ff_dtype dtype;         /* element type of G */
   const void* G;          /* DEVICE pointer, 16-byte aligned, BORROWED: must
                              stay valid and unmodified until ff_destroy */
@@ -92,6 +102,11 @@ typedef struct {
                              caller, >= ff_workspace_size() bytes; must stay
                              valid until ff_destroy */
   size_t workspace_bytes;
+  ff_sample_form form;    /* 0 = FF_SAMPLES_DENSE (a zeroed config is dense) */
+  const void* x;          /* RANK1: DEVICE [N][n] token inputs, row-major,
+                             dtype, 16-byte aligned, BORROWED like G.  G is
+                             ignored (may be NULL) */
+  const void* g;          /* RANK1: DEVICE [N][m] token output gradients */
 } ff_config;
 
 /* Bytes of device workspace ff_init needs for cfg (only the shape, dtype and

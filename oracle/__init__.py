@@ -12,8 +12,11 @@ from .flipflop import (FlipFlopResult, NotSPDError, as_f64_samples, half_step_B,
                        half_step_A, normalise, damp, flipflop, loglik, objective)
 from .metrics import kron_rel_error, kron_rel_error_scale_free, trace_identity
 from .kron import kron_apply, mismatch_factor
+from .tokens import (half_step_A_tokens, half_step_B_tokens, half_step_B_tokens_rows, flipflop_tokens, loglik_tokens,
+                     objective_tokens, materialise, token_weights)
 
 __all__ = ["FlipFlopResult", "NotSPDError", "as_f64_samples", "half_step_B", "half_step_B_rows",
            "half_step_A", "normalise", "damp", "flipflop", "loglik", "objective",
            "kron_rel_error", "kron_rel_error_scale_free", "trace_identity",
-           "kron_apply", "mismatch_factor"]
+           "kron_apply", "mismatch_factor", "half_step_A_tokens", "half_step_B_tokens", "half_step_B_tokens_rows",
+           "flipflop_tokens", "loglik_tokens", "objective_tokens", "materialise", "token_weights"]

@@ -18,6 +18,7 @@ FF_OK, FF_ERR_INVALID_ARG, FF_ERR_NOT_SPD, FF_ERR_WORKSPACE, FF_ERR_HIP, FF_ERR_
 FF_F32, FF_BF16 = 0, 1
 FF_ORDER_B_FIRST, FF_ORDER_A_FIRST = 0, 1
 FF_APPLY, FF_APPLY_INV = 0, 1
+FF_SAMPLES_DENSE, FF_SAMPLES_RANK1 = 0, 1
 KERNEL_IDS = {"whiten": 0, "syrk": 1, "reduce": 2, "cholinv": 3}
 
 
@@ -36,6 +37,9 @@ class ff_config(ctypes.Structure):
         ("whiten_split", ctypes.c_int),
         ("workspace", ctypes.c_void_p),
         ("workspace_bytes", ctypes.c_size_t),
+        ("form", ctypes.c_int),
+        ("x", ctypes.c_void_p),
+        ("g", ctypes.c_void_p),
     ]
 
 
@@ -165,28 +169,53 @@ class FlipFlop:
     and keeps it alive; the workspace is a torch uint8 tensor on G's device.
     """
 
-    def __init__(self, G, *, order: str = "B_FIRST", damping: float = 0.0, A0=None, B0=None,
-                 whiten_split: int = 1, stream=None, workspace=None):
+    def __init__(self, G=None, *, tokens=None, order: str = "B_FIRST", damping: float = 0.0,
+                 A0=None, B0=None, whiten_split: int = 1, stream=None, workspace=None):
+        """G: (N, m, n) samples; or tokens = (x, g) with x (N, n) inputs and
+        g (N, m) output gradients, the samples being G_t = g_t x_t^T (the
+        rank-one form; both tensors of one dtype)."""
         import torch
-        if not isinstance(G, torch.Tensor) or not G.is_cuda:
-            raise TypeError("G must be a CUDA tensor")
-        if G.dim() != 3 or not G.is_contiguous():
-            raise ValueError("G must be a contiguous (N, m, n) tensor")
-        if G.dtype == torch.bfloat16:
+        if (G is None) == (tokens is None):
+            raise ValueError("give either G or tokens=(x, g)")
+        if tokens is not None:
+            x, g = tokens
+            for name, T in (("x", x), ("g", g)):
+                if not isinstance(T, torch.Tensor) or not T.is_cuda:
+                    raise TypeError(f"{name} must be a CUDA tensor")
+                if T.dim() != 2 or not T.is_contiguous():
+                    raise ValueError(f"{name} must be a contiguous (N, dim) tensor")
+            if x.shape[0] != g.shape[0] or x.dtype != g.dtype or x.device != g.device:
+                raise ValueError("x and g must have the same N, dtype and device")
+            ref, (N, n), m = x, x.shape, g.shape[1]
+            form = FF_SAMPLES_RANK1
+        else:
+            if not isinstance(G, torch.Tensor) or not G.is_cuda:
+                raise TypeError("G must be a CUDA tensor")
+            if G.dim() != 3 or not G.is_contiguous():
+                raise ValueError("G must be a contiguous (N, m, n) tensor")
+            ref = G
+            N, m, n = G.shape
+            form = FF_SAMPLES_DENSE
+        if ref.dtype == torch.bfloat16:
             dt = FF_BF16
-        elif G.dtype == torch.float32:
+        elif ref.dtype == torch.float32:
             dt = FF_F32
         else:
-            raise TypeError("G must be float32 or bfloat16")
-        N, m, n = G.shape
-        self.device = G.device
-        self.stream = stream if stream is not None else torch.cuda.current_stream(G.device)
+            raise TypeError("samples must be float32 or bfloat16")
+        self.device = ref.device
+        self.stream = stream if stream is not None else torch.cuda.current_stream(ref.device)
         self.m, self.n, self.N = int(m), int(n), int(N)
-        self._keep = [G]
         cfg = ff_config()
         cfg.m, cfg.n, cfg.N = self.m, self.n, self.N
         cfg.dtype = dt
-        cfg.G = G.data_ptr()
+        cfg.form = form
+        if form == FF_SAMPLES_RANK1:
+            self._keep = [x, g]
+            cfg.x, cfg.g = x.data_ptr(), g.data_ptr()
+        else:
+            self._keep = [G]
+            cfg.G = G.data_ptr()
+        G = ref
         cfg.stream = self.stream.cuda_stream
         cfg.order = {"B_FIRST": FF_ORDER_B_FIRST, "A_FIRST": FF_ORDER_A_FIRST}[order]
         cfg.damping = float(damping)
@@ -215,10 +244,12 @@ class FlipFlop:
         self.iters_done = 0
 
     @staticmethod
-    def workspace_bytes(m: int, n: int, N: int, dtype: str = "bf16", whiten_split: int = 1) -> int:
+    def workspace_bytes(m: int, n: int, N: int, dtype: str = "bf16", whiten_split: int = 1,
+                        rank1: bool = False) -> int:
         """Bytes a caller-provided workspace tensor needs (alignment slack included)."""
         cfg = ff_config()
         cfg.m, cfg.n, cfg.N = m, n, N
+        cfg.form = FF_SAMPLES_RANK1 if rank1 else FF_SAMPLES_DENSE
         cfg.dtype = FF_BF16 if dtype == "bf16" else FF_F32
         cfg.whiten_split = whiten_split
         return ff_workspace_size(cfg) + 256

@@ -43,6 +43,52 @@ __global__ __launch_bounds__(256) void k_pack(const T* __restrict__ G, T* __rest
   }
 }
 
+// ------------------------------------------- rank-one (per-token) weights
+// w[r] = sum_j v(r, j) over cols entries of row r (square = 0: v = P[r][j];
+// square = 1: v = P[r][j]^2), one wave per row, fixed reduction order.
+__global__ __launch_bounds__(256) void k_row_sums(const float* __restrict__ P, int64_t rows,
+                                                  int64_t cols, int square, float* __restrict__ w,
+                                                  const int* st) {
+  if (ff_halted(st)) return;
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= rows) return;
+  const float* p = P + r * cols;
+  double s = 0.0;
+  for (int64_t j = lane; j < cols; j += 64) {
+    const double v = p[j];
+    s += square ? v * v : v;
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o);
+  if (lane == 0) w[r] = (float)s;
+}
+
+// out[c][r] = sqrt(w[r]) * M[r][c] for the rows_p x cols_p matrix M: the
+// rows of M (tokens) weighted and turned into the k axis of a symmetric
+// product.  64 x 64 tiles through LDS.
+template <typename T>
+__global__ __launch_bounds__(256) void k_scale_transpose(const T* __restrict__ M,
+                                                         const float* __restrict__ w,
+                                                         int64_t rows_p, int64_t cols_p,
+                                                         T* __restrict__ out, const int* st) {
+  if (ff_halted(st)) return;
+  __shared__ float tile[64][65];
+  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int y = ty; y < 64; y += 4) {
+    const int64_t r = r0 + y, c = c0 + tx;
+    float v = 0.0f;
+    if (r < rows_p && c < cols_p) v = sqrtf(w[r]) * Elem<T>::to_f32(M[r * cols_p + c]);
+    tile[y][tx] = v;
+  }
+  __syncthreads();
+  for (int y = ty; y < 64; y += 4) {
+    const int64_t c = c0 + y, r = r0 + tx;
+    if (c < cols_p && r < rows_p) out[c * rows_p + r] = Elem<T>::from_f32(tile[tx][y]);
+  }
+}
+
 // --------------------------------------------------------- inverse convert
 template <typename T>
 __global__ __launch_bounds__(256) void k_convert_inverse(const float* __restrict__ Li, int64_t dim,
@@ -207,6 +253,34 @@ hipError_t launch_pack(const void* G, void* out, int64_t N, int64_t m, int64_t n
   else if (elem_bytes == 4)
     hipLaunchKernelGGL(k_pack<float>, grid, dim3(256), 0, s, (const float*)G, (float*)out, m, n,
                        rows_p, cols_p, transpose);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_row_sums(const float* P, int64_t rows, int64_t cols, int square, float* w,
+                           const int* st, hipStream_t s) {
+  if (rows < 0 || cols < 1) return hipErrorInvalidValue;
+  if (rows == 0) return hipSuccess;
+  const int64_t blocks = (rows + 3) / 4;
+  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_row_sums, dim3((uint32_t)blocks), dim3(256), 0, s, P, rows, cols, square, w,
+                     st);
+  return hipGetLastError();
+}
+
+hipError_t launch_scale_transpose(const void* M, const float* w, int64_t rows_p, int64_t cols_p,
+                                  void* out, int elem_bytes, const int* st, hipStream_t s) {
+  if (rows_p < 1 || cols_p < 1) return hipErrorInvalidValue;
+  const int64_t gx = (cols_p + 63) / 64, gy = (rows_p + 63) / 64;
+  if (gx > 0x7fffffff || gy > 65535) return hipErrorInvalidValue;
+  const dim3 grid((uint32_t)gx, (uint32_t)gy);
+  if (elem_bytes == 2)
+    hipLaunchKernelGGL(k_scale_transpose<bf16_t>, grid, dim3(256), 0, s, (const bf16_t*)M, w,
+                       rows_p, cols_p, (bf16_t*)out, st);
+  else if (elem_bytes == 4)
+    hipLaunchKernelGGL(k_scale_transpose<float>, grid, dim3(256), 0, s, (const float*)M, w, rows_p,
+                       cols_p, (float*)out, st);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

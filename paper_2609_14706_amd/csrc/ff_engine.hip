@@ -68,7 +68,14 @@ struct Side {
 struct Layout {
   int64_t m_p, n_p;
   bool own_gx;
-  size_t off_small, off_ll, off_slotsA, off_slotsB, off_gx, off_gt, off_w, off_p;
+  bool rank1;
+  int64_t T_p;  // rank-one form: padded token count
+  // dense: gx = padded G, gt = padded transposed G, w = whitened samples;
+  // rank-one: gx = padded x (T_p x n_p), gt = padded g (T_p x m_p),
+  // w = row-norm partials (bf16) or whitened tokens (fp32), s = weighted
+  // transposed tokens, wv = token weights (2 T_p floats)
+  size_t off_small, off_ll, off_slotsA, off_slotsB, off_gx, off_gt, off_w, off_p, off_s, off_wv;
+  size_t w_bytes;  // capacity of the w region
   size_t off_A[6], off_B[6];  // F0, F1, L, Li, Lw, Lw2
   size_t total;
   int splitsA, splitsB;
@@ -110,7 +117,12 @@ ff_status validate_shape(const ff_config* c) {
   if (c->m < 1 || c->n < 1 || c->N < 1)
     return fail(FF_ERR_INVALID_ARG, "m, n and N must be >= 1");
   if (c->dtype != FF_F32 && c->dtype != FF_BF16) return fail(FF_ERR_INVALID_ARG, "unknown dtype");
-  if (c->N > 65535) return fail(FF_ERR_INVALID_ARG, "N must be <= 65535");
+  if (c->form != FF_SAMPLES_DENSE && c->form != FF_SAMPLES_RANK1)
+    return fail(FF_ERR_INVALID_ARG, "unknown sample form");
+  if (c->form == FF_SAMPLES_DENSE && c->N > 65535)
+    return fail(FF_ERR_INVALID_ARG, "N must be <= 65535");
+  if (c->form == FF_SAMPLES_RANK1 && c->N > (1 << 22))
+    return fail(FF_ERR_INVALID_ARG, "N (tokens) must be <= 4194304");
   if (c->m > (1 << 20) || c->n > (1 << 20))
     return fail(FF_ERR_INVALID_ARG, "m and n must be <= 1048576");
   if (is_bf16(c) && c->whiten_split != 1 && c->whiten_split != 2)
@@ -124,7 +136,9 @@ Layout make_layout(const ff_config* c) {
   const int64_t m = c->m, n = c->n, N = c->N;
   L.m_p = round_up(m, g);
   L.n_p = round_up(n, g);
-  L.own_gx = !(L.m_p == m && L.n_p == n);
+  L.rank1 = c->form == FF_SAMPLES_RANK1;
+  L.own_gx = L.rank1 || !(L.m_p == m && L.n_p == n);
+  L.T_p = L.rank1 ? round_up(N, g) : 0;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
@@ -135,19 +149,34 @@ Layout make_layout(const ff_config* c) {
   L.off_ll = take(sizeof(double) * kLLCap);
   L.off_slotsA = take(sizeof(double) * ((n + kLeaf - 1) / kLeaf));
   L.off_slotsB = take(sizeof(double) * ((m + kLeaf - 1) / kLeaf));
-  const size_t gbytes = (size_t)N * L.m_p * L.n_p * e;
-  L.off_gx = L.own_gx ? take(gbytes) : 0;
-  L.off_gt = take(gbytes);
-  L.off_w = take(std::max(gbytes, (size_t)m * n * sizeof(float)));
+  const int64_t dmax = std::max(L.m_p, L.n_p);
+  if (L.rank1) {
+    L.off_gx = take((size_t)L.T_p * L.n_p * e);
+    L.off_gt = take((size_t)L.T_p * L.m_p * e);
+    L.w_bytes = std::max(is_bf16(c) ? (size_t)L.T_p * 2 * (dmax / kTileBF16) * sizeof(float)
+                                    : (size_t)L.T_p * dmax * sizeof(float),
+                         (size_t)m * n * sizeof(float));
+    L.off_w = take(L.w_bytes);
+    L.off_s = take((size_t)dmax * L.T_p * e);
+    L.off_wv = take(2 * (size_t)L.T_p * sizeof(float));
+  } else {
+    const size_t gbytes = (size_t)N * L.m_p * L.n_p * e;
+    L.off_gx = L.own_gx ? take(gbytes) : 0;
+    L.off_gt = take(gbytes);
+    L.w_bytes = std::max(gbytes, (size_t)m * n * sizeof(float));
+    L.off_w = take(L.w_bytes);
+  }
+  // k depth of the symmetric products: the stacked samples, or the tokens
+  const int64_t kB = L.rank1 ? L.T_p : N * L.n_p, kA = L.rank1 ? L.T_p : N * L.m_p;
   if (is_bf16(c)) {
-    L.splitsB = choose_splits_bf16(L.m_p, N * L.n_p / 64);
-    L.splitsA = choose_splits_bf16(L.n_p, N * L.m_p / 64);
+    L.splitsB = choose_splits_bf16(L.m_p, kB / 64);
+    L.splitsA = choose_splits_bf16(L.n_p, kA / 64);
     const int64_t TB = L.m_p / kTileBF16, TA = L.n_p / kTileBF16;
     L.partialB = (size_t)L.splitsB * (TB * (TB + 1) / 2) * kTileBF16 * kTileBF16;
     L.partialA = (size_t)L.splitsA * (TA * (TA + 1) / 2) * kTileBF16 * kTileBF16;
   } else {
-    L.splitsB = choose_splits_f32(L.m_p, N * L.n_p);
-    L.splitsA = choose_splits_f32(L.n_p, N * L.m_p);
+    L.splitsB = choose_splits_f32(L.m_p, kB);
+    L.splitsA = choose_splits_f32(L.n_p, kA);
     L.partialB = (size_t)L.splitsB * L.m_p * L.m_p;
     L.partialA = (size_t)L.splitsA * L.n_p * L.n_p;
   }
@@ -182,6 +211,8 @@ struct ff_handle_s {
   void* Gt = nullptr;
   void* W = nullptr;
   float* P = nullptr;
+  void* S = nullptr;      // rank-one form: weighted transposed tokens
+  float* wv = nullptr;    // rank-one form: token weights (2 x T_p)
   Side A, B;
   int* st = nullptr;
   double* c = nullptr;
@@ -293,9 +324,82 @@ ff_status cholinv(ff_handle_s* h, Side& s, int slot, int iteration) {
   return cholinv_from(h, s, s.F[slot], iteration);
 }
 
+// Rank-one form: token weights wbuf[t] = ||L_p^-1 v_t||^2 for the token
+// vectors v_t of side p's dimension (x_t when p = A, g_t when p = B).
+ff_status token_weights(ff_handle_s* h, Side& p, float* wbuf) {
+  const void* V = (&p == &h->A) ? h->Gx : h->Gt;
+  const int64_t T_p = h->lay.T_p, Kp = p.dim_p;
+  const double wflop = (double)h->N * p.dim * p.dim;
+  Timed t(h, 0, wflop);
+  if (h->bf16) {
+    FF_HIP(launch_whiten_norm_bf16((const bf16_t*)V, (const bf16_t*)p.Lw, (const bf16_t*)p.Lw2,
+                                   (float*)h->W, T_p, Kp, h->st, h->stream));
+    FF_HIP(launch_row_sums((const float*)h->W, T_p, 2 * (Kp / kTileBF16), 0, wbuf, h->st,
+                           h->stream));
+  } else {
+    GemmF32 g{};
+    g.st = h->st;
+    g.ksplit = 1;
+    g.kseg = Kp;
+    g.A = (const float*)V; g.lda = Kp; g.transA = 0;
+    g.B = (const float*)p.Lw; g.ldb = Kp; g.transB = 1;
+    g.C = (float*)h->W; g.ldc = Kp;
+    g.M = T_p; g.N = Kp; g.K = Kp;
+    g.alpha = 1.f; g.beta = 0.f; g.flags = kKHiCol;
+    FF_HIP(launch_gemm_f32(g, 1, h->stream));
+    FF_HIP(launch_row_sums((const float*)h->W, T_p, Kp, 1, wbuf, h->st, h->stream));
+  }
+  return FF_OK;
+}
+
+// Rank-one form of the half step (Section 5): s.F[slot] =
+// (1/(N p.dim)) sum_t ||L_p^-1 v_t||^2 u_t u_t^T with u_t the token vector of
+// side s, as a symmetric product over tokens of the weighted, transposed u.
+ff_status update_rank1(ff_handle_s* h, Side& s, Side& p, int slot, bool finish) {
+  float* wbuf = h->wv;
+  ff_status rc = token_weights(h, p, wbuf);
+  if (rc != FF_OK) return rc;
+  const void* U = (&s == &h->B) ? h->Gt : h->Gx;
+  const int64_t T_p = h->lay.T_p;
+  const double scale = 1.0 / ((double)h->N * (double)p.dim);
+  const double sflop = (double)h->N * s.dim * s.dim;
+  {
+    Timed t(h, 2, 0.0);
+    FF_HIP(launch_scale_transpose(U, wbuf, T_p, s.dim_p, h->S, h->elem, h->st, h->stream));
+  }
+  if (h->bf16) {
+    {
+      Timed t(h, 1, sflop);
+      FF_HIP(launch_syrk_bf16((const bf16_t*)h->S, s.dim_p, T_p, s.dim_p * T_p, 1, s.splits, h->P,
+                              h->st, h->stream));
+    }
+    Timed t(h, 2, 0.0);
+    FF_HIP(launch_reduce_frag(h->P, s.splits, s.dim_p, s.F[slot], s.dim, scale, h->st, h->stream));
+  } else {
+    {
+      Timed t(h, 1, sflop);
+      GemmF32 q{};
+      q.st = h->st;
+      q.A = (const float*)h->S; q.lda = T_p; q.transA = 0;
+      q.B = (const float*)h->S; q.ldb = T_p; q.transB = 1;
+      q.C = h->P; q.ldc = s.dim_p; q.sC = s.dim_p * s.dim_p;
+      q.M = s.dim_p; q.N = s.dim_p; q.K = T_p;
+      q.kseg = T_p; q.segA = q.segB = 0;
+      q.alpha = 1.f; q.beta = 0.f; q.flags = kCLower; q.ksplit = s.splits;
+      FF_HIP(launch_gemm_f32(q, 1, h->stream));
+    }
+    Timed t(h, 2, 0.0);
+    FF_HIP(launch_reduce_rowmajor(h->P, s.splits, s.dim_p, s.F[slot], s.dim, scale, h->st,
+                                  h->stream));
+  }
+  if (finish) FF_HIP(launch_trace_damp(s.F[slot], s.dim, h->cfg.damping, s.tr, h->st, h->stream));
+  return FF_OK;
+}
+
 // s.F[slot] = (1/(N p.dim)) sum_i X_i Li_p^T Li_p X_i^T  (+ damping), trace into
 // s.tr; with finish = false, without damping and trace.
 ff_status update(ff_handle_s* h, Side& s, Side& p, int slot, bool finish = true) {
+  if (h->lay.rank1) return update_rank1(h, s, p, slot, finish);
   const void* X = (&s == &h->B) ? h->Gx : h->Gt;
   const int64_t N = h->N, rows = N * s.dim_p, Kp = p.dim_p;
   const double scale = 1.0 / ((double)N * (double)p.dim);
@@ -451,8 +555,13 @@ ff_status ff_init(const ff_config* cfg, ff_handle* out) {
   ff_status rc = validate_shape(cfg);
   if (rc != FF_OK) return rc;
   if (out == nullptr) return fail(FF_ERR_INVALID_ARG, "out is NULL");
-  if (cfg->G == nullptr || ((uintptr_t)cfg->G % 16) != 0)
+  if (cfg->form == FF_SAMPLES_RANK1) {
+    if (cfg->x == nullptr || cfg->g == nullptr || ((uintptr_t)cfg->x % 16) != 0 ||
+        ((uintptr_t)cfg->g % 16) != 0)
+      return fail(FF_ERR_INVALID_ARG, "x and g must be non-NULL 16-byte aligned device pointers");
+  } else if (cfg->G == nullptr || ((uintptr_t)cfg->G % 16) != 0) {
     return fail(FF_ERR_INVALID_ARG, "G must be a non-NULL 16-byte aligned device pointer");
+  }
   if (cfg->order != FF_ORDER_B_FIRST && cfg->order != FF_ORDER_A_FIRST)
     return fail(FF_ERR_INVALID_ARG, "unknown order");
   if (!(cfg->damping >= 0.0) || !isfinite(cfg->damping))
@@ -497,6 +606,10 @@ ff_status ff_init(const ff_config* cfg, ff_handle* out) {
   h->Gt = ws + lay.off_gt;
   h->W = ws + lay.off_w;
   h->P = (float*)(ws + lay.off_p);
+  if (lay.rank1) {
+    h->S = ws + lay.off_s;
+    h->wv = (float*)(ws + lay.off_wv);
+  }
   auto side = [&](Side& s, const size_t* o, int64_t dim, int64_t dim_p, int splits, int code) {
     s.dim = dim;
     s.dim_p = dim_p;
@@ -515,9 +628,15 @@ ff_status ff_init(const ff_config* cfg, ff_handle* out) {
   auto setup = [&]() -> ff_status {
     FF_HIP(launch_set_int(h->st, 4, 0, h->stream));
     const int64_t N = h->N, m = h->m, n = h->n;
-    if (lay.own_gx)
-      FF_HIP(launch_pack(cfg->G, (void*)h->Gx, N, m, n, lay.m_p, lay.n_p, 0, h->elem, h->stream));
-    FF_HIP(launch_pack(cfg->G, h->Gt, N, m, n, lay.n_p, lay.m_p, 1, h->elem, h->stream));
+    if (lay.rank1) {
+      // tokens as one padded matrix each: x -> T_p x n_p, g -> T_p x m_p
+      FF_HIP(launch_pack(cfg->x, (void*)h->Gx, 1, N, n, lay.T_p, lay.n_p, 0, h->elem, h->stream));
+      FF_HIP(launch_pack(cfg->g, h->Gt, 1, N, m, lay.T_p, lay.m_p, 0, h->elem, h->stream));
+    } else {
+      if (lay.own_gx)
+        FF_HIP(launch_pack(cfg->G, (void*)h->Gx, N, m, n, lay.m_p, lay.n_p, 0, h->elem, h->stream));
+      FF_HIP(launch_pack(cfg->G, h->Gt, N, m, n, lay.n_p, lay.m_p, 1, h->elem, h->stream));
+    }
     // Upper blocks of L^-1 are never written by the factorisation: zero once.
     FF_HIP(launch_fill_f32(h->A.Li, n * n, 0.0f, h->stream));
     FF_HIP(launch_fill_f32(h->B.Li, m * m, 0.0f, h->stream));
@@ -592,8 +711,7 @@ ff_status ff_kron_apply(ff_handle h, const float* X, float* Y, int64_t batch, ff
     if ((rc = cholinv(h, h->B, cur, -1)) != FF_OK) return rc;
   }
   float* T = (float*)h->W;
-  const size_t tcap = std::max((size_t)h->N * h->lay.m_p * h->lay.n_p * h->elem,
-                               (size_t)mn * sizeof(float)) / sizeof(float);
+  const size_t tcap = h->lay.w_bytes / sizeof(float);  // >= m n floats
   const int64_t chunk = std::max<int64_t>(1, (int64_t)(tcap / (size_t)mn));
   for (int64_t b0 = 0; b0 < batch; b0 += chunk) {
     const int bc = (int)std::min<int64_t>(chunk, batch - b0);
@@ -650,6 +768,30 @@ ff_status ff_objective(ff_handle h, const float* A, const float* B, double* psi)
   ff_status rc;
   if ((rc = cholinv_from(h, h->A, Af, -1)) != FF_OK) return rc;
   if ((rc = cholinv_from(h, h->B, Bf, -1)) != FF_OK) return rc;
+  if (h->lay.rank1) {
+    // tr(B^-1 g x^T A^-1 x g^T) = (x^T A^-1 x)(g^T B^-1 g): a dot of token weights
+    float* w = h->wv;
+    float* v = h->wv + h->lay.T_p;
+    if ((rc = token_weights(h, h->A, w)) != FF_OK) return rc;
+    if ((rc = token_weights(h, h->B, v)) != FF_OK) return rc;
+    double* scratch = reinterpret_cast<double*>(h->P);
+    double* out = scratch + 512;
+    FF_HIP(launch_objective_terms(w, v, h->lay.T_p, h->A.slots, h->A.nslots, h->B.slots,
+                                  h->B.nslots, scratch, out, h->st, h->stream));
+    double terms[3];
+    FF_HIP(hipMemcpyAsync(terms, out, sizeof terms, hipMemcpyDeviceToHost, h->stream));
+    int st[4];
+    if ((rc = read_status(h, st)) != FF_OK) return rc;
+    if (st[0] != 0) {
+      if ((rc = clear_status(h)) != FF_OK) return rc;
+      FF_HIP(hipStreamSynchronize(h->stream));
+      return fail(FF_ERR_NOT_SPD, std::string("factor ") + (st[1] == 1 ? "A" : "B") +
+                                      " not positive definite in ff_objective");
+    }
+    const double mn = (double)h->m * (double)h->n;
+    *psi = log(terms[0] / ((double)h->N * mn)) + terms[1] / (double)h->n + terms[2] / (double)h->m;
+    return FF_OK;
+  }
   // M = (1/(N n)) sum_i G_i A^-1 G_i^T into the spare B buffer (no damping)
   if ((rc = update(h, h->B, h->A, spare, false)) != FF_OK) return rc;
   // Y = L_B^-1 M; tr(B^-1 M) = sum_jk Y_jk (L_B^-1)_jk

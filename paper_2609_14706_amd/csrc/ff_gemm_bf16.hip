@@ -102,6 +102,11 @@ __device__ __forceinline__ void read_frags(const Ring& sm, int buf, int wave, in
   }
 }
 
+// SW = false: acc[i][j] = A rows of tile i x B rows of tile j (element r of
+// lane l: row 8 (r/4) + 4 (l/32) + r%4, column l%32).  SW = true: the
+// operands swapped, acc[i][j] holds the transposed tile (row l%32, column
+// 8 (r/4) + 4 (l/32) + r%4), so each lane holds 16 values of one row.
+template <bool SW = false>
 __device__ __forceinline__ void mfma_slot(const Frags& f, f32x16 (&acc)[4][4]) {
 #pragma unroll
   for (int kk = 0; kk < 2; ++kk)
@@ -109,7 +114,8 @@ __device__ __forceinline__ void mfma_slot(const Frags& f, f32x16 (&acc)[4][4]) {
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[kk][i], f[kk][4 + j], acc[i][j], 0, 0, 0);
+        acc[i][j] = SW ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[kk][4 + j], f[kk][i], acc[i][j], 0, 0, 0)
+                       : __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[kk][i], f[kk][4 + j], acc[i][j], 0, 0, 0);
 }
 
 // Slices requested but not yet known to have landed may number at most
@@ -127,7 +133,7 @@ __device__ __forceinline__ void wait_pending(int pending) {
 // registers, so its slot is free), request slice i + 5 into that slot, then
 // read slice i + 1 into the other register set interleaved with the 32
 // products of slice i.
-template <int CUR, class Addr>
+template <bool SW, int CUR, class Addr>
 __device__ __forceinline__ void loop_step(Ring& sm, int i, int n, int kt0, const Addr& addr,
                                           const uint32_t (&oa)[4], const uint32_t (&ob)[4],
                                           int wave, int lane, Frags (&F)[2],
@@ -141,7 +147,7 @@ __device__ __forceinline__ void loop_step(Ring& sm, int i, int n, int kt0, const
     issue_stage(sm, (i + NSTAGE) % NSTAGE, pa, pb, oa, ob, wave);
   }
   read_frags(sm, (i + 1) % NSTAGE, wave, lane, F[CUR ^ 1]);
-  mfma_slot(F[CUR], acc);
+  mfma_slot<SW>(F[CUR], acc);
 #pragma unroll
   for (int q = 0; q < 16; ++q) {
     __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
@@ -153,7 +159,7 @@ __device__ __forceinline__ void loop_step(Ring& sm, int i, int n, int kt0, const
 // addr(kt, pa, pb) yields the slice base pointers (row 0, k = 32 kt).
 // Slices are copied global -> LDS five slots ahead; fragments are read one
 // slice ahead into a second register set.
-template <class Addr>
+template <bool SW = false, class Addr>
 __device__ __forceinline__ void mainloop(Ring& sm, int kt0, int kt1, uint32_t lda, uint32_t ldb,
                                          const Addr& addr, f32x16 (&acc)[4][4]) {
   const int tid = threadIdx.x, lane = tid & 63;
@@ -174,17 +180,17 @@ __device__ __forceinline__ void mainloop(Ring& sm, int kt0, int kt1, uint32_t ld
   read_frags(sm, 0, wave, lane, F[0]);
   int i = 0;
   for (; i + 2 < n; i += 2) {
-    loop_step<0>(sm, i, n, kt0, addr, oa, ob, wave, lane, F, acc);
-    loop_step<1>(sm, i + 1, n, kt0, addr, oa, ob, wave, lane, F, acc);
+    loop_step<SW, 0>(sm, i, n, kt0, addr, oa, ob, wave, lane, F, acc);
+    loop_step<SW, 1>(sm, i + 1, n, kt0, addr, oa, ob, wave, lane, F, acc);
   }
   if (n - i == 2) {
-    loop_step<0>(sm, i, n, kt0, addr, oa, ob, wave, lane, F, acc);
+    loop_step<SW, 0>(sm, i, n, kt0, addr, oa, ob, wave, lane, F, acc);
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
       for (int t = 0; t < 8; ++t) F[0][kk][t] = F[1][kk][t];
   }
-  mfma_slot(F[0], acc);
+  mfma_slot<SW>(F[0], acc);
   __syncthreads();
 }
 
@@ -241,6 +247,61 @@ __global__ __launch_bounds__(NTHR, 1) void k_whiten_bf16(const bf16_t* __restric
         const int col = wn * 128 + j * 32 + (lane & 31);
         cb[(size_t)row * Kp + col] = f32_to_bf16(acc[i][j][r]);
       }
+}
+
+// Row norms of the whitened rows, for the rank-one (per-token) form of the
+// updates (Section 5: the weight of token t in one half step is x_t^T A^-1 x_t
+// = ||L^-1 x_t||^2).  Same tiles and k ranges as k_whiten_bf16, with the
+// operands swapped so that every lane holds values of one row; the whitened
+// values are never stored.  part[row][2 cj + wn] receives the sum of squares
+// over the 128 columns of wave column wn of tile column cj.
+__global__ __launch_bounds__(NTHR, 1) void k_whiten_norm_bf16(const bf16_t* __restrict__ X,
+                                                              const bf16_t* __restrict__ Y,
+                                                              const bf16_t* __restrict__ Y2,
+                                                              float* __restrict__ part, uint32_t Kp,
+                                                              const int* st) {
+  if (ff_halted(st)) return;
+  __shared__ Ring sm;
+  const uint32_t ncol = Kp / TM;
+  const uint32_t t = xcd_remap(blockIdx.x, gridDim.x);
+  const uint32_t rb = t / ncol;
+  const uint32_t cj = ncol - 1 - t % ncol;
+  const int kt1 = (int)((cj + 1) * (TM / TK));
+  const bf16_t* xa = X + (size_t)rb * TM * Kp;
+  f32x16 acc[4][4];
+  zero_acc(acc);
+  {
+    const bf16_t* yb = Y + (size_t)cj * TM * Kp;
+    auto addr = [&](int kt, const bf16_t*& pa, const bf16_t*& pb) {
+      pa = xa + kt * TK;
+      pb = yb + kt * TK;
+    };
+    mainloop<true>(sm, 0, kt1, Kp, Kp, addr, acc);
+  }
+  if (Y2 != nullptr) {
+    const bf16_t* yb = Y2 + (size_t)cj * TM * Kp;
+    auto addr = [&](int kt, const bf16_t*& pa, const bf16_t*& pb) {
+      pa = xa + kt * TK;
+      pb = yb + kt * TK;
+    };
+    mainloop<true>(sm, 0, kt1, Kp, Kp, addr, acc);
+  }
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int wm = wave >> 1, wn = wave & 1;
+  const uint32_t npart = 2 * ncol;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float s = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s += acc[i][j][r] * acc[i][j][r];
+    s += __shfl_xor(s, 32);  // lanes l and l + 32 hold the two column halves of row l % 32
+    if (lane < 32) {
+      const size_t row = (size_t)rb * TM + wm * 128 + i * 32 + lane;
+      part[row * npart + 2 * cj + wn] = s;
+    }
+  }
 }
 
 // Upper-triangle tile index -> (ti, tj), ti <= tj, row-major over the triangle.
@@ -331,6 +392,16 @@ hipError_t launch_whiten_bf16(const bf16_t* X, const bf16_t* Y, const bf16_t* Y2
   const int64_t tiles = (rows / TM) * (Kp / TM);
   if (tiles > 0x7fffffff) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_whiten_bf16, dim3((uint32_t)tiles), dim3(NTHR), 0, s, X, Y, Y2, C,
+                     (uint32_t)Kp, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_whiten_norm_bf16(const bf16_t* X, const bf16_t* Y, const bf16_t* Y2, float* part,
+                                   int64_t rows, int64_t Kp, const int* st, hipStream_t s) {
+  if (rows <= 0 || Kp <= 0 || rows % TM || Kp % TM || Kp > (1 << 20)) return hipErrorInvalidValue;
+  const int64_t tiles = (rows / TM) * (Kp / TM);
+  if (tiles > 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_whiten_norm_bf16, dim3((uint32_t)tiles), dim3(NTHR), 0, s, X, Y, Y2, part,
                      (uint32_t)Kp, st);
   return hipGetLastError();
 }

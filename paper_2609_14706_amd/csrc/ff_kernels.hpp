@@ -22,6 +22,12 @@ constexpr int kTileBF16 = 256;
 hipError_t launch_whiten_bf16(const bf16_t* X, const bf16_t* Y, const bf16_t* Y2, bf16_t* C,
                               int64_t rows, int64_t Kp, const int* st, hipStream_t s);
 
+// Row norms of the whitened rows without storing them: part[r][2 cj + h]
+// (2 Kp / 256 floats per row) = sum of squares of (X Y^T (+ X Y2^T))[r][.]
+// over the 128 columns h of column tile cj.  Same shape rules as above.
+hipError_t launch_whiten_norm_bf16(const bf16_t* X, const bf16_t* Y, const bf16_t* Y2, float* part,
+                                   int64_t rows, int64_t Kp, const int* st, hipStream_t s);
+
 // Symmetric rank-k product over segmented rows, split over k:
 //   P[z][tile] = partial sums of X X^T for upper tiles (ti <= tj),
 // where row r of X is the concatenation over segments s < nseg of
@@ -105,6 +111,14 @@ hipError_t launch_normalise(float* FA, int64_t n, float* FB, int64_t m, const do
 hipError_t launch_loglik(const double* slotsA, int nA, const double* slotsB, int nB,
                          const double* c, int first_is_B, double m, double n, double N,
                          double* ll_out, const int* st, hipStream_t s);
+
+// w[r] = sum_j P[r][j] (square = 0) or sum_j P[r][j]^2 (square = 1), rows x cols.
+hipError_t launch_row_sums(const float* P, int64_t rows, int64_t cols, int square, float* w,
+                           const int* st, hipStream_t s);
+
+// out (cols_p x rows_p) = transpose(diag(sqrt(w)) M) for M rows_p x cols_p.
+hipError_t launch_scale_transpose(const void* M, const float* w, int64_t rows_p, int64_t cols_p,
+                                  void* out, int elem_bytes, const int* st, hipStream_t s);
 
 // out[0] = sum_i a[i] b[i] (fp64, fixed order), out[1] = 2 sum(slotsA),
 // out[2] = 2 sum(slotsB).  scratch: 512 doubles.

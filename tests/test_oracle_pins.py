@@ -377,3 +377,43 @@ def test_objective_is_mismatch_factor_up_to_the_data_term():
     # rank-deficient H (N < mn): psi is still finite and scale-invariant
     Gs = G[:3]
     assert np.isfinite(oracle.objective(Gs, A, B))
+
+
+# ------------------------------------------------- rank-one (per-token) form
+
+def test_token_half_steps_equal_dense_half_steps_on_materialised_samples():
+    """Section 5's rank-one half steps (weights x^T A^-1 x and g^T B^-1 g)
+    against the dense half steps on G_t = g_t x_t^T, at arbitrary factors;
+    a whole run (both orders, damping) against the dense oracle; and the
+    token log-likelihood and objective against the dense ones."""
+    rng = np.random.default_rng(31)
+    T, m, n = 400, 5, 7
+    x = rng.standard_normal((T, n)) * np.linspace(0.5, 2.0, n)
+    g = rng.standard_normal((T, m)) @ rand_spd(m, rng, 4)
+    G = oracle.materialise(x, g)
+    A, B = rand_spd(n, rng, 6), rand_spd(m, rng, 9)
+    assert np.allclose(oracle.half_step_B_tokens(x, g, A), oracle.half_step_B(G, A), rtol=1e-12, atol=0)
+    assert np.allclose(oracle.half_step_A_tokens(x, g, B), oracle.half_step_A(G, B), rtol=1e-12, atol=0)
+    for order, kappa in (("B_FIRST", 0.0), ("A_FIRST", 0.1)):
+        rt = oracle.flipflop_tokens(x, g, 6, order=order, damping=kappa)
+        rd = oracle.flipflop(G, 6, order=order, damping=kappa)
+        assert oracle.kron_rel_error(rt.A, rt.B, rd.A, rd.B) < 1e-12
+    r = oracle.flipflop_tokens(x, g, 4)
+    assert abs(oracle.loglik_tokens(x, g, r.A, r.B) - oracle.loglik(G, r.A, r.B)) < 1e-9 * T * m * n
+    assert abs(oracle.objective_tokens(x, g, A, B) - oracle.objective(G, A, B)) < 1e-12
+
+
+def test_token_fixed_point_recovers_independent_kronecker_factors():
+    """Inputs and gradients independent (one component): H = E[xx^T] (x)
+    E[gg^T] is a Kronecker product, and the fixed point is that product up
+    to scale (error shrinking like T^-1/2)."""
+    rng = np.random.default_rng(32)
+    m, n = 4, 6
+    At, Bt = rand_spd(n, rng, 5), rand_spd(m, rng, 5)
+    errs = []
+    for T in (4000, 64000):
+        x = rng.standard_normal((T, n)) @ np.linalg.cholesky(At).T
+        g = rng.standard_normal((T, m)) @ np.linalg.cholesky(Bt).T
+        r = oracle.flipflop_tokens(x, g, 30)
+        errs.append(oracle.kron_rel_error(r.A, r.B, At, Bt))
+    assert errs[1] < 0.5 * errs[0] and errs[1] < 0.03
