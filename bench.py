@@ -88,13 +88,45 @@ def cpu_baseline(G, w, budget_s: float):
                       f"of {w.name}, {t_total:.1f} s, scaled to a full iteration ({per_iter:.1f} s)"}
 
 
+def cpu_baseline_tokens(x, g, w, budget_s: float):
+    """Oracle time of one iteration of the per-token form, from a bounded
+    number of tokens: both half steps on the first k tokens (k grows in
+    blocks of 4096 until the budget is used), against fixed SPD factors,
+    scaled by T / k."""
+    import numpy as np
+    import torch
+    from threadpoolctl import threadpool_info
+
+    import oracle
+
+    In, Im = np.eye(w.n), np.eye(w.m)
+    k, t_total = 0, 0.0
+    while k < w.T and (t_total < budget_s or k == 0):
+        kb = min(4096, w.T - k)
+        xs = x[k:k + kb].view(torch.int16).cpu().numpy().view(np.uint16) if x.dtype == torch.bfloat16 \
+            else x[k:k + kb].cpu().numpy()
+        gs = g[k:k + kb].view(torch.int16).cpu().numpy().view(np.uint16) if g.dtype == torch.bfloat16 \
+            else g[k:k + kb].cpu().numpy()
+        t0 = time.perf_counter()
+        oracle.half_step_B_tokens(xs, gs, In)
+        oracle.half_step_A_tokens(xs, gs, Im)
+        t_total += time.perf_counter() - t0
+        k += kb
+    per_iter = t_total * w.T / k
+    cores = max((i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"),
+                default=1)
+    return {"value": 1.0 / per_iter, "unit": "iter/s", "cores": cores, "kind": "oracle",
+            "sample": f"both fp64 rank-one half steps on {k} of {w.T} tokens of {w.name}, "
+                      f"{t_total:.1f} s, scaled to a full iteration ({per_iter:.1f} s)"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10, help="timed flip-flop iterations")
     ap.add_argument("--warmup", type=int, default=2, help="untimed iterations on a separate handle")
     ap.add_argument("--workload", default="attn",
-                    help="tiny | attn | mlp_up | mlp_down | mlp_large")
+                    help="tiny | attn | mlp_up | mlp_down | mlp_large | tokens_tiny | tokens_attn")
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--whiten-split", type=int, default=1)
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time")
@@ -113,18 +145,29 @@ def main():
     import paper_2609_14706_amd as ffe
 
     dev = torch.device("cuda:0")
-    w = synth.workload(args.workload)
+    tokens = args.workload.startswith("tokens")
     t0 = time.perf_counter()
-    G = synth.generate_device(w, seed=args.seed, device=dev)
+    if tokens:
+        w = synth.token_workload(args.workload)
+        x, g = synth.generate_tokens_device(w, seed=args.seed, device=dev)
+        src = {"tokens": (x, g)}
+        nbytes_in = (x.numel() + g.numel()) * x.element_size()
+        N = w.T
+    else:
+        w = synth.workload(args.workload)
+        G = synth.generate_device(w, seed=args.seed, device=dev)
+        src = {"G": G}
+        nbytes_in = G.numel() * G.element_size()
+        N = w.N
     torch.cuda.synchronize()
-    print(f"[bench] generated {w.name} ({G.numel() * G.element_size() / 1e9:.2f} GB) in "
+    print(f"[bench] generated {w.name} ({nbytes_in / 1e9:.2f} GB) in "
           f"{time.perf_counter() - t0:.1f} s", file=sys.stderr, flush=True)
-    nbytes = ffe.FlipFlop.workspace_bytes(w.m, w.n, w.N, w.dtype, args.whiten_split)
+    nbytes = ffe.FlipFlop.workspace_bytes(w.m, w.n, N, w.dtype, args.whiten_split, rank1=tokens)
     ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
 
     if args.warmup > 0:
-        f = ffe.FlipFlop(G, whiten_split=args.whiten_split, workspace=ws, stream=stream)
+        f = ffe.FlipFlop(**src, whiten_split=args.whiten_split, workspace=ws, stream=stream)
         f.iterate(args.warmup)
         f.close()
     torch.cuda.synchronize()
@@ -134,7 +177,7 @@ def main():
     ev1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     ev0.record(stream)
-    f = ffe.FlipFlop(G, whiten_split=args.whiten_split, workspace=ws, stream=stream)
+    f = ffe.FlipFlop(**src, whiten_split=args.whiten_split, workspace=ws, stream=stream)
     f.set_timing(True)
     ll = f.iterate(args.steps)
     ev1.record(stream)
@@ -154,7 +197,8 @@ def main():
     dom = max(("whiten", "syrk"), key=lambda k: kern[k][1])
     n_l, ms_l, fl_l = kern[dom]
     achieved = fl_l / (ms_l * 1e-3) / 1e12 if ms_l > 0 else 0.0
-    roofline = {"bound": "mfma", "kernel": {"whiten": "k_whiten_bf16", "syrk": "k_syrk_bf16"}[dom]
+    wname = "k_whiten_norm_bf16" if tokens else "k_whiten_bf16"
+    roofline = {"bound": "mfma", "kernel": {"whiten": wname, "syrk": "k_syrk_bf16"}[dom]
                 if w.dtype == "bf16" else "k_gemm_f32",
                 "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4), "traffic": None,
@@ -165,7 +209,8 @@ def main():
     if w.dtype == "bf16":
         roofline["traffic"] = recorded_traffic(roofline["kernel"], w.name)
     out = {
-        "metric": METRIC,
+        "metric": METRIC if not tokens else
+        f"flip-flop iter/s + TFLOP/s, per-token form, m={w.m} n={w.n} T={w.T}",
         "value": round(iters_per_s, 4),
         "unit": "iter/s",
         "n_gpus": 1,
@@ -177,7 +222,7 @@ def main():
         "vs_baseline": None,
         "dtype": w.dtype,
         "data": "synthetic",
-        "config": {"workload": w.name, "m": w.m, "n": w.n, "N": w.N,
+        "config": {"workload": w.name, "m": w.m, "n": w.n, ("T" if tokens else "N"): N,
                    "timed_job": f"ff_init + {args.steps} iterations",
                    "whiten_split": args.whiten_split},
         "tflops": round(tflops, 2),
@@ -190,7 +235,8 @@ def main():
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the fp64 oracle on host cores", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(G, w, args.cpu_budget)
+        out["cpu_baseline"] = (cpu_baseline_tokens(x, g, w, args.cpu_budget) if tokens
+                               else cpu_baseline(G, w, args.cpu_budget))
     print(json.dumps(out), flush=True)
 
 

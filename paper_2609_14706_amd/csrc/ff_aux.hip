@@ -64,13 +64,16 @@ __global__ __launch_bounds__(256) void k_row_sums(const float* __restrict__ P, i
   if (lane == 0) w[r] = (float)s;
 }
 
-// out[c][r] = sqrt(w[r]) * M[r][c] for the rows_p x cols_p matrix M: the
-// rows of M (tokens) weighted and turned into the k axis of a symmetric
-// product.  64 x 64 tiles through LDS.
+// sqrt(w[r]) * M[r][c] for the rows_p x cols_p matrix M: the rows of M
+// (tokens) weighted and turned into the k axis of a symmetric product, in
+// segments of seg tokens: element (c, r) goes to
+// out[(r / seg) * cols_p * seg + c * seg + r % seg], so that the product reads
+// short rows (seg elements) instead of rows_p-long ones.  64 x 64 tiles
+// through LDS; seg is a multiple of 64.
 template <typename T>
 __global__ __launch_bounds__(256) void k_scale_transpose(const T* __restrict__ M,
                                                          const float* __restrict__ w,
-                                                         int64_t rows_p, int64_t cols_p,
+                                                         int64_t rows_p, int64_t cols_p, int64_t seg,
                                                          T* __restrict__ out, const int* st) {
   if (ff_halted(st)) return;
   __shared__ float tile[64][65];
@@ -83,9 +86,10 @@ __global__ __launch_bounds__(256) void k_scale_transpose(const T* __restrict__ M
     tile[y][tx] = v;
   }
   __syncthreads();
+  T* o = out + (r0 / seg) * cols_p * seg + (r0 % seg);
   for (int y = ty; y < 64; y += 4) {
     const int64_t c = c0 + y, r = r0 + tx;
-    if (c < cols_p && r < rows_p) out[c * rows_p + r] = Elem<T>::from_f32(tile[tx][y]);
+    if (c < cols_p && r < rows_p) o[c * seg + tx] = Elem<T>::from_f32(tile[tx][y]);
   }
 }
 
@@ -270,17 +274,18 @@ hipError_t launch_row_sums(const float* P, int64_t rows, int64_t cols, int squar
 }
 
 hipError_t launch_scale_transpose(const void* M, const float* w, int64_t rows_p, int64_t cols_p,
-                                  void* out, int elem_bytes, const int* st, hipStream_t s) {
-  if (rows_p < 1 || cols_p < 1) return hipErrorInvalidValue;
+                                  int64_t seg, void* out, int elem_bytes, const int* st,
+                                  hipStream_t s) {
+  if (rows_p < 1 || cols_p < 1 || seg < 64 || seg % 64 || rows_p % seg) return hipErrorInvalidValue;
   const int64_t gx = (cols_p + 63) / 64, gy = (rows_p + 63) / 64;
   if (gx > 0x7fffffff || gy > 65535) return hipErrorInvalidValue;
   const dim3 grid((uint32_t)gx, (uint32_t)gy);
   if (elem_bytes == 2)
     hipLaunchKernelGGL(k_scale_transpose<bf16_t>, grid, dim3(256), 0, s, (const bf16_t*)M, w,
-                       rows_p, cols_p, (bf16_t*)out, st);
+                       rows_p, cols_p, seg, (bf16_t*)out, st);
   else if (elem_bytes == 4)
     hipLaunchKernelGGL(k_scale_transpose<float>, grid, dim3(256), 0, s, (const float*)M, w, rows_p,
-                       cols_p, (float*)out, st);
+                       cols_p, seg, (float*)out, st);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

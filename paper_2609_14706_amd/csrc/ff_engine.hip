@@ -43,6 +43,7 @@ ff_status fail(ff_status s, const std::string& msg) {
   } while (0)
 
 constexpr size_t kAlign = 256;
+constexpr int64_t kTokenSeg = 256;  // tokens per segment of the weighted, transposed tokens
 constexpr int kLLCap = 1024;      // log-likelihood values per device ring
 constexpr int kTimedKernels = 4;  // whiten, symmetric product, reduction, factorisation
 
@@ -138,7 +139,7 @@ Layout make_layout(const ff_config* c) {
   L.n_p = round_up(n, g);
   L.rank1 = c->form == FF_SAMPLES_RANK1;
   L.own_gx = L.rank1 || !(L.m_p == m && L.n_p == n);
-  L.T_p = L.rank1 ? round_up(N, g) : 0;
+  L.T_p = L.rank1 ? round_up(N, 256) : 0;  // a multiple of the token segment (and of g)
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
@@ -363,15 +364,17 @@ ff_status update_rank1(ff_handle_s* h, Side& s, Side& p, int slot, bool finish) 
   const int64_t T_p = h->lay.T_p;
   const double scale = 1.0 / ((double)h->N * (double)p.dim);
   const double sflop = (double)h->N * s.dim * s.dim;
+  // tokens in segments of kTokenSeg: the product streams short rows
+  const int64_t seg = kTokenSeg, nseg = T_p / kTokenSeg;
   {
     Timed t(h, 2, 0.0);
-    FF_HIP(launch_scale_transpose(U, wbuf, T_p, s.dim_p, h->S, h->elem, h->st, h->stream));
+    FF_HIP(launch_scale_transpose(U, wbuf, T_p, s.dim_p, seg, h->S, h->elem, h->st, h->stream));
   }
   if (h->bf16) {
     {
       Timed t(h, 1, sflop);
-      FF_HIP(launch_syrk_bf16((const bf16_t*)h->S, s.dim_p, T_p, s.dim_p * T_p, 1, s.splits, h->P,
-                              h->st, h->stream));
+      FF_HIP(launch_syrk_bf16((const bf16_t*)h->S, s.dim_p, seg, s.dim_p * seg, nseg, s.splits,
+                              h->P, h->st, h->stream));
     }
     Timed t(h, 2, 0.0);
     FF_HIP(launch_reduce_frag(h->P, s.splits, s.dim_p, s.F[slot], s.dim, scale, h->st, h->stream));
@@ -380,11 +383,11 @@ ff_status update_rank1(ff_handle_s* h, Side& s, Side& p, int slot, bool finish) 
       Timed t(h, 1, sflop);
       GemmF32 q{};
       q.st = h->st;
-      q.A = (const float*)h->S; q.lda = T_p; q.transA = 0;
-      q.B = (const float*)h->S; q.ldb = T_p; q.transB = 1;
+      q.A = (const float*)h->S; q.lda = seg; q.transA = 0;
+      q.B = (const float*)h->S; q.ldb = seg; q.transB = 1;
       q.C = h->P; q.ldc = s.dim_p; q.sC = s.dim_p * s.dim_p;
       q.M = s.dim_p; q.N = s.dim_p; q.K = T_p;
-      q.kseg = T_p; q.segA = q.segB = 0;
+      q.kseg = seg; q.segA = q.segB = s.dim_p * seg;
       q.alpha = 1.f; q.beta = 0.f; q.flags = kCLower; q.ksplit = s.splits;
       FF_HIP(launch_gemm_f32(q, 1, h->stream));
     }

@@ -116,9 +116,12 @@ hipError_t launch_loglik(const double* slotsA, int nA, const double* slotsB, int
 hipError_t launch_row_sums(const float* P, int64_t rows, int64_t cols, int square, float* w,
                            const int* st, hipStream_t s);
 
-// out (cols_p x rows_p) = transpose(diag(sqrt(w)) M) for M rows_p x cols_p.
+// transpose(diag(sqrt(w)) M) for M rows_p x cols_p, stored as rows_p / seg
+// segments of cols_p x seg (element (c, r) at
+// (r / seg) * cols_p * seg + c * seg + r % seg); seg | rows_p, 64 | seg.
 hipError_t launch_scale_transpose(const void* M, const float* w, int64_t rows_p, int64_t cols_p,
-                                  void* out, int elem_bytes, const int* st, hipStream_t s);
+                                  int64_t seg, void* out, int elem_bytes, const int* st,
+                                  hipStream_t s);
 
 // out[0] = sum_i a[i] b[i] (fp64, fixed order), out[1] = 2 sum(slotsA),
 // out[2] = 2 sum(slotsB).  scratch: 512 doubles.

@@ -75,3 +75,66 @@ def test_tokens_bf16_multi_tile(gpu, split):
     print(f"tokens bf16 600x520 T=6000 split={split}: rel err {err:.3e}")
     assert done == w.iters and err < TOL_BF16
     assert abs(psi - oracle.objective_tokens(d.x, d.g, ref.A, ref.B)) < TOL_BF16
+
+
+def test_tokens_attn_fullsize(gpu):
+    """The paper's calibration size (256 x 2048 = 524288 tokens) at the
+    attention width 4096 x 4096, bf16: sampled rows of the first B update
+    (with A = I) from the token oracle, then properties after 10 iterations:
+    trace normalisation, symmetry, positive definiteness, the likelihood
+    rising then flat, the trace identity (1/(T m n)) sum_t w_t v_t = 1, and
+    the device log-likelihood against an fp64 evaluation from the factors."""
+    import torch
+    import paper_2609_14706_amd as ffe
+    w = synth.token_workload("tokens_attn")
+    print(f"[{w.name}] generating on the device", flush=True)
+    x, g = synth.generate_tokens_device(w, device=gpu)
+    f = ffe.FlipFlop(tokens=(x, g))
+    f.iterate(1)
+    _, B1 = f.factors()
+    f.close()
+    rows = np.array([0, 1, 1000, 2049, 4095])
+    print(f"[{w.name}] oracle rows of the first B update", flush=True)
+    xh = x.view(torch.int16).cpu().numpy().view(np.uint16)
+    gh = g.view(torch.int16).cpu().numpy().view(np.uint16)
+    ref = oracle.half_step_B_tokens_rows(xh, gh, None, rows)
+    del xh, gh
+    got = B1.double().cpu().numpy()[rows]
+    # Unlike the dense form (where A = I makes the first update exact up to
+    # fp32 accumulation), the tokens scaled by sqrt(w_t) are rounded to bf16
+    # before the product, so the bf16 bar applies here (measured ~8e-5).
+    for k, r in enumerate(rows):
+        a = got[k] / got[k, r]
+        b = ref[k] / ref[k, r]
+        err = np.linalg.norm(a - b) / np.linalg.norm(b)
+        print(f"[{w.name}] row {r}: rel err {err:.3e}", flush=True)
+        assert err < TOL_BF16, (r, err)
+    print(f"[{w.name}] {w.iters} iterations", flush=True)
+    f = ffe.FlipFlop(tokens=(x, g))
+    ll = f.iterate(w.iters)
+    A, B = f.factors()
+    f.close()
+    print(f"[{w.name}] loglik per iteration: {ll}", flush=True)
+    Tmn = w.T * w.m * w.n
+    assert abs(float(torch.trace(A.double())) - w.n) < 1e-6 * w.n
+    assert bool((A == A.T).all()) and bool((B == B.T).all())
+    LA = torch.linalg.cholesky(A.double())
+    LB = torch.linalg.cholesky(B.double())
+    assert ll[1] > ll[0] and ll[-1] > ll[0]
+    tail = ll[w.iters // 2:]
+    assert max(tail) - min(tail) < 1e-4 * Tmn
+    tot = 0.0
+    LA32, LB32 = LA.float(), LB.float()
+    for t0 in range(0, w.T, 65536):
+        xs = torch.linalg.solve_triangular(LA32, x[t0:t0 + 65536].float().T, upper=False)
+        gs = torch.linalg.solve_triangular(LB32, g[t0:t0 + 65536].float().T, upper=False)
+        tot += float(((xs.double() ** 2).sum(0) * (gs.double() ** 2).sum(0)).sum())
+    t = tot / Tmn
+    print(f"[{w.name}] trace identity: {t:.6f}", flush=True)
+    assert abs(t - 1.0) < 5e-3
+    ldA = 2.0 * float(torch.log(torch.diagonal(LA)).sum())
+    ldB = 2.0 * float(torch.log(torch.diagonal(LB)).sum())
+    llref = -0.5 * w.T * (w.m * ldA + w.n * ldB) - 0.5 * Tmn * (1.0 + np.log(2 * np.pi))
+    bound = 32 * float(np.finfo(np.float32).eps) * Tmn      # fp32 pivots, as for the dense form
+    print(f"[{w.name}] loglik device {ll[-1]:.9e} fp64 {llref:.9e} (bound {bound:.3e})", flush=True)
+    assert abs(ll[-1] - llref) < bound
