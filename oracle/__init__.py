@@ -12,6 +12,8 @@ from .flipflop import (FlipFlopResult, NotSPDError, as_f64_samples, half_step_B,
                        half_step_A, normalise, damp, flipflop, loglik, objective)
 from .metrics import kron_rel_error, kron_rel_error_scale_free, trace_identity
 from .kron import kron_apply, mismatch_factor
+from .waterkron import (rev_cholesky, normalised_inverse, waterfilling_scales, gptq,
+                        two_sided_gptq, distortion)
 from .tokens import (half_step_A_tokens, half_step_B_tokens, half_step_B_tokens_rows, flipflop_tokens, loglik_tokens,
                      objective_tokens, materialise, token_weights)
 
@@ -19,4 +21,6 @@ __all__ = ["FlipFlopResult", "NotSPDError", "as_f64_samples", "half_step_B", "ha
            "half_step_A", "normalise", "damp", "flipflop", "loglik", "objective",
            "kron_rel_error", "kron_rel_error_scale_free", "trace_identity",
            "kron_apply", "mismatch_factor", "half_step_A_tokens", "half_step_B_tokens", "half_step_B_tokens_rows",
-           "flipflop_tokens", "loglik_tokens", "objective_tokens", "materialise", "token_weights"]
+           "flipflop_tokens", "loglik_tokens", "objective_tokens", "materialise", "token_weights",
+           "rev_cholesky", "normalised_inverse", "waterfilling_scales", "gptq", "two_sided_gptq",
+           "distortion"]

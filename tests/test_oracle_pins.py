@@ -417,3 +417,64 @@ def test_token_fixed_point_recovers_independent_kronecker_factors():
         r = oracle.flipflop_tokens(x, g, 30)
         errs.append(oracle.kron_rel_error(r.A, r.B, At, Bt))
     assert errs[1] < 0.5 * errs[0] and errs[1] < 0.03
+
+
+# ------------------------------------------------------------- WaterKron
+
+def test_rev_cholesky_definition_and_inverse():
+    """RevCholesky(M) is lower triangular with L^T L = M; its inverse is the
+    Cholesky factor of M^-1 (Section 3 background)."""
+    rng = np.random.default_rng(41)
+    M = rand_spd(7, rng, 50)
+    L = oracle.rev_cholesky(M)
+    assert np.allclose(np.triu(L, 1), 0) and np.all(np.diag(L) > 0)
+    assert np.allclose(L.T @ L, M, atol=1e-12)
+    assert np.allclose(np.linalg.inv(L), np.linalg.cholesky(np.linalg.inv(M)), atol=1e-10)
+
+
+def test_waterfilling_scales_of_the_babai_figure():
+    """The Babai-rounding figure: L = [[2, 0], [1, 3]] gives the optimal input
+    scales (3/sqrt 6, 2/sqrt 6) (volume-preserving, alpha_j proportional to
+    1/L_jj)."""
+    L = np.array([[2.0, 0.0], [1.0, 3.0]])
+    alpha, beta = oracle.waterfilling_scales(L.T @ L, np.eye(1), 1.0)
+    assert np.allclose(alpha, [3 / np.sqrt(6), 2 / np.sqrt(6)], atol=1e-14)
+    assert np.allclose(beta, [1.0])
+
+
+def test_two_sided_gptq_reductions():
+    """Algorithm 2 with B = I is Algorithm 1; Algorithm 2 is Algorithm 1 on
+    vec(W)^T with the Kronecker factor A (x) B and scales alpha (x) beta (the
+    proof of the achievability corollary); the error lies in the Babai cell:
+    |(L^B (V - W) L^A^T)_ij| <= alpha_j beta_i L^A_jj L^B_ii / 2."""
+    rng = np.random.default_rng(42)
+    m, n = 5, 6
+    A, B = rand_spd(n, rng, 20), rand_spd(m, rng, 30)
+    W = rng.standard_normal((m, n))
+    alpha, beta = oracle.waterfilling_scales(A, B, 0.3)
+    Z1, _ = oracle.gptq(W, A, alpha, np.full(m, beta[0]))
+    Z2, _ = oracle.two_sided_gptq(W, A, np.eye(m), alpha, np.full(m, beta[0]))
+    assert np.array_equal(Z1, Z2)
+    Z, V = oracle.two_sided_gptq(W, A, B, alpha, beta)
+    wv = W.reshape(1, -1, order="F")
+    Zv, _ = oracle.gptq(wv, np.kron(A, B), np.kron(alpha, beta), np.ones(1))
+    assert np.array_equal(Zv.reshape(m, n, order="F"), Z)
+    LA, LB = oracle.rev_cholesky(A), oracle.rev_cholesky(B)
+    Err = LB @ (V - W) @ LA.T
+    cell = np.outer(beta * np.diag(LB), alpha * np.diag(LA)) / 2
+    assert np.all(np.abs(Err) <= cell * (1 + 1e-9))
+
+
+def test_high_rate_distortion():
+    """Achievability corollary: D_{A,B} -> (gamma^2 / 12) |A|^(1/n) |B|^(1/m)
+    as gamma -> 0 (Gaussian W)."""
+    rng = np.random.default_rng(43)
+    m, n = 24, 20
+    A, B = rand_spd(n, rng, 40), rand_spd(m, rng, 60)
+    W = rng.standard_normal((m, n))
+    gamma = 1e-3
+    alpha, beta = oracle.waterfilling_scales(A, B, gamma)
+    _, V = oracle.two_sided_gptq(W, A, B, alpha, beta)
+    D = oracle.distortion(V, W, A, B)
+    pred = gamma ** 2 / 12 * np.exp(np.linalg.slogdet(A)[1] / n + np.linalg.slogdet(B)[1] / m)
+    assert abs(D / pred - 1.0) < 0.1
