@@ -170,17 +170,62 @@ ff_status ff_kron_apply(ff_handle h, const float* X, float* Y, int64_t batch,
  * FF_ERR_HIP. */
 ff_status ff_objective(ff_handle h, const float* A, const float* B, double* psi);
 
+/* Scales of the quantisation grid for ff_quantize.  FF_SCALES_WATERFILL:
+ * computed by Corollary 3.2, alpha_j = sqrt(gamma) |A|^(1/2n) / L^A_jj and
+ * beta_i = sqrt(gamma) |B|^(1/2m) / L^B_ii with L = RevCholesky (the lower
+ * triangular L with positive diagonal and L^T L = M, Section 2), and written
+ * to alpha and beta.  FF_SCALES_GIVEN: alpha and beta are inputs (Algorithm 2
+ * takes them as given). */
+typedef enum { FF_SCALES_WATERFILL = 0, FF_SCALES_GIVEN = 1 } ff_scale_mode;
+
+/* Bytes of the device workspace ff_quantize needs for an m x n weight
+ * matrix.  Errors: FF_ERR_INVALID_ARG (m or n < 1 or > 1048576, bytes NULL). */
+ff_status ff_quantize_workspace_size(int64_t m, int64_t n, size_t* bytes);
+
+/* WaterKron (Section 3): two-sided GPTQ, Algorithm 2, of the weights W
+ * (m x n) under the Kronecker Hessian A (x) B, on the grid
+ * V = beta alpha^T (.) Z (Section 2.1).  Entry by entry (columns in order,
+ * rows in order within a column) the current value is rounded to the nearest
+ * grid point (ties to even) and the error is spread over the entries below
+ * and to the right with the outer product of the columns of the normalised
+ * inverse factors, L^-1 with each column divided by its diagonal entry, of
+ * L^B = RevCholesky(B) and L^A = RevCholesky(A).  The result is the one whose
+ * transformed error E = (L~B)^-1 (V - W) (L~A)^-T lies in the cell
+ * |E_ij| <= alpha_j beta_i / 2 (L~ the normalised inverses), unique up to ties.
+ *
+ * h: the handle whose shape (m, n) is used.  W: DEVICE fp32 m x n row-major.
+ * A (n x n), B (m x m): DEVICE fp32 symmetric positive definite (lower
+ * triangles read); NULL means the handle's current factor.  gamma > 0: the
+ * step parameter of FF_SCALES_WATERFILL (ignored for FF_SCALES_GIVEN).
+ * alpha (n), beta (m): DEVICE fp32, outputs or inputs by mode; given scales
+ * must be finite and > 0.  Z: DEVICE int32 m x n, the integer codes (exact
+ * while |Z| < 2^24).  V: DEVICE fp32 m x n, the quantised weights, or NULL.
+ * distortion: HOST, receives D_{A,B} = ||L^B (V - W) L^A^T||_F^2 / (m n)
+ * (Section 2.3), or NULL.  workspace: DEVICE, 256-byte aligned, at least
+ * ff_quantize_workspace_size(m, n) bytes, owned by the caller, contents
+ * undefined afterwards.  The factorisations run in fp32 on the handle's
+ * stream; the handle's factors are untouched (the next ff_iterate
+ * refactorises them).  Synchronises the stream.
+ * Errors: FF_ERR_INVALID_ARG, FF_ERR_WORKSPACE, FF_ERR_NOT_SPD (A or B not
+ * positive definite), FF_ERR_HIP. */
+ff_status ff_quantize(ff_handle h, const float* W, const float* A, const float* B,
+                      double gamma, ff_scale_mode mode, float* alpha, float* beta, int32_t* Z,
+                      float* V, double* distortion, void* workspace, size_t workspace_bytes);
+
 /* Release the handle (host memory only; waits for the handle's stream).
  * NULL is accepted. */
 ff_status ff_destroy(ff_handle h);
 
 /* Measurement hook (not needed for estimation).  With timing enabled,
- * ff_iterate brackets each launch of the main kernels with HIP events on the
- * handle's stream and accumulates their durations and algorithmic flop
- * counts; enabling resets the counters.  Kernel ids: 0 = whitening
+ * ff_iterate and ff_quantize bracket each launch of the main kernels with HIP
+ * events on the handle's stream and accumulate their durations and
+ * algorithmic flop counts; enabling resets the counters.  Kernel ids: 0 = whitening
  * (N m n^2 or N m^2 n flop per launch), 1 = symmetric product over the
  * stacked samples (N n m^2 or N m n^2), 2 = reduction of its partial sums
- * (0 flop), 3 = Cholesky + inverse of one factor (dim^3 / 3 flop).
+ * (0 flop), 3 = Cholesky + inverse of one factor (dim^3 / 3 flop), 4 = one
+ * launch (one anti-diagonal of 64 x 64 tiles) of the ff_quantize sweep; the
+ * m^2 n + m n^2 flop of the products that spread the rounding errors are
+ * shared evenly over its ceil(m/64) + ceil(n/64) - 1 launches.
  * Errors: FF_ERR_INVALID_ARG, FF_ERR_HIP. */
 ff_status ff_set_timing(ff_handle h, int enable);
 ff_status ff_kernel_timing(ff_handle h, int kernel, int64_t* launches, double* total_ms,

@@ -19,7 +19,8 @@ FF_F32, FF_BF16 = 0, 1
 FF_ORDER_B_FIRST, FF_ORDER_A_FIRST = 0, 1
 FF_APPLY, FF_APPLY_INV = 0, 1
 FF_SAMPLES_DENSE, FF_SAMPLES_RANK1 = 0, 1
-KERNEL_IDS = {"whiten": 0, "syrk": 1, "reduce": 2, "cholinv": 3}
+FF_SCALES_WATERFILL, FF_SCALES_GIVEN = 0, 1
+KERNEL_IDS = {"whiten": 0, "syrk": 1, "reduce": 2, "cholinv": 3, "quant_diag": 4}
 
 
 class ff_config(ctypes.Structure):
@@ -64,6 +65,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "ff_factors": (st, [H, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int]),
         "ff_kron_apply": (st, [H, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int]),
         "ff_objective": (st, [H, ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(ctypes.c_double)]),
+        "ff_quantize_workspace_size": (st, [ctypes.c_int64, ctypes.c_int64,
+                                            ctypes.POINTER(ctypes.c_size_t)]),
+        "ff_quantize": (st, [H, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_double,
+                             ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                             ctypes.c_void_p, ctypes.POINTER(ctypes.c_double), ctypes.c_void_p,
+                             ctypes.c_size_t]),
         "ff_destroy": (st, [H]),
         "ff_set_timing": (st, [H, ctypes.c_int]),
         "ff_kernel_timing": (st, [H, ctypes.c_int, ctypes.POINTER(ctypes.c_int64),
@@ -142,6 +149,20 @@ def ff_kron_apply(h, X_ptr: int, Y_ptr: int, batch: int, mode: int):
 def ff_objective(h, A_ptr, B_ptr) -> float:
     out = ctypes.c_double(0.0)
     _check(load_library().ff_objective(h, A_ptr, B_ptr, ctypes.byref(out)))
+    return out.value
+
+
+def ff_quantize_workspace_size(m: int, n: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load_library().ff_quantize_workspace_size(m, n, ctypes.byref(out)))
+    return out.value
+
+
+def ff_quantize(h, W_ptr, A_ptr, B_ptr, gamma: float, mode: int, alpha_ptr, beta_ptr, Z_ptr,
+                V_ptr, ws_ptr, ws_bytes: int) -> float:
+    out = ctypes.c_double(0.0)
+    _check(load_library().ff_quantize(h, W_ptr, A_ptr, B_ptr, float(gamma), mode, alpha_ptr,
+                                      beta_ptr, Z_ptr, V_ptr, ctypes.byref(out), ws_ptr, ws_bytes))
     return out.value
 
 
@@ -304,6 +325,54 @@ class FlipFlop:
         pa, pb = ptr(A, self.n), ptr(B, self.m)
         torch.cuda.current_stream(self.device).synchronize()
         return ff_objective(self.h, pa, pb)
+
+    def quantize(self, W, A=None, B=None, *, gamma=None, alpha=None, beta=None, workspace=None):
+        """WaterKron quantisation of W (m, n): two-sided GPTQ (Algorithm 2)
+        under A (x) B (default: the current factors).  Give either gamma (the
+        Corollary 3.2 waterfilling scales are computed) or alpha (n) and
+        beta (m).  Returns (Z int32, V fp32, alpha, beta, distortion D_{A,B});
+        see ff_quantize."""
+        import torch
+        if (gamma is None) == (alpha is None or beta is None):
+            raise ValueError("give either gamma or both alpha and beta")
+        dev = self.device
+        keep = []
+
+        def dev32(M, shape, name):
+            M = M.to(device=dev, dtype=torch.float32).contiguous()
+            if tuple(M.shape) != shape:
+                raise ValueError(f"{name} must have shape {shape}")
+            keep.append(M)
+            return M
+        W = dev32(W, (self.m, self.n), "W")
+        pa = None if A is None else dev32(A, (self.n, self.n), "A").data_ptr()
+        pb = None if B is None else dev32(B, (self.m, self.m), "B").data_ptr()
+        if gamma is None:
+            al = dev32(alpha, (self.n,), "alpha").clone()
+            be = dev32(beta, (self.m,), "beta").clone()
+            mode, g = FF_SCALES_GIVEN, 0.0
+        else:
+            al = torch.empty(self.n, dtype=torch.float32, device=dev)
+            be = torch.empty(self.m, dtype=torch.float32, device=dev)
+            mode, g = FF_SCALES_WATERFILL, float(gamma)
+        Z = torch.empty((self.m, self.n), dtype=torch.int32, device=dev)
+        V = torch.empty((self.m, self.n), dtype=torch.float32, device=dev)
+        nbytes = ff_quantize_workspace_size(self.m, self.n)
+        if workspace is None:
+            workspace = torch.empty(nbytes + 256, dtype=torch.uint8, device=dev)
+        elif (workspace.device != dev or workspace.dtype != torch.uint8
+              or workspace.numel() < nbytes + 256):
+            raise ValueError(f"workspace must be a uint8 tensor of >= {nbytes + 256} bytes on {dev}")
+        base = (workspace.data_ptr() + 255) // 256 * 256
+        torch.cuda.current_stream(dev).synchronize()
+        dist = ff_quantize(self.h, W.data_ptr(), pa, pb, g, mode, al.data_ptr(), be.data_ptr(),
+                           Z.data_ptr(), V.data_ptr(), base, nbytes)
+        return Z, V, al, be, dist
+
+    @staticmethod
+    def quantize_workspace_bytes(m: int, n: int) -> int:
+        """Bytes a caller-provided quantiser workspace tensor needs (slack included)."""
+        return ff_quantize_workspace_size(m, n) + 256
 
     def set_timing(self, enable: bool = True):
         ff_set_timing(self.h, enable)

@@ -17,7 +17,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libff.so")
 BENCH = os.path.join(HERE, "ffbench")
-SOURCES = ["ff_gemm_bf16.hip", "ff_gemm_f32.hip", "ff_chol.hip", "ff_aux.hip", "ff_engine.hip"]
+SOURCES = ["ff_gemm_bf16.hip", "ff_gemm_f32.hip", "ff_chol.hip", "ff_aux.hip", "ff_waterkron.hip",
+           "ff_engine.hip"]
 ARCH = "gfx950"
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

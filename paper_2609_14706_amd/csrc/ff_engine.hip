@@ -45,7 +45,8 @@ ff_status fail(ff_status s, const std::string& msg) {
 constexpr size_t kAlign = 256;
 constexpr int64_t kTokenSeg = 256;  // tokens per segment of the weighted, transposed tokens
 constexpr int kLLCap = 1024;      // log-likelihood values per device ring
-constexpr int kTimedKernels = 4;  // whiten, symmetric product, reduction, factorisation
+constexpr int kTimedKernels = 5;  // whiten, symmetric product, reduction, factorisation,
+                                  // quantiser anti-diagonal
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 int64_t round_up(int64_t x, int64_t g) { return (x + g - 1) / g * g; }
@@ -226,9 +227,9 @@ struct ff_handle_s {
   size_t ev_used = 0;
   struct Pending { int kernel; size_t ev; double flop; };
   std::vector<Pending> pending;
-  int64_t t_launches[kTimedKernels] = {0, 0, 0, 0};
-  double t_ms[kTimedKernels] = {0, 0, 0, 0};
-  double t_flop[kTimedKernels] = {0, 0, 0, 0};
+  int64_t t_launches[kTimedKernels] = {};
+  double t_ms[kTimedKernels] = {};
+  double t_flop[kTimedKernels] = {};
 };
 
 namespace {
@@ -525,6 +526,75 @@ ff_status iterate_chunk(ff_handle_s* h, int iters, int* done, double* loglik) {
   }
   second.lw_valid = true;
   return FF_OK;
+}
+
+// ------------------------------------------------------------ quantiser
+struct QuantLayout {
+  int MT, NT;
+  int64_t mq, nq;
+  size_t off_La, off_Lb, off_al, off_be, off_dA, off_dB, off_racc, off_pre, off_x, off_e,
+      off_dpart, off_dist, total;
+};
+
+QuantLayout quant_layout(int64_t m, int64_t n) {
+  QuantLayout q{};
+  q.MT = (int)((m + kTileWK - 1) / kTileWK);
+  q.NT = (int)((n + kTileWK - 1) / kTileWK);
+  q.mq = (int64_t)q.MT * kTileWK;
+  q.nq = (int64_t)q.NT * kTileWK;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  const size_t tiles = (size_t)q.MT * q.NT * kTileWK * kTileWK * sizeof(float);
+  q.off_La = take((size_t)q.nq * q.nq * sizeof(float));
+  q.off_Lb = take((size_t)q.mq * q.mq * sizeof(float));
+  q.off_al = take((size_t)q.nq * sizeof(float));
+  q.off_be = take((size_t)q.mq * sizeof(float));
+  q.off_dA = take((size_t)q.nq * sizeof(float));
+  q.off_dB = take((size_t)q.mq * sizeof(float));
+  q.off_racc = take(tiles);
+  q.off_pre = take(tiles);
+  q.off_x = take(tiles);
+  q.off_e = take(tiles);
+  q.off_dpart = take((size_t)q.MT * q.NT * sizeof(double));
+  q.off_dist = take(sizeof(double));
+  q.total = off;
+  return q;
+}
+
+// Normalised inverse of RevCholesky(M) (padded), its diagonal and the padded
+// scales of one side: J M J is factorised in s.L / s.Li.
+ff_status quant_side(ff_handle_s* h, Side& s, const float* M, int64_t dq, float* Lt, float* diag,
+                     double gamma, int given, float* user, float* scale) {
+  FF_HIP(launch_wk_reverse(M, s.dim, s.L, h->st, h->stream));
+  {
+    Timed t(h, 3, (double)s.dim * s.dim * s.dim / 3.0);
+    ff_status rc = cholinv_rec(h, s, 0, s.dim, -1);
+    if (rc != FF_OK) return rc;
+  }
+  FF_HIP(launch_wk_normalise(s.Li, s.dim, dq, Lt, diag, h->st, h->stream));
+  FF_HIP(launch_wk_scales(diag, s.dim, dq, s.slots, s.nslots, gamma, given, user, scale, h->st,
+                          h->stream));
+  return FF_OK;
+}
+
+bool finite_positive(const float* dev, int64_t count, hipStream_t stream, std::string* why) {
+  std::vector<float> host((size_t)count);
+  if (hipMemcpyAsync(host.data(), dev, (size_t)count * sizeof(float), hipMemcpyDeviceToHost,
+                     stream) != hipSuccess ||
+      hipStreamSynchronize(stream) != hipSuccess) {
+    *why = "copying the given scales failed";
+    return false;
+  }
+  for (int64_t k = 0; k < count; ++k)
+    if (!(host[(size_t)k] > 0.0f) || !isfinite(host[(size_t)k])) {
+      *why = "given scales must be finite and > 0 (index " + std::to_string(k) + ")";
+      return false;
+    }
+  return true;
 }
 
 }  // namespace
@@ -828,6 +898,117 @@ ff_status ff_objective(ff_handle h, const float* A, const float* B, double* psi)
   return FF_OK;
 }
 
+ff_status ff_quantize_workspace_size(int64_t m, int64_t n, size_t* bytes) {
+  if (m < 1 || n < 1 || m > (1 << 20) || n > (1 << 20))
+    return fail(FF_ERR_INVALID_ARG, "m and n must be in [1, 1048576]");
+  if (bytes == nullptr) return fail(FF_ERR_INVALID_ARG, "bytes is NULL");
+  *bytes = quant_layout(m, n).total;
+  return FF_OK;
+}
+
+ff_status ff_quantize(ff_handle h, const float* W, const float* A, const float* B, double gamma,
+                      ff_scale_mode mode, float* alpha, float* beta, int32_t* Z, float* V,
+                      double* distortion, void* workspace, size_t workspace_bytes) {
+  if (h == nullptr) return fail(FF_ERR_INVALID_ARG, "handle is NULL");
+  if (mode != FF_SCALES_WATERFILL && mode != FF_SCALES_GIVEN)
+    return fail(FF_ERR_INVALID_ARG, "unknown scale mode");
+  const int given = mode == FF_SCALES_GIVEN ? 1 : 0;
+  if (!given && !(gamma > 0.0 && isfinite(gamma)))
+    return fail(FF_ERR_INVALID_ARG, "gamma must be finite and > 0");
+  if (W == nullptr || Z == nullptr || alpha == nullptr || beta == nullptr)
+    return fail(FF_ERR_INVALID_ARG, "W, Z, alpha and beta must be non-NULL device pointers");
+  auto misaligned = [](const void* p) { return ((uintptr_t)p % 4) != 0; };
+  if (misaligned(W) || misaligned(Z) || misaligned(alpha) || misaligned(beta) ||
+      misaligned(V) || misaligned(A) || misaligned(B))
+    return fail(FF_ERR_INVALID_ARG, "device arrays must be 4-byte aligned");
+  const int64_t m = h->m, n = h->n;
+  const QuantLayout q = quant_layout(m, n);
+  if (workspace == nullptr || ((uintptr_t)workspace % kAlign) != 0)
+    return fail(FF_ERR_WORKSPACE, "workspace must be a non-NULL 256-byte aligned device pointer");
+  if (workspace_bytes < q.total) {
+    char msg[128];
+    snprintf(msg, sizeof msg, "workspace too small: %zu < %zu bytes", workspace_bytes, q.total);
+    return fail(FF_ERR_WORKSPACE, msg);
+  }
+  if (given) {
+    std::string why;
+    if (!finite_positive(alpha, n, h->stream, &why) || !finite_positive(beta, m, h->stream, &why))
+      return fail(FF_ERR_INVALID_ARG, why);
+  }
+  char* ws = (char*)workspace;
+  float* La = (float*)(ws + q.off_La);
+  float* Lb = (float*)(ws + q.off_Lb);
+  float* al = (float*)(ws + q.off_al);
+  float* be = (float*)(ws + q.off_be);
+  float* dA = (float*)(ws + q.off_dA);
+  float* dB = (float*)(ws + q.off_dB);
+  double* dpart = (double*)(ws + q.off_dpart);
+  double* dist = (double*)(ws + q.off_dist);
+  // The factorisation buffers are reused: the whitening operands are stale.
+  h->A.lw_valid = h->B.lw_valid = false;
+  const int cur = h->cur;
+  ff_status rc;
+  if ((rc = quant_side(h, h->A, A != nullptr ? A : h->A.F[cur], q.nq, La, dA, gamma, given, alpha,
+                       al)) != FF_OK)
+    return rc;
+  if ((rc = quant_side(h, h->B, B != nullptr ? B : h->B.F[cur], q.mq, Lb, dB, gamma, given, beta,
+                       be)) != FF_OK)
+    return rc;
+  int st[4];
+  if ((rc = read_status(h, st)) != FF_OK) return rc;
+  if (st[0] != 0) {
+    if ((rc = clear_status(h)) != FF_OK) return rc;
+    FF_HIP(hipStreamSynchronize(h->stream));
+    if (h->timing) collect_timing(h);
+    return fail(FF_ERR_NOT_SPD, std::string("factor ") + (st[1] == 1 ? "A" : "B") +
+                                    " not positive definite in ff_quantize");
+  }
+  const int64_t tile_floats = (int64_t)q.MT * q.NT * kTileWK * kTileWK;
+  FF_HIP(launch_fill_f32((float*)(ws + q.off_racc), tile_floats, 0.0f, h->stream));
+  FF_HIP(launch_fill_f32((float*)(ws + q.off_pre), tile_floats, 0.0f, h->stream));
+  WkParams p{};
+  p.W = W;
+  p.m = m;
+  p.n = n;
+  p.La = La;
+  p.Lb = Lb;
+  p.alpha = al;
+  p.beta = be;
+  p.dA = dA;
+  p.dB = dB;
+  p.Racc = (float*)(ws + q.off_racc);
+  p.Pre = (float*)(ws + q.off_pre);
+  p.X = (float*)(ws + q.off_x);
+  p.E = (float*)(ws + q.off_e);
+  p.Z = Z;
+  p.dpart = dpart;
+  p.mq = q.mq;
+  p.nq = q.nq;
+  p.MT = q.MT;
+  p.NT = q.NT;
+  p.st = h->st;
+  const int ndiag = q.MT + q.NT - 1;
+  const double dflop = ((double)m * m * n + (double)m * n * n) / ndiag;
+  for (int d = 0; d < ndiag; ++d) {
+    Timed t(h, 4, dflop);
+    FF_HIP(launch_wk_diagonal(p, d, h->stream));
+  }
+  if (V != nullptr) FF_HIP(launch_wk_dequant(Z, m, n, al, be, V, h->st, h->stream));
+  FF_HIP(launch_wk_sum(dpart, (int64_t)q.MT * q.NT, 1.0 / ((double)m * (double)n), dist, h->st,
+                       h->stream));
+  double dh = 0.0;
+  FF_HIP(hipMemcpyAsync(&dh, dist, sizeof dh, hipMemcpyDeviceToHost, h->stream));
+  if ((rc = read_status(h, st)) != FF_OK) return rc;
+  if (h->timing) collect_timing(h);
+  if (st[0] != 0) {
+    if ((rc = clear_status(h)) != FF_OK) return rc;
+    FF_HIP(hipStreamSynchronize(h->stream));
+    return fail(FF_ERR_STATE, "device status set during the quantiser sweep");
+  }
+  if (distortion != nullptr) *distortion = dh;
+  return FF_OK;
+}
+
 ff_status ff_destroy(ff_handle h) {
   if (h == nullptr) return FF_OK;
   hipStreamSynchronize(h->stream);
@@ -839,7 +1020,7 @@ ff_status ff_destroy(ff_handle h) {
 ff_status ff_set_timing(ff_handle h, int enable) {
   if (h == nullptr) return fail(FF_ERR_INVALID_ARG, "handle is NULL");
   if (enable && h->events.empty()) {
-    h->events.resize(2 * 10 * 32 + 16);
+    h->events.resize(2 * 1024 + 16);  // enough for one quantiser sweep up to m + n = 65000
     for (auto& e : h->events) FF_HIP(hipEventCreate(&e));
   }
   h->timing = enable != 0;

@@ -135,4 +135,56 @@ hipError_t launch_fill_f32(float* dst, int64_t count, float v, hipStream_t s);
 hipError_t launch_identity_f32(float* dst, int64_t dim, hipStream_t s);
 hipError_t launch_set_int(int* dst, int64_t count, int v, hipStream_t s);
 
+// ------------------------------------------------------------ WaterKron
+// Tile edge of the quantiser sweep; padded dimensions are multiples of it.
+constexpr int kTileWK = 64;
+
+// Device operands of one quantiser sweep.  La (nq x nq) and Lb (mq x mq) are
+// the padded normalised inverse factors (identity in the padding); alpha
+// (nq) and beta (mq) the padded scales (1 in the padding); dA, dB the
+// RevCholesky diagonals.  Racc, Pre, X, E: MT * NT tiles of 64 x 64 floats
+// each (tile (I, J) at offset (I * NT + J) * 4096; Racc and Pre zeroed
+// before the first diagonal).  Z: m x n codes; dpart: MT * NT doubles.
+struct WkParams {
+  const float* W;
+  int64_t m, n;
+  const float* La;
+  const float* Lb;
+  const float* alpha;
+  const float* beta;
+  const float* dA;
+  const float* dB;
+  float* Racc;
+  float* Pre;
+  float* X;
+  float* E;
+  int32_t* Z;
+  double* dpart;
+  int64_t mq, nq;
+  int MT, NT;
+  const int* st;
+};
+
+// J M J for M d x d.
+hipError_t launch_wk_reverse(const float* M, int64_t d, float* out, const int* st, hipStream_t s);
+// Normalised inverse of RevCholesky(M) (padded dq x dq) and its diagonal,
+// from Ci = Cholesky(J M J)^-1.
+hipError_t launch_wk_normalise(const float* Ci, int64_t d, int64_t dq, float* Lt, float* diag,
+                               const int* st, hipStream_t s);
+// Padded scales; given = 0: waterfilling from diag and the log-pivot slots
+// (also written to user), given = 1: copied from user.
+hipError_t launch_wk_scales(const float* diag, int64_t d, int64_t dq, const double* slots,
+                            int nslots, double gamma, int given, float* user, float* scale,
+                            const int* st, hipStream_t s);
+// Workgroups pushing the tiles of diagonal d - 1 forward.
+int64_t wk_push_units(int d, int MT, int NT);
+// Anti-diagonal d (0 <= d <= MT + NT - 2) of the sweep.
+hipError_t launch_wk_diagonal(const WkParams& p, int d, hipStream_t s);
+// V = beta alpha^T (.) Z (m x n).
+hipError_t launch_wk_dequant(const int32_t* Z, int64_t m, int64_t n, const float* alpha,
+                             const float* beta, float* V, const int* st, hipStream_t s);
+// *out = scale * sum part[0..count), fixed order.
+hipError_t launch_wk_sum(const double* part, int64_t count, double scale, double* out,
+                         const int* st, hipStream_t s);
+
 }  // namespace ff

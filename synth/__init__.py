@@ -12,15 +12,18 @@ The paper calibrates on LLM layers (256 x 2048 tokens of a public text
 corpus, gradients of real models; Appendix B).  Neither the weights nor the
 data are available here, so these draws stand in for them at the layer
 shapes of the workloads below.  ``tokens`` draws the per-token form instead
-(inputs x_t and output gradients g_t, samples G_t = g_t x_t^T).
+(inputs x_t and output gradients g_t, samples G_t = g_t x_t^T); ``quant``
+draws the weights and factors the WaterKron quantiser consumes.
 """
 from .generator import (WORKLOADS, Workload, workload, generate, generate_device,
                         power_law_spectrum, haar_orthogonal, f32_to_bf16_bits,
                         bf16_bits_to_f32)
 from .tokens import (TOKEN_WORKLOADS, TokenWorkload, token_workload, generate_tokens,
                      generate_tokens_device)
+from .quant import QUANT_WORKLOADS, QuantWorkload, quant_workload, generate_quant
 
 __all__ = ["WORKLOADS", "Workload", "workload", "generate", "generate_device",
            "power_law_spectrum", "haar_orthogonal", "f32_to_bf16_bits",
            "bf16_bits_to_f32", "TOKEN_WORKLOADS", "TokenWorkload", "token_workload",
-           "generate_tokens", "generate_tokens_device"]
+           "generate_tokens", "generate_tokens_device", "QUANT_WORKLOADS", "QuantWorkload",
+           "quant_workload", "generate_quant"]

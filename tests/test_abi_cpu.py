@@ -115,3 +115,24 @@ def test_null_handle_calls(lib):
     assert lib.ff_factors(None, None, None, 1) == ff.FF_ERR_INVALID_ARG
     assert lib.ff_kron_apply(None, None, None, 1, 0) == ff.FF_ERR_INVALID_ARG
     assert lib.ff_destroy(None) == ff.FF_OK
+
+
+def test_quantize_workspace_sizes(lib):
+    b = ff.ff_quantize_workspace_size(4096, 4096)
+    # two padded normalised inverse factors and four tile-blocked accumulators
+    assert 6 * 4096 * 4096 * 4 <= b < 6 * 4096 * 4096 * 4 + (1 << 20)
+    r = ff.ff_quantize_workspace_size(100, 70)           # padded to 128 x 128 tiles
+    assert 6 * 128 * 128 * 4 <= r < 6 * 128 * 128 * 4 + 8192
+    assert ff.ff_quantize_workspace_size(1, 1) >= 6 * 64 * 64 * 4
+    for m, n in [(0, 5), (5, 0), (-3, 4), ((1 << 20) + 1, 4)]:
+        with pytest.raises(ff.FlipFlopError) as ei:
+            ff.ff_quantize_workspace_size(m, n)
+        assert ei.value.code == ff.FF_ERR_INVALID_ARG
+
+
+def test_quantize_rejects_null_handle(lib):
+    d = ctypes.c_double(0.0)
+    assert lib.ff_quantize(None, None, None, None, 1.0, 0, None, None, None, None,
+                           ctypes.byref(d), None, 0) == ff.FF_ERR_INVALID_ARG
+    assert "handle" in ff.ff_last_error()
+    assert lib.ff_objective(None, None, None, ctypes.byref(d)) == ff.FF_ERR_INVALID_ARG
