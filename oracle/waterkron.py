@@ -24,11 +24,11 @@ import numpy as np
 
 def rev_cholesky(M):
     """L lower triangular, positive diagonal, L^T L = M (via the reversal
-    J: L = J chol(J M J)^T J)."""
+    J: L = J chol(J M J)^T J; the products with the exchange matrix J are
+    taken as the row and column reversals they are)."""
     M = np.asarray(M, np.float64)
-    J = np.eye(M.shape[0])[::-1]
-    C = np.linalg.cholesky(J @ M @ J)
-    return J @ C.T @ J
+    C = np.linalg.cholesky(np.ascontiguousarray(M[::-1, ::-1]))      # chol(J M J)
+    return np.ascontiguousarray(C.T[::-1, ::-1])                     # J C^T J
 
 
 def normalised_inverse(M):
