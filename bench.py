@@ -120,13 +120,121 @@ def cpu_baseline_tokens(x, g, w, budget_s: float):
                       f"{t_total:.1f} s, scaled to a full iteration ({per_iter:.1f} s)"}
 
 
+def cpu_baseline_quant(w, budget_s: float):
+    """Oracle time of Algorithm 2 on the layer, from bounded sub-problems.
+
+    The oracle updates the whole m x n matrix after every entry, so its time
+    grows as (m n)^2; it is timed on the leading k x k blocks of a 256 x 256
+    instance of the workload's recipe (k doubling until the budget is used)
+    and scaled to m x n by that law.  Its updates are numpy elementwise
+    operations, which run on one thread.
+    """
+    import numpy as np
+    import oracle
+    import synth
+    d = synth.generate_quant(w.scaled(m=min(w.m, 256), n=min(w.n, 256)))
+    k, used, last = 16, 0.0, None
+    while k <= min(w.m, w.n, 256) and used < budget_s:
+        W = d.W[:k, :k].astype(np.float64)
+        A = d.A[:k, :k].astype(np.float64)
+        B = d.B[:k, :k].astype(np.float64)
+        al, be = oracle.waterfilling_scales(A, B, w.gamma)
+        t0 = time.perf_counter()
+        oracle.two_sided_gptq(W, A, B, al, be)
+        dt = time.perf_counter() - t0
+        used += dt
+        last = (k, dt)
+        k *= 2
+    k, dt = last
+    per_layer = dt * (w.m * w.n / float(k * k)) ** 2
+    return {"value": 1.0 / per_layer, "unit": "quantisations/s", "cores": 1, "kind": "oracle",
+            "sample": f"fp64 Algorithm 2 on the leading {k}x{k} block of a 256x256 instance "
+                      f"({dt:.2f} s), scaled to {w.m}x{w.n} by the oracle's (m n)^2 cost law"}
+
+
+def main_quant(args):
+    """A step is one whole WaterKron quantisation of the layer (ff_quantize):
+    both reverse Cholesky factorisations, the waterfilling scales, the
+    anti-diagonal sweep of Algorithm 2, the grid values and the distortion."""
+    import torch
+    import synth
+    import paper_2609_14706_amd as ffe
+
+    dev = torch.device("cuda:0")
+    w = synth.quant_workload(args.workload)
+    d = synth.generate_quant(w, seed=args.seed)
+    W = torch.from_numpy(d.W).to(dev)
+    A = torch.from_numpy(d.A).to(dev)
+    B = torch.from_numpy(d.B).to(dev)
+    G = torch.zeros((1, w.m, w.n), dtype=torch.float32, device=dev)
+    G[0, 0, 0] = 1.0
+    stream = torch.cuda.current_stream(dev)
+    h = ffe.FlipFlop(G, stream=stream)
+    ws = torch.empty(h.quantize_workspace_bytes(w.m, w.n), dtype=torch.uint8, device=dev)
+    for _ in range(args.warmup):
+        h.quantize(W, A, B, gamma=w.gamma, workspace=ws)
+    torch.cuda.synchronize()
+    print(f"[bench] warmup done ({args.warmup} quantisations of {w.name})", file=sys.stderr,
+          flush=True)
+    h.set_timing(True)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        Z, V, al, be, D = h.quantize(W, A, B, gamma=w.gamma, workspace=ws)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms_total = ev0.elapsed_time(ev1)
+    n_d, ms_d, fl_d = h.kernel_timing("quant_diag")
+    n_c, ms_c, _ = h.kernel_timing("cholinv")
+    h.close()
+    ms_per_step = ms_total / args.steps
+    achieved = fl_d / (ms_d * 1e-3) / 1e12 if ms_d > 0 else 0.0
+    print(f"[bench] {args.steps} quantisations in {ms_total:.2f} ms; sweep {n_d} launches "
+          f"{ms_d:.2f} ms, factorisations {n_c} x {ms_c / max(n_c, 1):.3f} ms, D = {D:.6e}",
+          file=sys.stderr, flush=True)
+    peak = PEAK_TFLOPS["f32"]
+    out = {
+        "metric": f"WaterKron quantisations/s (two-sided GPTQ, waterfilling scales), "
+                  f"m={w.m} n={w.n}",
+        "value": round(1000.0 / ms_per_step, 4),
+        "unit": "quantisations/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "m": w.m, "n": w.n, "gamma": w.gamma,
+                   "timed_job": f"{args.steps} x ff_quantize"},
+        "weights_per_s": round(w.m * w.n * 1000.0 / ms_per_step, 1),
+        "distortion": D,
+        "kernels_ms": {"quant_diag": round(ms_d, 3), "cholinv": round(ms_c, 3)},
+        "roofline": {"bound": "mfma", "kernel": "k_wk_diagonal",
+                     "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 5), "traffic": None,
+                     "launches": n_d, "avg_launch_ms": round(ms_d / max(n_d, 1), 4),
+                     "alg_flop_per_launch": fl_d / max(n_d, 1)},
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the fp64 oracle on host cores", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline_quant(w, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10, help="timed flip-flop iterations")
     ap.add_argument("--warmup", type=int, default=2, help="untimed iterations on a separate handle")
     ap.add_argument("--workload", default="attn",
-                    help="tiny | attn | mlp_up | mlp_down | mlp_large | tokens_tiny | tokens_attn")
+                    help="tiny | attn | mlp_up | mlp_down | mlp_large | tokens_tiny | tokens_attn"
+                         " | quant_small | quant_multi | quant_attn")
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--whiten-split", type=int, default=1)
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time")
@@ -138,6 +246,9 @@ def main():
               "(sharding over samples is described in the design notes, not built).",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.workload.startswith("quant"):
+        return main_quant(args)
 
     import torch
 

@@ -532,7 +532,7 @@ ff_status iterate_chunk(ff_handle_s* h, int iters, int* done, double* loglik) {
 struct QuantLayout {
   int MT, NT;
   int64_t mq, nq;
-  size_t off_La, off_Lb, off_al, off_be, off_dA, off_dB, off_racc, off_pre, off_x, off_e,
+  size_t off_La, off_Lb, off_al, off_be, off_dA, off_dB, off_racc, off_pre, off_x, off_e, off_z,
       off_dpart, off_dist, total;
 };
 
@@ -559,6 +559,7 @@ QuantLayout quant_layout(int64_t m, int64_t n) {
   q.off_pre = take(tiles);
   q.off_x = take(tiles);
   q.off_e = take(tiles);
+  q.off_z = take((size_t)q.mq * q.nq * sizeof(int32_t));
   q.off_dpart = take((size_t)q.MT * q.NT * sizeof(double));
   q.off_dist = take(sizeof(double));
   q.total = off;
@@ -980,7 +981,7 @@ ff_status ff_quantize(ff_handle h, const float* W, const float* A, const float* 
   p.Pre = (float*)(ws + q.off_pre);
   p.X = (float*)(ws + q.off_x);
   p.E = (float*)(ws + q.off_e);
-  p.Z = Z;
+  p.Z = (int32_t*)(ws + q.off_z);
   p.dpart = dpart;
   p.mq = q.mq;
   p.nq = q.nq;
@@ -993,7 +994,7 @@ ff_status ff_quantize(ff_handle h, const float* W, const float* A, const float* 
     Timed t(h, 4, dflop);
     FF_HIP(launch_wk_diagonal(p, d, h->stream));
   }
-  if (V != nullptr) FF_HIP(launch_wk_dequant(Z, m, n, al, be, V, h->st, h->stream));
+  FF_HIP(launch_wk_finish(p.Z, q.nq, m, n, al, be, Z, V, h->st, h->stream));
   FF_HIP(launch_wk_sum(dpart, (int64_t)q.MT * q.NT, 1.0 / ((double)m * (double)n), dist, h->st,
                        h->stream));
   double dh = 0.0;

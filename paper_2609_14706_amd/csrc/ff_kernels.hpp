@@ -144,7 +144,8 @@ constexpr int kTileWK = 64;
 // (nq) and beta (mq) the padded scales (1 in the padding); dA, dB the
 // RevCholesky diagonals.  Racc, Pre, X, E: MT * NT tiles of 64 x 64 floats
 // each (tile (I, J) at offset (I * NT + J) * 4096; Racc and Pre zeroed
-// before the first diagonal).  Z: m x n codes; dpart: MT * NT doubles.
+// before the first diagonal).  Z: mq x nq codes (padded, leading dimension
+// nq); dpart: MT * NT doubles.
 struct WkParams {
   const float* W;
   int64_t m, n;
@@ -180,9 +181,11 @@ hipError_t launch_wk_scales(const float* diag, int64_t d, int64_t dq, const doub
 int64_t wk_push_units(int d, int MT, int NT);
 // Anti-diagonal d (0 <= d <= MT + NT - 2) of the sweep.
 hipError_t launch_wk_diagonal(const WkParams& p, int d, hipStream_t s);
-// V = beta alpha^T (.) Z (m x n).
-hipError_t launch_wk_dequant(const int32_t* Z, int64_t m, int64_t n, const float* alpha,
-                             const float* beta, float* V, const int* st, hipStream_t s);
+// Z (m x n) from the padded codes Zp (leading dimension nq) and, when V is
+// non-null, V = beta alpha^T (.) Z.
+hipError_t launch_wk_finish(const int32_t* Zp, int64_t nq, int64_t m, int64_t n,
+                           const float* alpha, const float* beta, int32_t* Z, float* V,
+                           const int* st, hipStream_t s);
 // *out = scale * sum part[0..count), fixed order.
 hipError_t launch_wk_sum(const double* part, int64_t count, double scale, double* out,
                          const int* st, hipStream_t s);

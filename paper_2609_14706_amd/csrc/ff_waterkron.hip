@@ -46,10 +46,6 @@ constexpr int WT = 64;   // tile edge
 constexpr int WTT = WT * WT;
 constexpr int OP = 96;   // operand pitch: rows k and k + 1 fall in opposite bank halves
 
-__device__ __forceinline__ float bcastf(float v, int lane) {
-  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
-}
-
 // ------------------------------------------------------------ preparation
 // out[i][j] = M[d-1-i][d-1-j]  (J M J)
 __global__ __launch_bounds__(256) void k_wk_reverse(const float* __restrict__ M, int64_t d,
@@ -117,12 +113,27 @@ __global__ __launch_bounds__(256) void k_wk_scales(const float* __restrict__ dia
 }
 
 // ------------------------------------------------------------- the sweep
-struct WkLDS {
-  float sa[WT][OP];  // left operand, [k][row]; the tile's residuals e[i][j] at [j][i]
-  float sb[WT][OP];  // right operand, [k][col]; the tile's input R[i][j] at [j][i]
-  float sl[WT][WT];  // scaled in-tile La: La[j][j'] alpha_j' / alpha_j
-  float su[WT][WT];  // scaled column updates u'[j][i]
-};
+constexpr int ST = 16;   // sub-tile edge
+constexpr int CP = 68;   // pitch of the in-tile contributions and residuals
+constexpr int PP = 17;   // pitch of a sub-tile product scratch
+constexpr int DP = 272;  // stride of the diagonal La blocks (16 x 16 + a bank offset)
+
+// LDS of a workgroup, in floats.  Tile workgroups: phase 1 (products from
+// outside the tile) stages operands in SA / SB; phase 2 (the in-tile sweep)
+// keeps Lb[I][I] and La[J][J] (row r rotated by 4 (r mod 16) to spread the
+// banks), the contributions C^T of the tile (a 16 x 16 block is replaced by
+// the row-block prefix Xs^T of its sub-tile once that sub-tile is done), the
+// residuals E^T, per-wave product scratch, the diagonal 16 x 16 blocks of
+// La[J][J] transposed, and the tile's scales.  Push workgroups use SA / SB.
+constexpr int L_LB = 0, L_LA = WTT, L_SA = 2 * WTT, L_SB = L_SA + WT * OP, L_TOTAL = L_SB + WT * OP;
+constexpr int L_CT = 2 * WTT, L_ET = L_CT + WT * CP, L_PS = L_ET + WT * CP;
+constexpr int L_LAD = L_PS + 4 * ST * PP, L_AL = L_LAD + 4 * DP;
+constexpr int L_BE = L_AL + WT, L_DA = L_BE + WT, L_DB = L_DA + WT;
+static_assert(L_DB + WT <= L_TOTAL, "tile LDS map");
+
+__device__ __forceinline__ int rot(int r, int c) { return r * WT + ((c + 4 * (r & 15)) & 63); }
+
+typedef __attribute__((ext_vector_type(4))) float f32x4v;
 
 // s[k][o] = P[o * ld + k]: operand contiguous along k
 __device__ __forceinline__ void stage_kmaj(float (*s)[OP], const float* __restrict__ P, int64_t ld,
@@ -150,16 +161,32 @@ __device__ __forceinline__ void stage_omaj(float (*s)[OP], const float* __restri
   }
 }
 
-// acc += sa^T sb over k < 64 for this wave's 32 x 32 quadrant (wm, wn).
-__device__ __forceinline__ void mac64(const float (*sa)[OP], const float (*sb)[OP], f32x16& acc,
-                                      int wm, int wn, int lane) {
+// acc += A B over k < 64 for this wave's 32 x 32 quadrant (wm, wn) of a
+// 64 x 64 product; fa(i, k) and fb(k, j) read the operands.
+template <class FA, class FB>
+__device__ __forceinline__ void mac64f(FA fa, FB fb, f32x16& acc, int wm, int wn, int lane) {
 #pragma unroll
   for (int s = 0; s < WT / 2; ++s) {
     const int kr = 2 * s + (lane >> 5);
-    const float a = sa[kr][wm * 32 + (lane & 31)];
-    const float b = sb[kr][wn * 32 + (lane & 31)];
-    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(fa(wm * 32 + (lane & 31), kr),
+                                               fb(kr, wn * 32 + (lane & 31)), acc, 0, 0, 0);
   }
+}
+
+__device__ __forceinline__ void mac64(const float (*sa)[OP], const float (*sb)[OP], f32x16& acc,
+                                      int wm, int wn, int lane) {
+  mac64f([&](int i, int k) { return sa[k][i]; }, [&](int k, int j) { return sb[k][j]; }, acc, wm,
+         wn, lane);
+}
+
+// acc += A B over k < 16 for one 16 x 16 block on the 16 x 16 x 4 fp32
+// matrix cores: fa(m, k), fb(k, n); this lane holds D[4 (lane / 16) + r][lane % 16].
+template <class FA, class FB>
+__device__ __forceinline__ void mac16(FA fa, FB fb, f32x4v& acc, int lane) {
+  const int n = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa(n, 4 * q + g), fb(4 * q + g, n), acc, 0, 0, 0);
 }
 
 // Row and column of accumulator element r of this lane in the 64 x 64 tile.
@@ -180,69 +207,166 @@ __device__ __forceinline__ void store_tile(const f32x16& acc, float* __restrict_
   for (int r = 0; r < 16; ++r) P[acc_row(wm, lane, r) * WT + acc_col(wn, lane)] = acc[r];
 }
 
-// The wave-0 recurrence of one tile.  R (at sb[j][i]) holds every
-// contribution from outside the tile; writes codes, residuals (sa[j][i] and
-// the transposed residual tile Et[j * 64 + i]) and returns this lane's share
-// of sum (L^B_ii e_ij L^A_jj)^2.
-__device__ __forceinline__ double tile_recurrence(const WkParams& p, WkLDS& sm, int I, int J,
-                                                  float* __restrict__ Et, int lane) {
-  const int i = lane;
-  const int64_t r0 = (int64_t)I * WT, c0 = (int64_t)J * WT;
-  const int64_t gi = r0 + i;
-  const float bi = p.beta[gi];
-  // row i of the in-tile Lb, scaled by beta_k / beta_i, strictly below the diagonal
-  float lbs[WT];
-  const float* lrow = p.Lb + gi * p.mq + r0;
-#pragma unroll
-  for (int k4 = 0; k4 < WT; k4 += 4) {
-    const f32x4 v = *reinterpret_cast<const f32x4*>(lrow + k4);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int k = k4 + e;
-      lbs[k] = k < i ? v[e] * (p.beta[r0 + k] / bi) : 0.0f;
+// State of wave 0's lanes over the 16 columns of a sub-diagonal (lane row
+// = one sub-tile, lane = one of its rows i).
+struct ChainCtx {
+  float lbs[ST];    // row i of the diagonal Lb block scaled by beta_k / beta_i, below the diagonal
+  float step[ST];   // alpha_j beta_i of the 16 columns
+  float rstep[ST];  // 1 / step
+  float bq[ST];     // column coupling inside the sub-tile (unscaled)
+  float cv[ST];     // contributions C^T[j][i] from outside the sub-tile
+  float da[ST];     // RevCholesky diagonal of A at the 16 columns
+  f32x4 cn[4];      // this column's coupling coefficients La[j'][j], j' = 16 b + 0..15
+  f32x4 cp[4];      // the previous column's
+  float u, e, z;    // the previous column's update, residual and code
+  float dist;
+  const float* ladT;  // La[J][J] block (b, b) transposed: ladT[c * 16 + c2] = La[16 b + c2][16 b + c]
+  float* et;          // E^T in LDS at (16 b, i)
+  float* erow;        // the transposed residual tile in memory at (16 b, i)
+  int32_t* zrow;      // padded codes at (i, 16 b)
+};
+
+__device__ __forceinline__ float cf(const f32x4 (&v)[4], int k) { return v[k >> 2][k & 3]; }
+
+// Work of the previous column C - 1 spread over the row steps K of column C:
+// loads of column C's coefficients (K < 4), the coupling updates of the
+// columns after C (one per step), and the previous column's stores.
+template <int C, int K>
+__device__ __forceinline__ void side(ChainCtx& x) {
+  if constexpr (K < 4)
+    x.cn[K] = *reinterpret_cast<const f32x4*>(x.ladT + C * ST + 4 * K);
+  if constexpr (C > 0) {
+    constexpr int c2 = C + 1 + K;  // updates of bq[c2] with the previous column's u
+    if constexpr (c2 < ST) x.bq[c2] = fmaf(cf(x.cp, c2), x.u, x.bq[c2]);
+    if constexpr (K == 12) x.et[(C - 1) * CP] = x.e;
+    if constexpr (K == 13) x.erow[(C - 1) * WT] = x.e;
+    if constexpr (K == 14) x.zrow[C - 1] = (int32_t)x.z;
+    if constexpr (K == 15) {
+      const float t = x.e * x.da[C - 1];
+      x.dist = fmaf(t, t, x.dist);
     }
   }
-  const bool row_live = gi < p.m;
-  const double dbi = (double)p.dB[gi];
-  double dist = 0.0;
-  for (int j = 0; j < WT; ++j) {
-    const int64_t gj = c0 + j;
-    const float step = p.alpha[gj] * bi;
-    // column coupling: sum_{j' < j} La~[j][j'] u'[j'][i], four partial sums
-    float b0 = 0.0f, b1 = 0.0f, b2 = 0.0f, b3 = 0.0f;
-    int jp = 0;
-    for (; jp + 4 <= j; jp += 4) {
-      b0 = fmaf(sm.sl[j][jp], sm.su[jp][i], b0);
-      b1 = fmaf(sm.sl[j][jp + 1], sm.su[jp + 1][i], b1);
-      b2 = fmaf(sm.sl[j][jp + 2], sm.su[jp + 2][i], b2);
-      b3 = fmaf(sm.sl[j][jp + 3], sm.su[jp + 3][i], b3);
-    }
-    for (; jp < j; ++jp) b0 = fmaf(sm.sl[j][jp], sm.su[jp][i], b0);
-    float q = sm.sb[j][i] / step + ((b0 + b1) + (b2 + b3));
-    const float qs = q;
-    // row chain: at step k row k is final; its scaled residual updates the rows below
-#pragma unroll
-    for (int k = 0; k < WT; ++k) {
-      const float dd = __builtin_rintf(q) - q;
-      q = fmaf(lbs[k], bcastf(dd, k), q);
-    }
-    const float z = __builtin_rintf(q);
-    const float e = (z - q) * step;
-    sm.su[j][i] = z - qs;
-    sm.sa[j][i] = e;
-    Et[j * WT + i] = e;
-    if (row_live && gj < p.n) {
-      p.Z[gi * p.n + gj] = (int32_t)z;
-      const double t = dbi * (double)e * (double)p.dA[gj];
-      dist += t * t;
-    }
-  }
-  return dist;
 }
 
-__global__ __launch_bounds__(256) void k_wk_diagonal(WkParams p, int d, int nrec, int ilo) {
+// Row step K of column C: row K is final; its scaled residual is broadcast
+// within the lane row (DPP row_newbcast) and updates the rows below it.
+template <int C, int K>
+__device__ __forceinline__ void rowstep(ChainCtx& x, float& q) {
+  const float dd = __builtin_rintf(q) - q;
+  __builtin_amdgcn_sched_barrier(0);
+  side<C, K>(x);
+  __builtin_amdgcn_sched_barrier(0);
+  const float D =
+      __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(dd), 0x150 + K, 0xF, 0xF, true));
+  q = fmaf(x.lbs[K], D, q);
+  if constexpr (K + 1 < ST) rowstep<C, K + 1>(x, q);
+}
+
+template <int C>
+__device__ __forceinline__ void column(ChainCtx& x) {
+  float q = (x.cv[C] + x.bq[C]) * x.rstep[C];
+  const float qs = q;
+  rowstep<C, 0>(x, q);
+  const float z = __builtin_rintf(q);
+  x.e = (z - q) * x.step[C];
+  x.u = (z - qs) * x.step[C];
+  x.z = z;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) x.cp[k] = x.cn[k];
+  if constexpr (C + 1 < ST) {
+    x.bq[C + 1] = fmaf(cf(x.cp, C + 1), x.u, x.bq[C + 1]);  // the next column needs it now
+    column<C + 1>(x);
+  }
+}
+
+// Wave 0: the sub-tiles (a, s - a) of in-tile sub-diagonal s, one per row of
+// 16 lanes (slot = lane / 16, a = alo + slot; rows of lanes beyond the nv
+// sub-tiles repeat slot 0 and store the same values).  Reads the
+// contributions C^T, writes residuals (LDS and the transposed residual tile
+// Et) and the padded codes; returns this lane's share of
+// sum (L^B_ii e_ij L^A_jj)^2 (the diagonals are 0 in the padding).
+__device__ __forceinline__ double subdiag_chain(const WkParams& p, float* lds, int s, int alo,
+                                                int nv, int64_t r0, int64_t c0,
+                                                float* __restrict__ Et, int lane) {
+  const int slot = lane >> 4, rr = lane & 15;
+  const bool live = slot < nv;
+  const int a = alo + (live ? slot : 0), b = s - a;
+  const int i = ST * a + rr;
+  const float bi = lds[L_BE + i];
+  ChainCtx x;
+#pragma unroll
+  for (int k = 0; k < ST; ++k)
+    x.lbs[k] = k < rr ? lds[L_LB + rot(i, ST * a + k)] * (lds[L_BE + ST * a + k] / bi) : 0.0f;
+  const float* ct = lds + L_CT + (ST * b) * CP + i;
+#pragma unroll
+  for (int c = 0; c < ST; ++c) {
+    x.step[c] = lds[L_AL + ST * b + c] * bi;
+    x.rstep[c] = 1.0f / x.step[c];
+    x.bq[c] = 0.0f;
+    x.cv[c] = ct[c * CP];
+    x.da[c] = lds[L_DA + ST * b + c];
+  }
+  x.ladT = lds + L_LAD + b * DP;
+  x.et = lds + L_ET + (ST * b) * CP + i;
+  x.erow = Et + (ST * b) * WT + i;
+  x.zrow = p.Z + (r0 + i) * p.nq + c0 + ST * b;
+  x.dist = 0.0f;
+  column<0>(x);
+  // the last column's stores
+  x.et[(ST - 1) * CP] = x.e;
+  x.erow[(ST - 1) * WT] = x.e;
+  x.zrow[ST - 1] = (int32_t)x.z;
+  const float t = x.e * x.da[ST - 1];
+  x.dist = fmaf(t, t, x.dist);
+  const double db = live ? (double)lds[L_DB + i] : 0.0;
+  return db * db * (double)x.dist;
+}
+
+// Wave w = slot: the contributions a sub-tile (a, b) of sub-diagonal s still
+// lacks, from the sub-tiles above it and to its left inside the tile:
+//   P^T[j][i]  = sum_{b' < b} sum_{j' in b'} La[j][j'] e[i][j']
+//   C^T[j][i] += sum_{a' < a} sum_{i' in a'} Xs^T[j][i'] Lb[i][i'] + sum_{i' in a} P^T[j][i'] Lb[i][i']
+// (transposed 16 x 16 blocks; Xs^T of the finished sub-tiles sits in their
+// blocks of C^T).  P is returned for the row-block prefix of (a, b).
+__device__ __forceinline__ void subtile_pull(float* lds, int a, int b, int wave, int lane,
+                                             f32x4v& P) {
+  const int n = lane & 15, g = lane >> 4;
+  P = f32x4v{0.0f, 0.0f, 0.0f, 0.0f};
+  for (int bp = 0; bp < b; ++bp)
+    mac16([&](int m, int k) { return lds[L_LA + rot(ST * b + m, ST * bp + k)]; },
+          [&](int k, int nn) { return lds[L_ET + (ST * bp + k) * CP + ST * a + nn]; }, P, lane);
+  float* ps = lds + L_PS + wave * ST * PP;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) ps[(4 * g + r) * PP + n] = P[r];
+  float* cblk = lds + L_CT + (ST * b) * CP + ST * a;
+  f32x4v acc;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) acc[r] = cblk[(4 * g + r) * CP + n];
+  for (int ap = 0; ap < a; ++ap)
+    mac16([&](int m, int k) { return lds[L_CT + (ST * b + m) * CP + ST * ap + k]; },
+          [&](int k, int nn) { return lds[L_LB + rot(ST * a + nn, ST * ap + k)]; }, acc, lane);
+  mac16([&](int m, int k) { return ps[m * PP + k]; },
+        [&](int k, int nn) { return lds[L_LB + rot(ST * a + nn, ST * a + k)]; }, acc, lane);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) cblk[(4 * g + r) * CP + n] = acc[r];
+}
+
+// After its chain: Xs^T = P^T + (La[b][b] e_ab^T), stored over the consumed
+// contribution block (a, b).
+__device__ __forceinline__ void subtile_prefix(float* lds, int a, int b, int lane, f32x4v P) {
+  const int n = lane & 15, g = lane >> 4;
+  mac16([&](int m, int k) { return lds[L_LA + rot(ST * b + m, ST * b + k)]; },
+        [&](int k, int nn) { return lds[L_ET + (ST * b + k) * CP + ST * a + nn]; }, P, lane);
+  float* cblk = lds + L_CT + (ST * b) * CP + ST * a;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) cblk[(4 * g + r) * CP + n] = P[r];
+}
+
+__global__ __launch_bounds__(256, 2) void k_wk_diagonal(WkParams p, int d, int nrec, int ilo) {
   if (ff_halted(p.st)) return;
-  __shared__ __align__(16) WkLDS sm;
+  __shared__ __align__(16) float lds[L_TOTAL];
+  float(*SA)[OP] = reinterpret_cast<float(*)[OP]>(lds + L_SA);
+  float(*SB)[OP] = reinterpret_cast<float(*)[OP]>(lds + L_SB);
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
   const int bid = blockIdx.x;
@@ -253,57 +377,83 @@ __global__ __launch_bounds__(256) void k_wk_diagonal(WkParams p, int d, int nrec
     // ------------------------------------------------ tile (I, J) of diagonal d
     const int I = ilo + bid, J = d - I;
     const int64_t r0 = (int64_t)I * WT, c0 = (int64_t)J * WT;
+    // the tile's diagonal factor blocks, rows rotated
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int idx = tid + 256 * q;
+      const int r = idx >> 4, c = (idx & 15) * 4;
+      *reinterpret_cast<f32x4*>(&lds[L_LB + rot(r, c)]) =
+          *reinterpret_cast<const f32x4*>(p.Lb + (r0 + r) * p.mq + r0 + c);
+      *reinterpret_cast<f32x4*>(&lds[L_LA + rot(r, c)]) =
+          *reinterpret_cast<const f32x4*>(p.La + (c0 + r) * p.nq + c0 + c);
+    }
     f32x16 pre;
     load_tile(pre, blk(p.Pre, I, J), wm, wn, lane);
     if (J > 0) {  // + E[I][J-1] La[J][J-1]^T
-      stage_omaj(sm.sa, blk(p.E, I, J - 1), WT, tid);
-      stage_kmaj(sm.sb, p.La + c0 * p.nq + (c0 - WT), p.nq, tid);
+      stage_omaj(SA, blk(p.E, I, J - 1), WT, tid);
+      stage_kmaj(SB, p.La + c0 * p.nq + (c0 - WT), p.nq, tid);
       __syncthreads();
-      mac64(sm.sa, sm.sb, pre, wm, wn, lane);
+      mac64(SA, SB, pre, wm, wn, lane);
       __syncthreads();
     }
     f32x16 racc;
     load_tile(racc, blk(p.Racc, I, J), wm, wn, lane);
     if (I > 0) {  // + Lb[I][I-1] X[I-1][J]
-      stage_kmaj(sm.sa, p.Lb + r0 * p.mq + (r0 - WT), p.mq, tid);
-      stage_omaj(sm.sb, blk(p.X, I - 1, J), WT, tid);
+      stage_kmaj(SA, p.Lb + r0 * p.mq + (r0 - WT), p.mq, tid);
+      stage_omaj(SB, blk(p.X, I - 1, J), WT, tid);
       __syncthreads();
-      mac64(sm.sa, sm.sb, racc, wm, wn, lane);
+      mac64(SA, SB, racc, wm, wn, lane);
       __syncthreads();
     }
     // + Lb[I][I] Pre
-    stage_kmaj(sm.sa, p.Lb + r0 * p.mq + r0, p.mq, tid);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) sm.sb[acc_row(wm, lane, r)][acc_col(wn, lane)] = pre[r];
+    for (int r = 0; r < 16; ++r) SB[acc_row(wm, lane, r)][acc_col(wn, lane)] = pre[r];
     __syncthreads();
-    mac64(sm.sa, sm.sb, racc, wm, wn, lane);
+    mac64f([&](int i, int k) { return lds[L_LB + rot(i, k)]; },
+           [&](int k, int j) { return SB[k][j]; }, racc, wm, wn, lane);
     __syncthreads();
-    // R = W + racc, transposed into sb; scaled in-tile La into sl
+    // C^T = (W + racc)^T; the tile's scales and RevCholesky diagonals
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int i = acc_row(wm, lane, r), j = acc_col(wn, lane);
       const int64_t gi = r0 + i, gj = c0 + j;
       const float w = (gi < p.m && gj < p.n) ? p.W[gi * p.n + gj] : 0.0f;
-      sm.sb[j][i] = racc[r] + w;
+      lds[L_CT + j * CP + i] = racc[r] + w;
     }
-    for (int idx = tid; idx < WTT; idx += 256) {
-      const int j = idx >> 6, jq = idx & 63;
-      sm.sl[j][jq] = jq < j ? p.La[(c0 + j) * p.nq + c0 + jq] * (p.alpha[c0 + jq] / p.alpha[c0 + j])
-                            : 0.0f;
+    if (tid < WT) {
+      lds[L_AL + tid] = p.alpha[c0 + tid];
+      lds[L_BE + tid] = p.beta[r0 + tid];
+      lds[L_DA + tid] = p.dA[c0 + tid];
+      lds[L_DB + tid] = p.dB[r0 + tid];
+    }
+    for (int idx = tid; idx < 4 * ST * ST; idx += 256) {  // diagonal La blocks, transposed
+      const int bb = idx >> 8, c2 = (idx >> 4) & 15, c = idx & 15;
+      lds[L_LAD + bb * DP + c * ST + c2] = p.La[(c0 + ST * bb + c2) * p.nq + c0 + ST * bb + c];
     }
     __syncthreads();
     float* Et = blk(p.E, I, J);
+    double dist = 0.0;
+    for (int s = 0; s < 7; ++s) {
+      const int alo = s > 3 ? s - 3 : 0;
+      const int nv = (s < 3 ? s : 3) - alo + 1;
+      const bool src = wave < nv;
+      const int a = alo + (src ? wave : 0), b = s - a;
+      f32x4v P;
+      if (src) subtile_pull(lds, a, b, wave, lane, P);
+      __syncthreads();
+      if (wave == 0) dist += subdiag_chain(p, lds, s, alo, nv, r0, c0, Et, lane);
+      __syncthreads();
+      if (src) subtile_prefix(lds, a, b, lane, P);
+      __syncthreads();
+    }
     if (wave == 0) {
-      double dist = tile_recurrence(p, sm, I, J, Et, lane);
 #pragma unroll
       for (int o = 32; o >= 1; o >>= 1) dist += __shfl_xor(dist, o);
       if (lane == 0) p.dpart[(int64_t)I * NT + J] = dist;
     }
-    __syncthreads();
-    // X[I][J] = Pre + E La[J][J]^T  (residuals already at sa[j][i])
-    stage_kmaj(sm.sb, p.La + c0 * p.nq + c0, p.nq, tid);
-    __syncthreads();
-    mac64(sm.sa, sm.sb, pre, wm, wn, lane);
+    // X[I][J] = Pre + E La[J][J]^T
+    mac64f([&](int i, int k) { return lds[L_ET + k * CP + i]; },
+           [&](int k, int j) { return lds[L_LA + rot(j, k)]; }, pre, wm, wn, lane);
     store_tile(pre, blk(p.X, I, J), wm, wn, lane);
     return;
   }
@@ -320,10 +470,10 @@ __global__ __launch_bounds__(256) void k_wk_diagonal(WkParams p, int d, int nrec
       const int I = Is + 2 + u;
       f32x16 acc;
       load_tile(acc, blk(p.Racc, I, Js), wm, wn, lane);
-      stage_kmaj(sm.sa, p.Lb + (int64_t)I * WT * p.mq + (int64_t)Is * WT, p.mq, tid);
-      stage_omaj(sm.sb, blk(p.X, Is, Js), WT, tid);
+      stage_kmaj(SA, p.Lb + (int64_t)I * WT * p.mq + (int64_t)Is * WT, p.mq, tid);
+      stage_omaj(SB, blk(p.X, Is, Js), WT, tid);
       __syncthreads();
-      mac64(sm.sa, sm.sb, acc, wm, wn, lane);
+      mac64(SA, SB, acc, wm, wn, lane);
       store_tile(acc, blk(p.Racc, I, Js), wm, wn, lane);
       return;
     }
@@ -333,10 +483,10 @@ __global__ __launch_bounds__(256) void k_wk_diagonal(WkParams p, int d, int nrec
       const int J2 = Js + 2 + u;
       f32x16 acc;
       load_tile(acc, blk(p.Pre, Is, J2), wm, wn, lane);
-      stage_omaj(sm.sa, blk(p.E, Is, Js), WT, tid);
-      stage_kmaj(sm.sb, p.La + (int64_t)J2 * WT * p.nq + (int64_t)Js * WT, p.nq, tid);
+      stage_omaj(SA, blk(p.E, Is, Js), WT, tid);
+      stage_kmaj(SB, p.La + (int64_t)J2 * WT * p.nq + (int64_t)Js * WT, p.nq, tid);
       __syncthreads();
-      mac64(sm.sa, sm.sb, acc, wm, wn, lane);
+      mac64(SA, SB, acc, wm, wn, lane);
       store_tile(acc, blk(p.Pre, Is, J2), wm, wn, lane);
       return;
     }
@@ -344,16 +494,21 @@ __global__ __launch_bounds__(256) void k_wk_diagonal(WkParams p, int d, int nrec
   }
 }
 
-// V[i][j] = alpha[j] beta[i] Z[i][j]
-__global__ __launch_bounds__(256) void k_wk_dequant(const int32_t* __restrict__ Z, int64_t m,
-                                                    int64_t n, const float* __restrict__ alpha,
-                                                    const float* __restrict__ beta,
-                                                    float* __restrict__ V, const int* st) {
+// Z[i][j] = Zp[i][j] (padded codes, leading dimension nq) and, when V is
+// non-null, V[i][j] = alpha[j] beta[i] Z[i][j].
+__global__ __launch_bounds__(256) void k_wk_finish(const int32_t* __restrict__ Zp, int64_t nq,
+                                                   int64_t m, int64_t n,
+                                                   const float* __restrict__ alpha,
+                                                   const float* __restrict__ beta,
+                                                   int32_t* __restrict__ Z, float* __restrict__ V,
+                                                   const int* st) {
   if (ff_halted(st)) return;
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (idx >= m * n) return;
   const int64_t i = idx / n, j = idx % n;
-  V[idx] = (alpha[j] * beta[i]) * (float)Z[idx];
+  const int32_t z = Zp[i * nq + j];
+  Z[idx] = z;
+  if (V != nullptr) V[idx] = (alpha[j] * beta[i]) * (float)z;
 }
 
 // out = scale * sum of part[0..count) in a fixed order (one workgroup).
@@ -425,11 +580,12 @@ hipError_t launch_wk_diagonal(const WkParams& p, int d, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_wk_dequant(const int32_t* Z, int64_t m, int64_t n, const float* alpha,
-                             const float* beta, float* V, const int* st, hipStream_t s) {
-  if (m < 1 || n < 1) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_wk_dequant, dim3(blocks_for(m * n)), dim3(256), 0, s, Z, m, n, alpha, beta, V,
-                     st);
+hipError_t launch_wk_finish(const int32_t* Zp, int64_t nq, int64_t m, int64_t n,
+                           const float* alpha, const float* beta, int32_t* Z, float* V,
+                           const int* st, hipStream_t s) {
+  if (m < 1 || n < 1 || nq < n) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_wk_finish, dim3(blocks_for(m * n)), dim3(256), 0, s, Zp, nq, m, n, alpha,
+                     beta, Z, V, st);
   return hipGetLastError();
 }
 

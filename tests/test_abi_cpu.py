@@ -119,11 +119,11 @@ def test_null_handle_calls(lib):
 
 def test_quantize_workspace_sizes(lib):
     b = ff.ff_quantize_workspace_size(4096, 4096)
-    # two padded normalised inverse factors and four tile-blocked accumulators
-    assert 6 * 4096 * 4096 * 4 <= b < 6 * 4096 * 4096 * 4 + (1 << 20)
+    # two padded normalised inverse factors, four tile-blocked accumulators, padded codes
+    assert 7 * 4096 * 4096 * 4 <= b < 7 * 4096 * 4096 * 4 + (1 << 20)
     r = ff.ff_quantize_workspace_size(100, 70)           # padded to 128 x 128 tiles
-    assert 6 * 128 * 128 * 4 <= r < 6 * 128 * 128 * 4 + 8192
-    assert ff.ff_quantize_workspace_size(1, 1) >= 6 * 64 * 64 * 4
+    assert 7 * 128 * 128 * 4 <= r < 7 * 128 * 128 * 4 + 8192
+    assert ff.ff_quantize_workspace_size(1, 1) >= 7 * 64 * 64 * 4
     for m, n in [(0, 5), (5, 0), (-3, 4), ((1 << 20) + 1, 4)]:
         with pytest.raises(ff.FlipFlopError) as ei:
             ff.ff_quantize_workspace_size(m, n)

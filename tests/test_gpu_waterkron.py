@@ -100,7 +100,8 @@ def draw(key, **kw):
 
 @pytest.mark.parametrize("key,shape", [("quant_small", None), ("quant_multi", None),
                                        ("quant_small", (1, 1)), ("quant_small", (5, 130)),
-                                       ("quant_small", (130, 5)), ("quant_small", (64, 64))])
+                                       ("quant_small", (130, 5)), ("quant_small", (64, 64)),
+                                       ("quant_multi", (330, 200)), ("quant_small", (40, 56))])
 def test_given_scales_codes_match_oracle(gpu, key, shape):
     """Algorithm 2 with the oracle's waterfilling scales (rounded to fp32)
     given to both sides: codes identical up to near ties, grid values exact."""
@@ -206,3 +207,53 @@ def test_errors(gpu):
         assert D > 0
     finally:
         h.close()
+
+
+# ---------------------------------------------------------------- full size
+
+@pytest.mark.timeout(600)
+def test_full_size_attention_layer(gpu):
+    """4096 x 4096 weights with power-law factors (cond ~ 1e4): every output
+    in the Babai cell, scales against the oracle, the reported distortion
+    against its definition, and the high-rate law D = gamma^2 |A|^(1/n)
+    |B|^(1/m) / 12 of uniform errors in the cell (Section 3), which holds to
+    the sampling error of 16.7M entries once the step is small next to W."""
+    import time
+    import torch
+    w = synth.quant_workload("quant_attn")
+    t0 = time.perf_counter()
+    d = synth.generate_quant(w)
+    print(f"generated {w.name} in {time.perf_counter() - t0:.1f} s", flush=True)
+    h = _handle(w.m, w.n, gpu)
+    try:
+        W, A, B = _dev(d.W, gpu), _dev(d.A, gpu), _dev(d.B, gpu)
+        h.quantize(W, A, B, gamma=w.gamma)                       # warm
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        Z, V, al, be, Dg = h.quantize(W, A, B, gamma=w.gamma)
+        torch.cuda.synchronize()
+        print(f"ff_quantize {w.m}x{w.n}: {1e3 * (time.perf_counter() - t0):.1f} ms", flush=True)
+    finally:
+        h.close()
+    Z, V = Z.cpu().numpy(), V.cpu().numpy()
+    al, be = al.cpu().numpy().astype(np.float64), be.cpu().numpy().astype(np.float64)
+    A64, B64 = d.A.astype(np.float64), d.B.astype(np.float64)
+    al_r, be_r = oracle.waterfilling_scales(A64, B64, w.gamma)
+    ea, eb = np.max(np.abs(al / al_r - 1)), np.max(np.abs(be / be_r - 1))
+    print(f"scale rel err alpha {ea:.2e} beta {eb:.2e}; max |Z| {np.abs(Z).max()}", flush=True)
+    assert ea < 1e-3 and eb < 1e-3
+    np.testing.assert_array_equal(V, np.outer(be.astype(np.float32), al.astype(np.float32))
+                                  * Z.astype(np.float32))
+    E = transformed_error(V, d.W, A64, B64)
+    ratio = np.abs(E) / (0.5 * np.outer(be, al))
+    print(f"max |E| / (step / 2) = {ratio.max():.6f}; fraction > 1: {np.mean(ratio > 1):.2e}",
+          flush=True)
+    assert ratio.max() <= 1.0 + CELL_SLACK
+    LA, LB = oracle.rev_cholesky(A64), oracle.rev_cholesky(B64)
+    D64 = float(np.mean((np.diag(LB)[:, None] * E * np.diag(LA)[None, :]) ** 2))
+    ldA = 2.0 * np.sum(np.log(np.diag(LA)))
+    ldB = 2.0 * np.sum(np.log(np.diag(LB)))
+    Dpred = w.gamma ** 2 * np.exp(ldA / w.n + ldB / w.m) / 12.0
+    print(f"distortion: reported {Dg:.6e}, fp64 {D64:.6e}, high-rate law {Dpred:.6e}", flush=True)
+    assert abs(Dg - D64) <= 1e-4 * D64
+    assert abs(D64 / Dpred - 1.0) < 5e-3
