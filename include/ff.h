@@ -203,9 +203,11 @@ ff_status ff_quantize_workspace_size(int64_t m, int64_t n, size_t* bytes);
  * distortion: HOST, receives D_{A,B} = ||L^B (V - W) L^A^T||_F^2 / (m n)
  * (Section 2.3), or NULL.  workspace: DEVICE, 256-byte aligned, at least
  * ff_quantize_workspace_size(m, n) bytes, owned by the caller, contents
- * undefined afterwards.  The factorisations run in fp32 on the handle's
- * stream; the handle's factors are untouched (the next ff_iterate
- * refactorises them).  Synchronises the stream.
+ * undefined afterwards.  The factorisations run in fp32, B's on a second
+ * stream the handle creates on first use (ordered after the work already on
+ * the handle's stream and joined back into it); the handle's factors are
+ * untouched (the next ff_iterate refactorises them).  Synchronises the
+ * stream.
  * Errors: FF_ERR_INVALID_ARG, FF_ERR_WORKSPACE, FF_ERR_NOT_SPD (A or B not
  * positive definite), FF_ERR_HIP. */
 ff_status ff_quantize(ff_handle h, const float* W, const float* A, const float* B,

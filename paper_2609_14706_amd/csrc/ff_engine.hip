@@ -204,6 +204,8 @@ Layout make_layout(const ff_config* c) {
 struct ff_handle_s {
   ff_config cfg{};
   hipStream_t stream = nullptr;
+  hipStream_t aux = nullptr;            // second stream of ff_quantize (created on first use)
+  hipEvent_t fork = nullptr, join = nullptr;
   int device = 0;
   int64_t m = 0, n = 0, N = 0;
   bool bf16 = false;
@@ -949,12 +951,27 @@ ff_status ff_quantize(ff_handle h, const float* W, const float* A, const float* 
   h->A.lw_valid = h->B.lw_valid = false;
   const int cur = h->cur;
   ff_status rc;
+  // The two factorisations are independent and latency bound: B's runs on a
+  // second stream, forked from and joined back into the handle's stream.
+  if (h->aux == nullptr) {
+    FF_HIP(hipStreamCreateWithFlags(&h->aux, hipStreamNonBlocking));
+    FF_HIP(hipEventCreateWithFlags(&h->fork, hipEventDisableTiming));
+    FF_HIP(hipEventCreateWithFlags(&h->join, hipEventDisableTiming));
+  }
+  FF_HIP(hipEventRecord(h->fork, h->stream));
+  FF_HIP(hipStreamWaitEvent(h->aux, h->fork, 0));
   if ((rc = quant_side(h, h->A, A != nullptr ? A : h->A.F[cur], q.nq, La, dA, gamma, given, alpha,
                        al)) != FF_OK)
     return rc;
-  if ((rc = quant_side(h, h->B, B != nullptr ? B : h->B.F[cur], q.mq, Lb, dB, gamma, given, beta,
-                       be)) != FF_OK)
-    return rc;
+  {
+    const hipStream_t main = h->stream;
+    h->stream = h->aux;
+    rc = quant_side(h, h->B, B != nullptr ? B : h->B.F[cur], q.mq, Lb, dB, gamma, given, beta, be);
+    h->stream = main;
+    if (rc != FF_OK) return rc;
+  }
+  FF_HIP(hipEventRecord(h->join, h->aux));
+  FF_HIP(hipStreamWaitEvent(h->stream, h->join, 0));
   int st[4];
   if ((rc = read_status(h, st)) != FF_OK) return rc;
   if (st[0] != 0) {
@@ -1013,6 +1030,12 @@ ff_status ff_quantize(ff_handle h, const float* W, const float* A, const float* 
 ff_status ff_destroy(ff_handle h) {
   if (h == nullptr) return FF_OK;
   hipStreamSynchronize(h->stream);
+  if (h->aux != nullptr) {
+    hipStreamSynchronize(h->aux);
+    hipStreamDestroy(h->aux);
+    hipEventDestroy(h->fork);
+    hipEventDestroy(h->join);
+  }
   for (hipEvent_t e : h->events) hipEventDestroy(e);
   delete h;
   return FF_OK;
