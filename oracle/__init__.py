@@ -14,6 +14,8 @@ from .metrics import kron_rel_error, kron_rel_error_scale_free, trace_identity
 from .kron import kron_apply, mismatch_factor
 from .waterkron import (rev_cholesky, normalised_inverse, waterfilling_scales, gptq,
                         two_sided_gptq, distortion)
+from .variants import (frobenius, frobenius_tokens, frob_half_step_A, frob_half_step_B,
+                       marginal_tokens, input_tokens)
 from .tokens import (half_step_A_tokens, half_step_B_tokens, half_step_B_tokens_rows, flipflop_tokens, loglik_tokens,
                      objective_tokens, materialise, token_weights)
 
@@ -23,4 +25,5 @@ __all__ = ["FlipFlopResult", "NotSPDError", "as_f64_samples", "half_step_B", "ha
            "kron_apply", "mismatch_factor", "half_step_A_tokens", "half_step_B_tokens", "half_step_B_tokens_rows",
            "flipflop_tokens", "loglik_tokens", "objective_tokens", "materialise", "token_weights",
            "rev_cholesky", "normalised_inverse", "waterfilling_scales", "gptq", "two_sided_gptq",
-           "distortion"]
+           "distortion", "frobenius", "frobenius_tokens", "frob_half_step_A", "frob_half_step_B",
+           "marginal_tokens", "input_tokens"]

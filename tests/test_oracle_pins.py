@@ -478,3 +478,102 @@ def test_high_rate_distortion():
     D = oracle.distortion(V, W, A, B)
     pred = gamma ** 2 / 12 * np.exp(np.linalg.slogdet(A)[1] / n + np.linalg.slogdet(B)[1] / m)
     assert abs(D / pred - 1.0) < 0.1
+
+
+# ------------------------------------------- Table 1 variants (Section 5 and 6)
+
+def _rearranged(H, m, n):
+    """R[(j, j'), (i, i')] = H[j m + i, j' m + i'] (column-major vec), so that
+    ||H - A (x) B||_F = ||R - vec(A) vec(B)^T||_F (Van Loan and Pitsianis's
+    rearrangement: the best Kronecker approximation is R's top singular pair)."""
+    return H.reshape(n, m, n, m).transpose(0, 2, 1, 3).reshape(n * n, m * m)
+
+
+def _second_moment(G):
+    N, m, n = G.shape
+    V = G.transpose(0, 2, 1).reshape(N, m * n)      # column-major vec: index j m + i
+    return V.T @ V / N
+
+
+def test_frobenius_converges_to_the_best_kronecker_approximation():
+    """Section 5: replacing the inverses by the factors gives a power
+    iteration minimising ||H - A (x) B||_F.  Its fixed point must be the top
+    singular pair of the rearranged H."""
+    rng = np.random.default_rng(11)
+    m, n, N = 3, 4, 30
+    G = rng.standard_normal((N, m, n))
+    G += 0.8 * rng.standard_normal((N, m, 1)) * rng.standard_normal((1, 1, n))
+    H = _second_moment(G)
+    U, S, Vt = np.linalg.svd(_rearranged(H, m, n))
+    assert S[0] > 1.5 * S[1]
+    As = U[:, 0].reshape(n, n)
+    Bs = Vt[0].reshape(m, m)
+    As *= n / np.trace(As)
+    Bs /= np.trace(Bs)
+    res = oracle.frobenius(G, 200)
+    np.testing.assert_allclose(res.A, As, rtol=0, atol=1e-9 * np.abs(As).max())
+    np.testing.assert_allclose(res.B / np.trace(res.B), Bs, rtol=0, atol=1e-9 * np.abs(Bs).max())
+    # and it is the best Kronecker product in Frobenius norm: the FlipFlop
+    # factors, optimally scaled, are no closer to H
+    def resid(A, B):
+        K = np.kron(A, B)
+        s = np.sum(H * K) / np.sum(K * K)
+        return np.linalg.norm(H - s * K)
+    ff = oracle.flipflop(G, 50)
+    assert resid(res.A, res.B) <= resid(ff.A, ff.B) + 1e-12
+
+
+def test_frobenius_and_flipflop_recover_kronecker_factors_on_an_orthogonal_design():
+    """G = S_B Z S_A^T over the complete design Z = sqrt(mn) e_k e_l^T has
+    H = A0 (x) B0 exactly; one iteration of either estimator returns A0, B0
+    (up to the scale exchanged between them)."""
+    rng = np.random.default_rng(12)
+    m, n = 3, 5
+    SA, SB = rng.standard_normal((n, n)), rng.standard_normal((m, m))
+    A0, B0 = SA @ SA.T, SB @ SB.T
+    G = np.stack([SB @ (np.sqrt(m * n) * np.outer(np.eye(m)[k], np.eye(n)[l])) @ SA.T
+                  for k in range(m) for l in range(n)])
+    np.testing.assert_allclose(_second_moment(G), np.kron(A0, B0), atol=1e-10)
+    for res in (oracle.frobenius(G, 1), oracle.flipflop(G, 1)):
+        np.testing.assert_allclose(res.A, A0 * n / np.trace(A0), rtol=1e-10, atol=1e-10)
+        np.testing.assert_allclose(res.B / np.trace(res.B), B0 / np.trace(B0), rtol=1e-10,
+                                   atol=1e-10)
+
+
+def test_marginal_equals_flipflop_and_frobenius_for_independent_tokens():
+    """Tokens made of every pair (x, g) of two sets have H = E[x x^T] (x) E[g g^T]
+    exactly: Marginal (Table 1) must equal the answer of both iterations."""
+    rng = np.random.default_rng(13)
+    m, n, p, q = 4, 6, 9, 7
+    X = rng.standard_normal((p, n)) * np.linspace(0.5, 2.0, n)
+    Gm = rng.standard_normal((q, m))
+    x = np.repeat(X, q, axis=0)
+    g = np.tile(Gm, (p, 1))
+    A, B = oracle.marginal_tokens(x, g)
+    np.testing.assert_allclose(np.trace(A), n)
+    for res in (oracle.flipflop_tokens(x, g, 1), oracle.flipflop_tokens(x, g, 3),
+                oracle.frobenius_tokens(x, g, 2)):
+        np.testing.assert_allclose(res.A, A, rtol=1e-10, atol=1e-12)
+        np.testing.assert_allclose(res.B / np.trace(res.B), B / np.trace(B), rtol=1e-10,
+                                   atol=1e-12)
+    # FlipFlop keeps the scale of H: its product is the marginal product
+    ff = oracle.flipflop_tokens(x, g, 1)
+    np.testing.assert_allclose(np.kron(ff.A, ff.B), np.kron(X.T @ X / p, Gm.T @ Gm / q),
+                               rtol=1e-10, atol=1e-12)
+    # Input: the same A, B = c I
+    Ai, Bi = oracle.input_tokens(x, m)
+    np.testing.assert_allclose(Ai, A, rtol=1e-12)
+    np.testing.assert_allclose(Bi, Bi[0, 0] * np.eye(m))
+
+
+def test_frobenius_tokens_equal_dense_frobenius_on_materialised_samples():
+    rng = np.random.default_rng(14)
+    x = rng.standard_normal((40, 5))
+    g = rng.standard_normal((40, 3))
+    a = oracle.frobenius_tokens(x, g, 3, damping=0.1)
+    b = oracle.frobenius(oracle.materialise(x, g), 3, damping=0.1)
+    np.testing.assert_allclose(a.A, b.A, rtol=1e-11)
+    np.testing.assert_allclose(a.B, b.B, rtol=1e-11)
+    c = oracle.frobenius_tokens(x, g, 3, order="A_FIRST")
+    d = oracle.frobenius(oracle.materialise(x, g), 3, order="A_FIRST")
+    np.testing.assert_allclose(c.A, d.A, rtol=1e-11)
