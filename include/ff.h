@@ -82,6 +82,34 @@ typedef enum { FF_APPLY = 0, FF_APPLY_INV = 1 } ff_apply_mode;
  * applied to these G_t; the cost per iteration is 2 N (m^2 + n^2). */
 typedef enum { FF_SAMPLES_DENSE = 0, FF_SAMPLES_RANK1 = 1 } ff_sample_form;
 
+/* Which Kronecker approximation A (x) B of H = E[x x^T (x) g g^T] the
+ * iteration computes (Table 1).  Every estimator ends each iteration with
+ * the trace normalisation tr(A) = n and applies the damping option after
+ * each update.
+ *   FF_EST_FLIPFLOP: the flip-flop iteration (Section 5), the default.
+ *   FF_EST_FROBENIUS: the same iteration with the factors in place of their
+ *     inverses, B <- (1/(N n)) sum_i G_i A G_i^T, A <- (1/(N m)) sum_i G_i^T B G_i
+ *     (rank-one form: weights x^T A x and g^T B g), a power iteration for
+ *     min ||H - A (x) B||_F (Section 5).  The whitening operand is
+ *     RevCholesky of the other factor (Y lower, Y^T Y = F, Section 2), from
+ *     an fp32 factorisation: a factor beyond fp32's reach (condition number
+ *     above ~1e7, which the undamped iteration reaches on few samples) is
+ *     reported as FF_ERR_NOT_SPD; the paper damps every iteration
+ *     (Appendix B).  Only FF_ORDER_B_FIRST: with A first, the trace
+ *     normalisation leaves B's scale growing doubly exponentially.
+ *   FF_EST_MARGINAL: A = E[x x^T], B = E[g g^T] (means over the tokens).
+ *   FF_EST_INPUT: A = E[x x^T], B = I_m.
+ * MARGINAL and INPUT need the rank-one form (they are functions of the
+ * tokens, not of G_t); every iteration recomputes the same estimate.  The
+ * per-iteration log-likelihood of ff_iterate is the matrix-normal one for
+ * FLIPFLOP only; the other estimators report NaN. */
+typedef enum {
+  FF_EST_FLIPFLOP = 0,
+  FF_EST_FROBENIUS = 1,
+  FF_EST_MARGINAL = 2,
+  FF_EST_INPUT = 3
+} ff_estimator;
+
 typedef struct {
   int64_t m, n, N;        /* G is [N][m][n], row-major, contiguous; all >= 1
                              (RANK1: N = number of tokens) */
@@ -107,6 +135,8 @@ typedef struct {
                              dtype, 16-byte aligned, BORROWED like G.  G is
                              ignored (may be NULL) */
   const void* g;          /* RANK1: DEVICE [N][m] token output gradients */
+  ff_estimator estimator; /* 0 = FF_EST_FLIPFLOP; FROBENIUS needs B_FIRST,
+                             MARGINAL and INPUT need FF_SAMPLES_RANK1 */
 } ff_config;
 
 /* Bytes of device workspace ff_init needs for cfg (only the shape, dtype and

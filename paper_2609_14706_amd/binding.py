@@ -20,6 +20,9 @@ FF_ORDER_B_FIRST, FF_ORDER_A_FIRST = 0, 1
 FF_APPLY, FF_APPLY_INV = 0, 1
 FF_SAMPLES_DENSE, FF_SAMPLES_RANK1 = 0, 1
 FF_SCALES_WATERFILL, FF_SCALES_GIVEN = 0, 1
+FF_EST_FLIPFLOP, FF_EST_FROBENIUS, FF_EST_MARGINAL, FF_EST_INPUT = 0, 1, 2, 3
+ESTIMATORS = {"flipflop": FF_EST_FLIPFLOP, "frobenius": FF_EST_FROBENIUS,
+              "marginal": FF_EST_MARGINAL, "input": FF_EST_INPUT}
 KERNEL_IDS = {"whiten": 0, "syrk": 1, "reduce": 2, "cholinv": 3, "quant_diag": 4}
 
 
@@ -41,6 +44,7 @@ class ff_config(ctypes.Structure):
         ("form", ctypes.c_int),
         ("x", ctypes.c_void_p),
         ("g", ctypes.c_void_p),
+        ("estimator", ctypes.c_int),
     ]
 
 
@@ -191,10 +195,13 @@ class FlipFlop:
     """
 
     def __init__(self, G=None, *, tokens=None, order: str = "B_FIRST", damping: float = 0.0,
-                 A0=None, B0=None, whiten_split: int = 1, stream=None, workspace=None):
+                 A0=None, B0=None, whiten_split: int = 1, stream=None, workspace=None,
+                 estimator: str = "flipflop"):
         """G: (N, m, n) samples; or tokens = (x, g) with x (N, n) inputs and
         g (N, m) output gradients, the samples being G_t = g_t x_t^T (the
-        rank-one form; both tensors of one dtype)."""
+        rank-one form; both tensors of one dtype).  estimator: "flipflop",
+        "frobenius", "marginal" or "input" (Table 1; the last two need
+        tokens)."""
         import torch
         if (G is None) == (tokens is None):
             raise ValueError("give either G or tokens=(x, g)")
@@ -230,6 +237,7 @@ class FlipFlop:
         cfg.m, cfg.n, cfg.N = self.m, self.n, self.N
         cfg.dtype = dt
         cfg.form = form
+        cfg.estimator = ESTIMATORS[estimator]
         if form == FF_SAMPLES_RANK1:
             self._keep = [x, g]
             cfg.x, cfg.g = x.data_ptr(), g.data_ptr()

@@ -220,6 +220,28 @@ __global__ __launch_bounds__(256) void k_copy_f32(const float* __restrict__ src,
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count; i += stride) dst[i] = src[i];
 }
 
+__global__ __launch_bounds__(256) void k_copy2d_f32(const float* __restrict__ src, int64_t lds,
+                                                    float* __restrict__ dst, int64_t ldd,
+                                                    int64_t rows, int64_t cols, const int* st) {
+  if (ff_halted(st)) return;
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < rows * cols; i += stride) {
+    const int64_t r = i / cols, c = i % cols;
+    dst[r * ldd + c] = src[r * lds + c];
+  }
+}
+
+// Y = J C^T J from the lower Cholesky factor C of J M J (RevCholesky, Section 2).
+__global__ __launch_bounds__(256) void k_rev_transpose(const float* __restrict__ C, int64_t d,
+                                                       float* __restrict__ Y, const int* st) {
+  if (ff_halted(st)) return;
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  for (int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x; k < d * d; k += stride) {
+    const int64_t i = k / d, j = k % d;
+    Y[k] = i >= j ? C[(d - 1 - j) * d + (d - 1 - i)] : 0.0f;
+  }
+}
+
 __global__ __launch_bounds__(256) void k_fill_f32(float* dst, int64_t count, float v) {
   const int64_t stride = (int64_t)gridDim.x * 256;
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count; i += stride) dst[i] = v;
@@ -340,6 +362,21 @@ hipError_t launch_objective_terms(const float* a, const float* b, int64_t count,
 hipError_t launch_copy_f32(const float* src, float* dst, int64_t count, const int* st,
                            hipStream_t s) {
   hipLaunchKernelGGL(k_copy_f32, dim3(grid_for(count)), dim3(256), 0, s, src, dst, count, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy2d_f32(const float* src, int64_t lds, float* dst, int64_t ldd, int64_t rows,
+                             int64_t cols, const int* st, hipStream_t s) {
+  if (rows < 0 || cols < 0 || lds < cols || ldd < cols) return hipErrorInvalidValue;
+  if (rows == 0 || cols == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_copy2d_f32, dim3(grid_for(rows * cols)), dim3(256), 0, s, src, lds, dst, ldd,
+                     rows, cols, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_rev_transpose(const float* C, int64_t d, float* Y, const int* st, hipStream_t s) {
+  if (d < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_rev_transpose, dim3(grid_for(d * d)), dim3(256), 0, s, C, d, Y, st);
   return hipGetLastError();
 }
 

@@ -211,10 +211,10 @@ __device__ __forceinline__ int cholinv_lds(LeafLDS& sm, int o, int wave, int lan
   return -1;
 }
 
-__global__ __launch_bounds__(256) void k_chol_leaf(const float* __restrict__ Lblk,
-                                                   float* __restrict__ Liblk, int64_t ld, int b,
-                                                   int64_t pivot_base, double* logdet, int slot,
-                                                   int iteration, int side, int* st) {
+__global__ __launch_bounds__(256) void k_chol_leaf(const float* Lblk, float* __restrict__ Liblk,
+                                                   int64_t ld, int b, int64_t pivot_base,
+                                                   double* logdet, int slot, int iteration,
+                                                   int side, int* st, float* Lout) {
   if (ff_halted(st)) return;
   __shared__ LeafLDS sm;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -277,6 +277,10 @@ __global__ __launch_bounds__(256) void k_chol_leaf(const float* __restrict__ Lbl
   if (j < b) {
 #pragma unroll 8
     for (int i = i0; i < b; i += 2) Liblk[(int64_t)i * ld + j] = j <= i ? sm.X[i][j] : 0.0f;
+    if (Lout != nullptr) {  // the factor itself, over the block it was read from
+#pragma unroll 8
+      for (int i = i0; i < b; i += 2) Lout[(int64_t)i * ld + j] = j <= i ? sm.S[i][j] : 0.0f;
+    }
   }
 }
 
@@ -284,10 +288,11 @@ __global__ __launch_bounds__(256) void k_chol_leaf(const float* __restrict__ Lbl
 
 hipError_t launch_chol_leaf(const float* Lblk, float* Liblk, int64_t ld, int b, int64_t pivot_base,
                             double* logdet, int slot, int iteration, int side, int* st,
-                            hipStream_t s) {
+                            hipStream_t s, float* Lout) {
   if (b < 1 || b > kLeaf || ld < b) return hipErrorInvalidValue;
+  if (Lout != nullptr && Lout != Lblk) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_chol_leaf, dim3(1), dim3(256), 0, s, Lblk, Liblk, ld, b, pivot_base, logdet,
-                     slot, iteration, side, st);
+                     slot, iteration, side, st, Lout);
   return hipGetLastError();
 }
 

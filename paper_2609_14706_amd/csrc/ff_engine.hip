@@ -125,6 +125,14 @@ ff_status validate_shape(const ff_config* c) {
     return fail(FF_ERR_INVALID_ARG, "N must be <= 65535");
   if (c->form == FF_SAMPLES_RANK1 && c->N > (1 << 22))
     return fail(FF_ERR_INVALID_ARG, "N (tokens) must be <= 4194304");
+  if (c->estimator < FF_EST_FLIPFLOP || c->estimator > FF_EST_INPUT)
+    return fail(FF_ERR_INVALID_ARG, "unknown estimator");
+  if (c->estimator == FF_EST_FROBENIUS && c->order != FF_ORDER_B_FIRST)
+    return fail(FF_ERR_INVALID_ARG,
+                "the Frobenius iteration runs B first (with A first its scale diverges)");
+  if ((c->estimator == FF_EST_MARGINAL || c->estimator == FF_EST_INPUT) &&
+      c->form != FF_SAMPLES_RANK1)
+    return fail(FF_ERR_INVALID_ARG, "the Marginal and Input estimators need the rank-one form");
   if (c->m > (1 << 20) || c->n > (1 << 20))
     return fail(FF_ERR_INVALID_ARG, "m and n must be <= 1048576");
   if (is_bf16(c) && c->whiten_split != 1 && c->whiten_split != 2)
@@ -271,16 +279,20 @@ void collect_timing(ff_handle_s* h) {
 }
 
 // ------------------------------------------------------- factorisation
-ff_status cholinv_rec(ff_handle_s* h, Side& s, int64_t o, int64_t sz, int iteration) {
+// keepL: leave the Cholesky factor itself in the lower triangle of s.L (the
+// recursion's scratch then goes to the unused upper blocks of s.L).
+ff_status cholinv_rec(ff_handle_s* h, Side& s, int64_t o, int64_t sz, int iteration,
+                      bool keepL = false) {
   const int64_t d = s.dim;
   if (sz <= kLeaf) {
-    FF_HIP(launch_chol_leaf(s.L + o * d + o, s.Li + o * d + o, d, (int)sz, o, s.slots,
-                            (int)(o / kLeaf), iteration, s.code, h->st, h->stream));
+    float* blk = s.L + o * d + o;
+    FF_HIP(launch_chol_leaf(blk, s.Li + o * d + o, d, (int)sz, o, s.slots, (int)(o / kLeaf),
+                            iteration, s.code, h->st, h->stream, keepL ? blk : nullptr));
     return FF_OK;
   }
   const int64_t nl = (sz + kLeaf - 1) / kLeaf;
   const int64_t hh = (nl + 1) / 2 * kLeaf, r = sz - hh;
-  ff_status rc = cholinv_rec(h, s, o, hh, iteration);
+  ff_status rc = cholinv_rec(h, s, o, hh, iteration, keepL);
   if (rc != FF_OK) return rc;
   float* L21 = s.L + (o + hh) * d + o;
   float* L22 = s.L + (o + hh) * d + (o + hh);
@@ -300,8 +312,22 @@ ff_status cholinv_rec(ff_handle_s* h, Side& s, int64_t o, int64_t sz, int iterat
   g.A = Li21; g.B = Li21; g.C = L22; g.M = r; g.N = r; g.K = hh;
   g.transA = 0; g.transB = 1; g.alpha = -1.f; g.beta = 1.f; g.flags = kCLower;
   FF_HIP(launch_gemm_f32(g, 1, h->stream));
-  rc = cholinv_rec(h, s, o + hh, r, iteration);
+  rc = cholinv_rec(h, s, o + hh, r, iteration, keepL);
   if (rc != FF_OK) return rc;
+  if (keepL) {
+    // X^T = (L21 Li11)^T = Li11^T L21^T into the A12 block (hh x r, above the diagonal)
+    float* Xt = s.L + o * d + (o + hh);
+    g.A = Li11; g.B = Li21; g.C = Xt; g.M = hh; g.N = r; g.K = hh;
+    g.transA = 1; g.transB = 1; g.alpha = 1.f; g.beta = 0.f; g.flags = kKLoRow;
+    FF_HIP(launch_gemm_f32(g, 1, h->stream));
+    // L21 (parked in Li21) into its place in L
+    FF_HIP(launch_copy2d_f32(Li21, d, L21, d, r, hh, h->st, h->stream));
+    // Li21 <- -Li22 X
+    g.A = Li22; g.B = Xt; g.C = Li21; g.M = r; g.N = hh; g.K = r;
+    g.transA = 0; g.transB = 1; g.alpha = -1.f; g.beta = 0.f; g.flags = kKHiRow;
+    FF_HIP(launch_gemm_f32(g, 1, h->stream));
+    return FF_OK;
+  }
   // X <- L21 Li11  (into the A21 block, no longer needed)
   g.A = Li21; g.B = Li11; g.C = L21; g.M = r; g.N = hh; g.K = hh;
   g.transA = 0; g.transB = 0; g.alpha = 1.f; g.beta = 0.f; g.flags = kKLoCol;
@@ -326,6 +352,26 @@ ff_status cholinv_from(ff_handle_s* h, Side& s, const float* src, int iteration)
 
 ff_status cholinv(ff_handle_s* h, Side& s, int slot, int iteration) {
   return cholinv_from(h, s, s.F[slot], iteration);
+}
+
+// Frobenius estimator: the whitening operand is Y = RevCholesky(F) = J C^T J
+// with C = Cholesky(J F J): Y is lower triangular with Y^T Y = F, so the
+// whitened samples X Y^T give X F X^T in the symmetric product.  Y goes where
+// L^-1 goes (s.Li, zeros above the diagonal) and into s.Lw; log|F| into s.slots.
+ff_status revchol_operand(ff_handle_s* h, Side& s, const float* src, int iteration) {
+  Timed t(h, 3, (double)s.dim * s.dim * s.dim / 3.0);
+  FF_HIP(launch_wk_reverse(src, s.dim, s.L, h->st, h->stream));
+  ff_status rc = cholinv_rec(h, s, 0, s.dim, iteration, true);
+  if (rc != FF_OK) return rc;
+  FF_HIP(launch_rev_transpose(s.L, s.dim, s.Li, h->st, h->stream));
+  FF_HIP(launch_convert_inverse(s.Li, s.dim, s.Lw, s.Lw2, s.dim_p, h->elem, h->st, h->stream));
+  return FF_OK;
+}
+
+// The whitening operand of the estimator for factor s.F[slot].
+ff_status operand(ff_handle_s* h, Side& s, int slot, int iteration) {
+  if (h->cfg.estimator == FF_EST_FROBENIUS) return revchol_operand(h, s, s.F[slot], iteration);
+  return cholinv(h, s, slot, iteration);
 }
 
 // Rank-one form: token weights wbuf[t] = ||L_p^-1 v_t||^2 for the token
@@ -359,13 +405,20 @@ ff_status token_weights(ff_handle_s* h, Side& p, float* wbuf) {
 // Rank-one form of the half step (Section 5): s.F[slot] =
 // (1/(N p.dim)) sum_t ||L_p^-1 v_t||^2 u_t u_t^T with u_t the token vector of
 // side s, as a symmetric product over tokens of the weighted, transposed u.
-ff_status update_rank1(ff_handle_s* h, Side& s, Side& p, int slot, bool finish) {
+// unit: all weights 1 and scale 1/N (the token mean E[u u^T] of the Marginal
+// and Input estimators, Table 1).
+ff_status update_rank1(ff_handle_s* h, Side& s, Side& p, int slot, bool finish,
+                       bool unit = false) {
   float* wbuf = h->wv;
-  ff_status rc = token_weights(h, p, wbuf);
-  if (rc != FF_OK) return rc;
-  const void* U = (&s == &h->B) ? h->Gt : h->Gx;
   const int64_t T_p = h->lay.T_p;
-  const double scale = 1.0 / ((double)h->N * (double)p.dim);
+  if (unit) {
+    FF_HIP(launch_fill_f32(wbuf, T_p, 1.0f, h->stream));
+  } else {
+    ff_status rc = token_weights(h, p, wbuf);
+    if (rc != FF_OK) return rc;
+  }
+  const void* U = (&s == &h->B) ? h->Gt : h->Gx;
+  const double scale = unit ? 1.0 / (double)h->N : 1.0 / ((double)h->N * (double)p.dim);
   const double sflop = (double)h->N * s.dim * s.dim;
   // tokens in segments of kTokenSeg: the product streams short rows
   const int64_t seg = kTokenSeg, nseg = T_p / kTokenSeg;
@@ -479,29 +532,63 @@ ff_status clear_status(ff_handle_s* h) {
 // the one iteration g + 1 needs, so its failure is attributed to g + 1:
 // iteration g is complete (the oracle also returns such a singular factor),
 // and only a later iteration that would invert it fails.
+// Marginal / Input estimators (Table 1): token means, no factorisation.
+ff_status iterate_means(ff_handle_s* h, int iters, int* done, double* loglik) {
+  *done = 0;
+  const int64_t base = h->iters_total;
+  ff_status rc;
+  for (int k = 1; k <= iters; ++k) {
+    const int slot = (int)((base + k) & 1);
+    if ((rc = update_rank1(h, h->A, h->B, slot, true, true)) != FF_OK) return rc;
+    if (h->cfg.estimator == FF_EST_MARGINAL) {
+      if ((rc = update_rank1(h, h->B, h->A, slot, true, true)) != FF_OK) return rc;
+    } else {
+      FF_HIP(launch_identity_f32(h->B.F[slot], h->m, h->stream));
+      FF_HIP(launch_trace_damp(h->B.F[slot], h->m, h->cfg.damping, h->B.tr, h->st, h->stream));
+    }
+    FF_HIP(launch_normalise(h->A.F[slot], h->n, h->B.F[slot], h->m, h->A.tr, h->c, h->st,
+                            h->stream));
+  }
+  int st[4];
+  if ((rc = read_status(h, st)) != FF_OK) return rc;
+  if (h->timing) collect_timing(h);
+  if (st[0] != 0) return fail(FF_ERR_STATE, "device status set during the token means");
+  if (loglik != nullptr)
+    for (int k = 0; k < iters; ++k) loglik[k] = NAN;
+  h->iters_total = base + iters;
+  h->cur = (int)(h->iters_total & 1);
+  h->A.lw_valid = h->B.lw_valid = false;
+  *done = iters;
+  return FF_OK;
+}
+
 ff_status iterate_chunk(ff_handle_s* h, int iters, int* done, double* loglik) {
+  if (h->cfg.estimator == FF_EST_MARGINAL || h->cfg.estimator == FF_EST_INPUT)
+    return iterate_means(h, iters, done, loglik);
   *done = 0;
   const bool bfirst = h->cfg.order == FF_ORDER_B_FIRST;
+  const bool flipflop = h->cfg.estimator == FF_EST_FLIPFLOP;
   Side& first = bfirst ? h->B : h->A;
   Side& second = bfirst ? h->A : h->B;
   const int64_t base = h->iters_total;
   ff_status rc;
   if (!second.lw_valid) {
-    rc = cholinv(h, second, h->cur, (int)(base + 1));
+    rc = operand(h, second, h->cur, (int)(base + 1));
     if (rc != FF_OK) return rc;
   }
   for (int k = 1; k <= iters; ++k) {
     const int64_t g = base + k;
     const int slot = (int)(g & 1);
     if ((rc = update(h, first, second, slot)) != FF_OK) return rc;
-    if ((rc = cholinv(h, first, slot, (int)g)) != FF_OK) return rc;
+    if ((rc = operand(h, first, slot, (int)g)) != FF_OK) return rc;
     if ((rc = update(h, second, first, slot)) != FF_OK) return rc;
     FF_HIP(launch_normalise(h->A.F[slot], h->n, h->B.F[slot], h->m, h->A.tr, h->c, h->st,
                             h->stream));
-    if ((rc = cholinv(h, second, slot, (int)(g + 1))) != FF_OK) return rc;
-    FF_HIP(launch_loglik(h->A.slots, h->A.nslots, h->B.slots, h->B.nslots, h->c, bfirst ? 1 : 0,
-                         (double)h->m, (double)h->n, (double)h->N, h->ll + (k - 1), h->st,
-                         h->stream));
+    if ((rc = operand(h, second, slot, (int)(g + 1))) != FF_OK) return rc;
+    if (flipflop)
+      FF_HIP(launch_loglik(h->A.slots, h->A.nslots, h->B.slots, h->B.nslots, h->c, bfirst ? 1 : 0,
+                           (double)h->m, (double)h->n, (double)h->N, h->ll + (k - 1), h->st,
+                           h->stream));
   }
   int st[4];
   if ((rc = read_status(h, st)) != FF_OK) return rc;
@@ -509,7 +596,10 @@ ff_status iterate_chunk(ff_handle_s* h, int iters, int* done, double* loglik) {
   int completed = iters;
   if (st[0] != 0) completed = (int)std::max<int64_t>(0, std::min<int64_t>(iters, st[0] - 1 - base));
   if (loglik != nullptr && completed > 0) {
-    FF_HIP(hipMemcpy(loglik, h->ll, sizeof(double) * completed, hipMemcpyDeviceToHost));
+    if (flipflop)
+      FF_HIP(hipMemcpy(loglik, h->ll, sizeof(double) * completed, hipMemcpyDeviceToHost));
+    else
+      for (int k = 0; k < completed; ++k) loglik[k] = NAN;
     if (st[0] != 0) loglik[completed - 1] = NAN;  // its closing factorisation failed
   }
   h->iters_total = base + completed;
@@ -785,6 +875,8 @@ ff_status ff_kron_apply(ff_handle h, const float* X, float* Y, int64_t batch, ff
     // Fresh factorisations of the current factors (label 0 marks them).
     if ((rc = cholinv(h, h->A, cur, -1)) != FF_OK) return rc;
     if ((rc = cholinv(h, h->B, cur, -1)) != FF_OK) return rc;
+    // the cached whitening operands of the other estimators are now stale
+    if (h->cfg.estimator != FF_EST_FLIPFLOP) h->A.lw_valid = h->B.lw_valid = false;
   }
   float* T = (float*)h->W;
   const size_t tcap = h->lay.w_bytes / sizeof(float);  // >= m n floats

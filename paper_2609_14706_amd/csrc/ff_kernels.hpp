@@ -80,10 +80,11 @@ constexpr int kLeaf = 128;  // diagonal block factorised inside one workgroup
 // Cholesky + inverse of a diagonal block of size b <= kLeaf.  Reads the lower
 // triangle of Lblk (ld), writes Li block (lower, zeros above), writes
 // sum(log diag L) to logdet[slot]; on a non-positive/NaN pivot sets
-// st = {iteration, side, pivot_base + j}.
+// st = {iteration, side, pivot_base + j}.  Lout (null, or equal to Lblk):
+// the factor L is also written over the block (lower, zeros above).
 hipError_t launch_chol_leaf(const float* Lblk, float* Liblk, int64_t ld, int b, int64_t pivot_base,
                             double* logdet, int slot, int iteration, int side, int* st,
-                            hipStream_t s);
+                            hipStream_t s, float* Lout = nullptr);
 
 // out[s][r][c] (rows_p x cols_p) from G[s] (m x n): copy (transpose = 0,
 // rows_p >= m, cols_p >= n) or transpose (transpose = 1, rows_p >= n,
@@ -131,6 +132,12 @@ hipError_t launch_objective_terms(const float* a, const float* b, int64_t count,
 
 hipError_t launch_copy_f32(const float* src, float* dst, int64_t count, const int* st,
                            hipStream_t s);
+// dst[r][c] = src[r][c] for r < rows, c < cols (leading dimensions lds, ldd).
+hipError_t launch_copy2d_f32(const float* src, int64_t lds, float* dst, int64_t ldd, int64_t rows,
+                             int64_t cols, const int* st, hipStream_t s);
+// Y[i][j] = C[d-1-j][d-1-i] for i >= j, 0 above: with C = Cholesky(J M J),
+// Y = J C^T J is lower triangular with Y^T Y = M (RevCholesky(M), Section 2).
+hipError_t launch_rev_transpose(const float* C, int64_t d, float* Y, const int* st, hipStream_t s);
 hipError_t launch_fill_f32(float* dst, int64_t count, float v, hipStream_t s);
 hipError_t launch_identity_f32(float* dst, int64_t dim, hipStream_t s);
 hipError_t launch_set_int(int* dst, int64_t count, int v, hipStream_t s);

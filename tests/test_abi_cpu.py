@@ -136,3 +136,20 @@ def test_quantize_rejects_null_handle(lib):
                            ctypes.byref(d), None, 0) == ff.FF_ERR_INVALID_ARG
     assert "handle" in ff.ff_last_error()
     assert lib.ff_objective(None, None, None, ctypes.byref(d)) == ff.FF_ERR_INVALID_ARG
+
+
+def test_estimator_validation(lib):
+    c = cfg()
+    c.estimator = 7
+    with pytest.raises(ff.FlipFlopError) as ei:
+        ff.ff_workspace_size(c)
+    assert ei.value.code == ff.FF_ERR_INVALID_ARG and "estimator" in ff.ff_last_error()
+    for est in (ff.FF_EST_MARGINAL, ff.FF_EST_INPUT):     # token means need the rank-one form
+        c.estimator = est
+        with pytest.raises(ff.FlipFlopError):
+            ff.ff_workspace_size(c)
+        c.form = ff.FF_SAMPLES_RANK1
+        assert ff.ff_workspace_size(c) > 0
+        c.form = ff.FF_SAMPLES_DENSE
+    c.estimator = ff.FF_EST_FROBENIUS
+    assert ff.ff_workspace_size(c) == ff.ff_workspace_size(cfg())
