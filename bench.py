@@ -47,7 +47,7 @@ def recorded_traffic(kernel: str, workload: str):
 PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 
 
-def cpu_baseline(G, w, budget_s: float):
+def cpu_baseline(G, w, budget_s: float, estimator: str = "flipflop"):
     """Oracle time of one iteration, from a bounded number of samples.
 
     Both half steps are timed on the first k samples (k grows until the
@@ -76,19 +76,23 @@ def cpu_baseline(G, w, budget_s: float):
         Gs = np.concatenate(host)
         t0 = time.perf_counter()
         Gk = oracle.as_f64_samples(Gs[-1:])
-        oracle.half_step_B(Gk, In)
-        oracle.half_step_A(Gk, Im)
+        if estimator == "frobenius":
+            oracle.frob_half_step_B(Gk, In)
+            oracle.frob_half_step_A(Gk, Im)
+        else:
+            oracle.half_step_B(Gk, In)
+            oracle.half_step_A(Gk, Im)
         t_total += time.perf_counter() - t0
         k += 1
     per_iter = t_total / k * w.N
     threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"]
                   or [1])
     return {"value": 1.0 / per_iter, "unit": "iter/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"both fp64 half steps (direct cho_solve + dgemm form) on {k} of {w.N} samples "
+            "sample": f"both fp64 {estimator} half steps (direct form) on {k} of {w.N} samples "
                       f"of {w.name}, {t_total:.1f} s, scaled to a full iteration ({per_iter:.1f} s)"}
 
 
-def cpu_baseline_tokens(x, g, w, budget_s: float):
+def cpu_baseline_tokens(x, g, w, budget_s: float, estimator: str = "flipflop"):
     """Oracle time of one iteration of the per-token form, from a bounded
     number of tokens: both half steps on the first k tokens (k grows in
     blocks of 4096 until the budget is used), against fixed SPD factors,
@@ -108,15 +112,22 @@ def cpu_baseline_tokens(x, g, w, budget_s: float):
         gs = g[k:k + kb].view(torch.int16).cpu().numpy().view(np.uint16) if g.dtype == torch.bfloat16 \
             else g[k:k + kb].cpu().numpy()
         t0 = time.perf_counter()
-        oracle.half_step_B_tokens(xs, gs, In)
-        oracle.half_step_A_tokens(xs, gs, Im)
+        if estimator == "marginal":
+            oracle.marginal_tokens(xs, gs)
+        elif estimator == "input":
+            oracle.input_tokens(xs, w.m)
+        elif estimator == "frobenius":
+            oracle.frobenius_tokens(xs, gs, 1)
+        else:
+            oracle.half_step_B_tokens(xs, gs, In)
+            oracle.half_step_A_tokens(xs, gs, Im)
         t_total += time.perf_counter() - t0
         k += kb
     per_iter = t_total * w.T / k
     cores = max((i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"),
                 default=1)
     return {"value": 1.0 / per_iter, "unit": "iter/s", "cores": cores, "kind": "oracle",
-            "sample": f"both fp64 rank-one half steps on {k} of {w.T} tokens of {w.name}, "
+            "sample": f"fp64 {estimator} estimate (rank-one form) on {k} of {w.T} tokens of {w.name}, "
                       f"{t_total:.1f} s, scaled to a full iteration ({per_iter:.1f} s)"}
 
 
@@ -237,6 +248,9 @@ def main():
                          " | quant_small | quant_multi | quant_attn")
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--whiten-split", type=int, default=1)
+    ap.add_argument("--estimator", default="flipflop",
+                    help="flipflop | frobenius | marginal | input (Table 1; the last two need tokens)")
+    ap.add_argument("--damping", type=float, default=0.0, help="kappa (Appendix B damping)")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
@@ -278,7 +292,8 @@ def main():
     stream = torch.cuda.current_stream(dev)
 
     if args.warmup > 0:
-        f = ffe.FlipFlop(**src, whiten_split=args.whiten_split, workspace=ws, stream=stream)
+        f = ffe.FlipFlop(**src, whiten_split=args.whiten_split, workspace=ws, stream=stream,
+                         estimator=args.estimator, damping=args.damping)
         f.iterate(args.warmup)
         f.close()
     torch.cuda.synchronize()
@@ -288,7 +303,8 @@ def main():
     ev1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     ev0.record(stream)
-    f = ffe.FlipFlop(**src, whiten_split=args.whiten_split, workspace=ws, stream=stream)
+    f = ffe.FlipFlop(**src, whiten_split=args.whiten_split, workspace=ws, stream=stream,
+                     estimator=args.estimator, damping=args.damping)
     f.set_timing(True)
     ll = f.iterate(args.steps)
     ev1.record(stream)
@@ -299,6 +315,8 @@ def main():
     ms_per_step = ms_total / args.steps
     iters_per_s = 1000.0 / ms_per_step
     flop_iter = w.flop_per_iter
+    if args.estimator in ("marginal", "input"):   # token means: symmetric products only
+        flop_iter = float(w.T) * (w.n * w.n + (w.m * w.m if args.estimator == "marginal" else 0))
     tflops = flop_iter / (ms_per_step * 1e-3) / 1e12
     peak = PEAK_TFLOPS[w.dtype]
     print(f"[bench] {args.steps} iterations in {ms_total:.2f} ms; kernels: " +
@@ -319,9 +337,15 @@ def main():
 
     if w.dtype == "bf16":
         roofline["traffic"] = recorded_traffic(roofline["kernel"], w.name)
+    flipflop = args.estimator == "flipflop"
+    if flipflop:
+        metric = (METRIC if not tokens else
+                  f"flip-flop iter/s + TFLOP/s, per-token form, m={w.m} n={w.n} T={w.T}")
+    else:
+        metric = (f"{args.estimator} estimator iter/s, m={w.m} n={w.n} " +
+                  (f"T={w.T}" if tokens else f"N={N}"))
     out = {
-        "metric": METRIC if not tokens else
-        f"flip-flop iter/s + TFLOP/s, per-token form, m={w.m} n={w.n} T={w.T}",
+        "metric": metric,
         "value": round(iters_per_s, 4),
         "unit": "iter/s",
         "n_gpus": 1,
@@ -335,19 +359,20 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "m": w.m, "n": w.n, ("T" if tokens else "N"): N,
                    "timed_job": f"ff_init + {args.steps} iterations",
-                   "whiten_split": args.whiten_split},
+                   "whiten_split": args.whiten_split, "estimator": args.estimator,
+                   "damping": args.damping},
         "tflops": round(tflops, 2),
         "pct_peak": round(100.0 * tflops / peak, 2),
         "alg_flop_per_iter": flop_iter,
-        "loglik_last": ll[-1] if ll else None,
+        "loglik_last": ll[-1] if ll and args.estimator == "flipflop" else None,
         "kernels_ms": {k: round(ms, 3) for k, (n, ms, _) in kern.items()},
         "roofline": roofline,
         "cpu_baseline": None,
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the fp64 oracle on host cores", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = (cpu_baseline_tokens(x, g, w, args.cpu_budget) if tokens
-                               else cpu_baseline(G, w, args.cpu_budget))
+        out["cpu_baseline"] = (cpu_baseline_tokens(x, g, w, args.cpu_budget, args.estimator)
+                               if tokens else cpu_baseline(G, w, args.cpu_budget, args.estimator))
     print(json.dumps(out), flush=True)
 
 

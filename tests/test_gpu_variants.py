@@ -187,3 +187,37 @@ def test_token_means_need_tokens(gpu):
         with pytest.raises(ffe.FlipFlopError) as ei:
             ffe.FlipFlop(dev(G, gpu), estimator=est)
         assert ei.value.code == ffe.FF_ERR_INVALID_ARG
+
+
+# ---------------------------------------------------------------- full size
+
+@pytest.mark.timeout(600)
+def test_frobenius_full_size_attention_layer(gpu):
+    """4096 x 4096, N = 128, bf16, the paper's damping: the returned A is the
+    damped, trace-normalised half step (1/(N m)) sum_i G_i^T B G_i of the
+    returned B (the last update of the iteration), evaluated here in fp64;
+    and the factors are symmetric positive definite with tr(A) = n."""
+    import torch
+    import paper_2609_14706_amd as ffe
+    w = synth.workload("attn")
+    G = synth.generate_device(w, device=gpu)
+    f = ffe.FlipFlop(G, estimator="frobenius", damping=0.1)
+    ll = f.iterate(3)
+    A, B = f.factors()
+    f.close()
+    assert len(ll) == 3 and all(np.isnan(v) for v in ll)
+    assert abs(float(torch.trace(A.double())) - w.n) < 1e-3
+    assert bool((A == A.T).all()) and bool((B == B.T).all())
+    torch.linalg.cholesky(A.double())
+    torch.linalg.cholesky(B.double())
+    Bd = B.double()
+    M = torch.zeros((w.n, w.n), dtype=torch.float64, device=gpu)
+    for i in range(w.N):
+        Gi = G[i].double()
+        M += Gi.T @ (Bd @ Gi)
+    M = M / (w.N * w.m)
+    M = M + (0.1 * float(torch.trace(M)) / w.n) * torch.eye(w.n, dtype=torch.float64, device=gpu)
+    M = M * (w.n / float(torch.trace(M)))
+    err = float(torch.linalg.norm(A.double() - M) / torch.linalg.norm(M))
+    print(f"frobenius full size: last half step vs fp64 {err:.3e}", flush=True)
+    assert err < TOL_BF16
