@@ -65,6 +65,11 @@ struct Side {
   size_t partial_floats = 0;
   bool lw_valid = false;             // Lw holds the inverse factor of F[cur]
   int code = 0;                      // 1 = A, 2 = B
+  // helper stream of the factorisation (created on first use): the product
+  // X = L21 L11^-1 of a recursion node runs there while the node's second
+  // half is factorised on the main stream
+  hipStream_t helper = nullptr;
+  hipEvent_t hfork = nullptr, hjoin = nullptr;
 };
 
 struct Layout {
@@ -290,6 +295,11 @@ ff_status cholinv_rec(ff_handle_s* h, Side& s, int64_t o, int64_t sz, int iterat
                             iteration, s.code, h->st, h->stream, keepL ? blk : nullptr));
     return FF_OK;
   }
+  if (s.helper == nullptr) {
+    FF_HIP(hipStreamCreateWithFlags(&s.helper, hipStreamNonBlocking));
+    FF_HIP(hipEventCreateWithFlags(&s.hfork, hipEventDisableTiming));
+    FF_HIP(hipEventCreateWithFlags(&s.hjoin, hipEventDisableTiming));
+  }
   const int64_t nl = (sz + kLeaf - 1) / kLeaf;
   const int64_t hh = (nl + 1) / 2 * kLeaf, r = sz - hh;
   ff_status rc = cholinv_rec(h, s, o, hh, iteration, keepL);
@@ -312,29 +322,35 @@ ff_status cholinv_rec(ff_handle_s* h, Side& s, int64_t o, int64_t sz, int iterat
   g.A = Li21; g.B = Li21; g.C = L22; g.M = r; g.N = r; g.K = hh;
   g.transA = 0; g.transB = 1; g.alpha = -1.f; g.beta = 1.f; g.flags = kCLower;
   FF_HIP(launch_gemm_f32(g, 1, h->stream));
-  rc = cholinv_rec(h, s, o + hh, r, iteration, keepL);
-  if (rc != FF_OK) return rc;
+  // X = L21 Li11 needs only what is done: on the helper stream, while the
+  // second half is factorised (it writes only blocks the second half does
+  // not touch; the last product waits for it).  The join event is recorded
+  // again by the nodes below, always later on the in-order helper stream.
+  const hipStream_t xs = s.helper;
+  FF_HIP(hipEventRecord(s.hfork, h->stream));
+  FF_HIP(hipStreamWaitEvent(s.helper, s.hfork, 0));
+  float* Xt = s.L + o * d + (o + hh);  // keepL: X^T in the A12 block (above the diagonal)
   if (keepL) {
-    // X^T = (L21 Li11)^T = Li11^T L21^T into the A12 block (hh x r, above the diagonal)
-    float* Xt = s.L + o * d + (o + hh);
+    // X^T = (L21 Li11)^T = Li11^T L21^T
     g.A = Li11; g.B = Li21; g.C = Xt; g.M = hh; g.N = r; g.K = hh;
     g.transA = 1; g.transB = 1; g.alpha = 1.f; g.beta = 0.f; g.flags = kKLoRow;
-    FF_HIP(launch_gemm_f32(g, 1, h->stream));
+    FF_HIP(launch_gemm_f32(g, 1, xs));
     // L21 (parked in Li21) into its place in L
-    FF_HIP(launch_copy2d_f32(Li21, d, L21, d, r, hh, h->st, h->stream));
-    // Li21 <- -Li22 X
-    g.A = Li22; g.B = Xt; g.C = Li21; g.M = r; g.N = hh; g.K = r;
-    g.transA = 0; g.transB = 1; g.alpha = -1.f; g.beta = 0.f; g.flags = kKHiRow;
-    FF_HIP(launch_gemm_f32(g, 1, h->stream));
-    return FF_OK;
+    FF_HIP(launch_copy2d_f32(Li21, d, L21, d, r, hh, h->st, xs));
+  } else {
+    // X <- L21 Li11  (into the A21 block, no longer needed)
+    g.A = Li21; g.B = Li11; g.C = L21; g.M = r; g.N = hh; g.K = hh;
+    g.transA = 0; g.transB = 0; g.alpha = 1.f; g.beta = 0.f; g.flags = kKLoCol;
+    FF_HIP(launch_gemm_f32(g, 1, xs));
   }
-  // X <- L21 Li11  (into the A21 block, no longer needed)
-  g.A = Li21; g.B = Li11; g.C = L21; g.M = r; g.N = hh; g.K = hh;
-  g.transA = 0; g.transB = 0; g.alpha = 1.f; g.beta = 0.f; g.flags = kKLoCol;
-  FF_HIP(launch_gemm_f32(g, 1, h->stream));
+  FF_HIP(hipEventRecord(s.hjoin, s.helper));
+  rc = cholinv_rec(h, s, o + hh, r, iteration, keepL);
+  if (rc != FF_OK) return rc;
+  FF_HIP(hipStreamWaitEvent(h->stream, s.hjoin, 0));
   // Li21 <- -Li22 X
-  g.A = Li22; g.B = L21; g.C = Li21; g.M = r; g.N = hh; g.K = r;
-  g.transA = 0; g.transB = 0; g.alpha = -1.f; g.beta = 0.f; g.flags = kKHiRow;
+  g.A = Li22; g.C = Li21; g.M = r; g.N = hh; g.K = r;
+  g.B = keepL ? Xt : L21; g.transB = keepL ? 1 : 0;
+  g.transA = 0; g.alpha = -1.f; g.beta = 0.f; g.flags = kKHiRow;
   FF_HIP(launch_gemm_f32(g, 1, h->stream));
   return FF_OK;
 }
@@ -1128,6 +1144,13 @@ ff_status ff_destroy(ff_handle h) {
     hipEventDestroy(h->fork);
     hipEventDestroy(h->join);
   }
+  for (Side* sd : {&h->A, &h->B})
+    if (sd->helper != nullptr) {
+      hipStreamSynchronize(sd->helper);
+      hipStreamDestroy(sd->helper);
+      hipEventDestroy(sd->hfork);
+      hipEventDestroy(sd->hjoin);
+    }
   for (hipEvent_t e : h->events) hipEventDestroy(e);
   delete h;
   return FF_OK;
