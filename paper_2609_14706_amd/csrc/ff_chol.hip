@@ -4,10 +4,10 @@
 // B^-1 in the two half steps); the iteration whitens with the inverse of the
 // lower Cholesky factor, L^-1 (Section 2 notation: Cholesky(M) is the lower
 // L with positive diagonal and L L^T = M).  Blocks of up to 128 rows are
-// handled here by one workgroup; larger factors are assembled by the host
-// recursion from these blocks and fp32 matrix-core products.
+// handled here by one workgroup; larger factors are assembled by the host's
+// blocked factorisation from these blocks and fp32 matrix-core products.
 //
-// Inside the block the same recursion runs in LDS: for a block [[A11, .],
+// Inside the block a recursion runs in LDS: for a block [[A11, .],
 // [A21, A22]] of size s (halves h = s/2)
 //     (L11, X11) = cholinv(A11);  L21 = A21 X11^T;  A22 -= L21 L21^T;
 //     (L22, X22) = cholinv(A22);  X21 = -X22 (L21 X11)

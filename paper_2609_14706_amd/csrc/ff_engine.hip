@@ -65,11 +65,12 @@ struct Side {
   size_t partial_floats = 0;
   bool lw_valid = false;             // Lw holds the inverse factor of F[cur]
   int code = 0;                      // 1 = A, 2 = B
-  // helper stream of the factorisation (created on first use): the product
-  // X = L21 L11^-1 of a recursion node runs there while the node's second
-  // half is factorised on the main stream
+  // streams of the blocked factorisation (created on first use): the helper
+  // runs the bulk of each trailing update, istream builds the inverse
   hipStream_t helper = nullptr;
   hipEvent_t hfork = nullptr, hjoin = nullptr;
+  hipStream_t istream = nullptr;
+  hipEvent_t ev_leaf = nullptr, ev_inv = nullptr;
 };
 
 struct Layout {
@@ -284,74 +285,126 @@ void collect_timing(ff_handle_s* h) {
 }
 
 // ------------------------------------------------------- factorisation
-// keepL: leave the Cholesky factor itself in the lower triangle of s.L (the
-// recursion's scratch then goes to the unused upper blocks of s.L).
-ff_status cholinv_rec(ff_handle_s* h, Side& s, int64_t o, int64_t sz, int iteration,
-                      bool keepL = false) {
-  const int64_t d = s.dim;
-  if (sz <= kLeaf) {
-    float* blk = s.L + o * d + o;
-    FF_HIP(launch_chol_leaf(blk, s.Li + o * d + o, d, (int)sz, o, s.slots, (int)(o / kLeaf),
-                            iteration, s.code, h->st, h->stream, keepL ? blk : nullptr));
-    return FF_OK;
-  }
+ff_status side_streams(Side& s) {
   if (s.helper == nullptr) {
     FF_HIP(hipStreamCreateWithFlags(&s.helper, hipStreamNonBlocking));
     FF_HIP(hipEventCreateWithFlags(&s.hfork, hipEventDisableTiming));
     FF_HIP(hipEventCreateWithFlags(&s.hjoin, hipEventDisableTiming));
   }
+  if (s.istream == nullptr) {
+    FF_HIP(hipStreamCreateWithFlags(&s.istream, hipStreamNonBlocking));
+    FF_HIP(hipEventCreateWithFlags(&s.ev_leaf, hipEventDisableTiming));
+    FF_HIP(hipEventCreateWithFlags(&s.ev_inv, hipEventDisableTiming));
+  }
+  return FF_OK;
+}
+
+// Off-diagonal blocks of L^-1 for the node [o, o + sz) of the leaf tree, on
+// stream st: Li21 = -Li22 (L21 Li11), with (L21 Li11)^T parked in the node's
+// block above the diagonal of s.L.  The children are done before (in order
+// on the same stream).
+ff_status inverse_node(ff_handle_s* h, Side& s, int64_t o, int64_t sz, hipStream_t st) {
+  const int64_t d = s.dim;
   const int64_t nl = (sz + kLeaf - 1) / kLeaf;
   const int64_t hh = (nl + 1) / 2 * kLeaf, r = sz - hh;
-  ff_status rc = cholinv_rec(h, s, o, hh, iteration, keepL);
-  if (rc != FF_OK) return rc;
   float* L21 = s.L + (o + hh) * d + o;
-  float* L22 = s.L + (o + hh) * d + (o + hh);
   float* Li11 = s.Li + o * d + o;
   float* Li21 = s.Li + (o + hh) * d + o;
   float* Li22 = s.Li + (o + hh) * d + (o + hh);
+  float* Tt = s.L + o * d + (o + hh);
   GemmF32 g{};
   g.lda = g.ldb = g.ldc = d;
   g.kseg = INT64_MAX / 4;
   g.ksplit = 1;
   g.st = h->st;
-  // Li21 <- A21 Li11^T  (the panel of L, parked in the Li21 block)
-  g.A = L21; g.B = Li11; g.C = Li21; g.M = r; g.N = hh; g.K = hh;
-  g.transA = 0; g.transB = 1; g.alpha = 1.f; g.beta = 0.f; g.flags = kKHiCol;
-  FF_HIP(launch_gemm_f32(g, 1, h->stream));
-  // A22 <- A22 - L21 L21^T  (lower triangle)
-  g.A = Li21; g.B = Li21; g.C = L22; g.M = r; g.N = r; g.K = hh;
-  g.transA = 0; g.transB = 1; g.alpha = -1.f; g.beta = 1.f; g.flags = kCLower;
-  FF_HIP(launch_gemm_f32(g, 1, h->stream));
-  // X = L21 Li11 needs only what is done: on the helper stream, while the
-  // second half is factorised (it writes only blocks the second half does
-  // not touch; the last product waits for it).  The join event is recorded
-  // again by the nodes below, always later on the in-order helper stream.
-  const hipStream_t xs = s.helper;
-  FF_HIP(hipEventRecord(s.hfork, h->stream));
-  FF_HIP(hipStreamWaitEvent(s.helper, s.hfork, 0));
-  float* Xt = s.L + o * d + (o + hh);  // keepL: X^T in the A12 block (above the diagonal)
-  if (keepL) {
-    // X^T = (L21 Li11)^T = Li11^T L21^T
-    g.A = Li11; g.B = Li21; g.C = Xt; g.M = hh; g.N = r; g.K = hh;
-    g.transA = 1; g.transB = 1; g.alpha = 1.f; g.beta = 0.f; g.flags = kKLoRow;
-    FF_HIP(launch_gemm_f32(g, 1, xs));
-    // L21 (parked in Li21) into its place in L
-    FF_HIP(launch_copy2d_f32(Li21, d, L21, d, r, hh, h->st, xs));
-  } else {
-    // X <- L21 Li11  (into the A21 block, no longer needed)
-    g.A = Li21; g.B = Li11; g.C = L21; g.M = r; g.N = hh; g.K = hh;
-    g.transA = 0; g.transB = 0; g.alpha = 1.f; g.beta = 0.f; g.flags = kKLoCol;
-    FF_HIP(launch_gemm_f32(g, 1, xs));
-  }
-  FF_HIP(hipEventRecord(s.hjoin, s.helper));
-  rc = cholinv_rec(h, s, o + hh, r, iteration, keepL);
+  // T^T = (L21 Li11)^T = Li11^T L21^T  (hh x r)
+  g.A = Li11; g.B = L21; g.C = Tt; g.M = hh; g.N = r; g.K = hh;
+  g.transA = 1; g.transB = 1; g.alpha = 1.f; g.beta = 0.f; g.flags = kKLoRow;
+  FF_HIP(launch_gemm_f32(g, 1, st));
+  // Li21 = -Li22 T
+  g.A = Li22; g.B = Tt; g.C = Li21; g.M = r; g.N = hh; g.K = r;
+  g.transA = 0; g.transB = 1; g.alpha = -1.f; g.beta = 0.f; g.flags = kKHiRow;
+  FF_HIP(launch_gemm_f32(g, 1, st));
+  return FF_OK;
+}
+
+// Enqueue, in post order, the inverse of every node of [o, o + sz) whose last
+// leaf is leaf `last` (children first).
+ff_status inverse_nodes_ending(ff_handle_s* h, Side& s, int64_t o, int64_t sz, int64_t last,
+                               hipStream_t st) {
+  if (sz <= kLeaf) return FF_OK;
+  const int64_t nl = (sz + kLeaf - 1) / kLeaf;
+  const int64_t hh = (nl + 1) / 2 * kLeaf;
+  const int64_t end_leaf = (o + sz - 1) / kLeaf;
+  ff_status rc;
+  if (last < (o + hh) / kLeaf) return inverse_nodes_ending(h, s, o, hh, last, st);
+  if ((rc = inverse_nodes_ending(h, s, o + hh, sz - hh, last, st)) != FF_OK) return rc;
+  if (end_leaf == last) return inverse_node(h, s, o, sz, st);
+  return FF_OK;
+}
+
+// Cholesky factor L (lower, in place in s.L) and its inverse (s.Li) of the
+// matrix in s.L: right-looking over 128-column panels.  Main stream, per
+// panel k: the leaf (L_kk and its inverse), the panel L_ik = A_ik L_kk^-T
+// (in place), the update of the next column block; the rest of the trailing
+// update runs on the helper stream, overlapping the next leaf; the
+// off-diagonal blocks of L^-1 are built on a third stream, each node of the
+// binary tree of leaves as soon as its last leaf is done.  The upper
+// triangle of s.L is scratch.
+ff_status chol_blocked(ff_handle_s* h, Side& s, int iteration) {
+  ff_status rc = side_streams(s);
   if (rc != FF_OK) return rc;
-  FF_HIP(hipStreamWaitEvent(h->stream, s.hjoin, 0));
-  // Li21 <- -Li22 X
-  g.A = Li22; g.C = Li21; g.M = r; g.N = hh; g.K = r;
-  g.B = keepL ? Xt : L21; g.transB = keepL ? 1 : 0;
-  g.transA = 0; g.alpha = -1.f; g.beta = 0.f; g.flags = kKHiRow;
-  FF_HIP(launch_gemm_f32(g, 1, h->stream));
+  const int64_t d = s.dim;
+  const int64_t nb = (d + kLeaf - 1) / kLeaf;
+  hipStream_t ms = h->stream;
+  GemmF32 g{};
+  g.lda = g.ldb = g.ldc = d;
+  g.kseg = INT64_MAX / 4;
+  g.ksplit = 1;
+  g.st = h->st;
+  // the inverse stream starts after the work already on the main stream
+  FF_HIP(hipEventRecord(s.ev_leaf, ms));
+  FF_HIP(hipStreamWaitEvent(s.istream, s.ev_leaf, 0));
+  FF_HIP(hipStreamWaitEvent(s.helper, s.ev_leaf, 0));
+  for (int64_t k = 0; k < nb; ++k) {
+    const int64_t o = k * kLeaf, bk = std::min<int64_t>(kLeaf, d - o), rest = d - o - bk;
+    float* Akk = s.L + o * d + o;
+    FF_HIP(launch_chol_leaf(Akk, s.Li + o * d + o, d, (int)bk, o, s.slots, (int)k, iteration,
+                            s.code, h->st, ms, Akk));
+    FF_HIP(hipEventRecord(s.ev_leaf, ms));
+    FF_HIP(hipStreamWaitEvent(s.istream, s.ev_leaf, 0));
+    if ((rc = inverse_nodes_ending(h, s, 0, d, k, s.istream)) != FF_OK) return rc;
+    if (rest == 0) break;
+    // the panel L_ik = A_ik Li_kk^T, in place (128-row tiles: each workgroup
+    // reads its rows before it writes them)
+    float* Pk = s.L + (o + bk) * d + o;
+    g.A = Pk; g.B = s.Li + o * d + o; g.C = Pk; g.M = rest; g.N = bk; g.K = bk;
+    g.transA = 0; g.transB = 1; g.alpha = 1.f; g.beta = 0.f; g.flags = kKHiCol; g.tile = 128;
+    FF_HIP(launch_gemm_f32(g, 1, ms));
+    g.tile = 0;
+    const int64_t b1 = std::min<int64_t>(kLeaf, rest);
+    // the next column block now (after the helper's update of it from panel k - 1),
+    // before the helper is released, so that it runs alone
+    if (k > 0) FF_HIP(hipStreamWaitEvent(ms, s.hjoin, 0));
+    g.A = Pk; g.B = Pk; g.C = s.L + (o + bk) * d + (o + bk); g.M = rest; g.N = b1; g.K = bk;
+    g.transA = 0; g.transB = 1; g.alpha = -1.f; g.beta = 1.f; g.flags = kCLower;
+    FF_HIP(launch_gemm_f32(g, 1, ms));
+    // rest of the trailing update on the helper: columns beyond the next block
+    if (rest > b1) {
+      FF_HIP(hipEventRecord(s.hfork, ms));
+      FF_HIP(hipStreamWaitEvent(s.helper, s.hfork, 0));
+    }
+    if (rest > b1) {
+      const int64_t q = o + bk + b1;
+      g.A = Pk + b1 * d; g.B = Pk + b1 * d; g.C = s.L + q * d + q;
+      g.M = rest - b1; g.N = rest - b1; g.K = bk;
+      g.transA = 0; g.transB = 1; g.alpha = -1.f; g.beta = 1.f; g.flags = kCLower;
+      FF_HIP(launch_gemm_f32(g, 1, s.helper));
+      FF_HIP(hipEventRecord(s.hjoin, s.helper));
+    }
+  }
+  FF_HIP(hipEventRecord(s.ev_inv, s.istream));
+  FF_HIP(hipStreamWaitEvent(ms, s.ev_inv, 0));
   return FF_OK;
 }
 
@@ -360,7 +413,7 @@ ff_status cholinv_rec(ff_handle_s* h, Side& s, int64_t o, int64_t sz, int iterat
 ff_status cholinv_from(ff_handle_s* h, Side& s, const float* src, int iteration) {
   Timed t(h, 3, (double)s.dim * s.dim * s.dim / 3.0);
   FF_HIP(launch_copy_f32(src, s.L, s.dim * s.dim, h->st, h->stream));
-  ff_status rc = cholinv_rec(h, s, 0, s.dim, iteration);
+  ff_status rc = chol_blocked(h, s, iteration);
   if (rc != FF_OK) return rc;
   FF_HIP(launch_convert_inverse(s.Li, s.dim, s.Lw, s.Lw2, s.dim_p, h->elem, h->st, h->stream));
   return FF_OK;
@@ -377,7 +430,7 @@ ff_status cholinv(ff_handle_s* h, Side& s, int slot, int iteration) {
 ff_status revchol_operand(ff_handle_s* h, Side& s, const float* src, int iteration) {
   Timed t(h, 3, (double)s.dim * s.dim * s.dim / 3.0);
   FF_HIP(launch_wk_reverse(src, s.dim, s.L, h->st, h->stream));
-  ff_status rc = cholinv_rec(h, s, 0, s.dim, iteration, true);
+  ff_status rc = chol_blocked(h, s, iteration);
   if (rc != FF_OK) return rc;
   FF_HIP(launch_rev_transpose(s.L, s.dim, s.Li, h->st, h->stream));
   FF_HIP(launch_convert_inverse(s.Li, s.dim, s.Lw, s.Lw2, s.dim_p, h->elem, h->st, h->stream));
@@ -681,7 +734,7 @@ ff_status quant_side(ff_handle_s* h, Side& s, const float* M, int64_t dq, float*
   FF_HIP(launch_wk_reverse(M, s.dim, s.L, h->st, h->stream));
   {
     Timed t(h, 3, (double)s.dim * s.dim * s.dim / 3.0);
-    ff_status rc = cholinv_rec(h, s, 0, s.dim, -1);
+    ff_status rc = chol_blocked(h, s, -1);
     if (rc != FF_OK) return rc;
   }
   FF_HIP(launch_wk_normalise(s.Li, s.dim, dq, Lt, diag, h->st, h->stream));
@@ -1144,13 +1197,20 @@ ff_status ff_destroy(ff_handle h) {
     hipEventDestroy(h->fork);
     hipEventDestroy(h->join);
   }
-  for (Side* sd : {&h->A, &h->B})
+  for (Side* sd : {&h->A, &h->B}) {
     if (sd->helper != nullptr) {
       hipStreamSynchronize(sd->helper);
       hipStreamDestroy(sd->helper);
       hipEventDestroy(sd->hfork);
       hipEventDestroy(sd->hjoin);
     }
+    if (sd->istream != nullptr) {
+      hipStreamSynchronize(sd->istream);
+      hipStreamDestroy(sd->istream);
+      hipEventDestroy(sd->ev_leaf);
+      hipEventDestroy(sd->ev_inv);
+    }
+  }
   for (hipEvent_t e : h->events) hipEventDestroy(e);
   delete h;
   return FF_OK;

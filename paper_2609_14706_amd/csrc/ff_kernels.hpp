@@ -65,6 +65,8 @@ struct GemmF32 {
   int64_t segA, segB;
   int ksplit;          // > 1: grid z splits k, C += z * sC, beta ignored
   const int* st;
+  int tile;            // 0: chosen by size; 128: 128 x 128 tiles (a workgroup reads all of
+                       // its rows of op(A) before it writes, so C may alias A when N <= 128)
 };
 // C = alpha * op(A) op(B) + beta * C on the fp32 matrix cores (64 x 64 tiles).
 hipError_t launch_gemm_f32(const GemmF32& p, int batch, hipStream_t s);
