@@ -31,10 +31,11 @@ constexpr int BS = 32;      // base block
 constexpr int SP = NB + 1;  // LDS row pitch (conflict-free column reads)
 
 struct LeafLDS {
+  float C[BS][BS];  // column j of the base block's L at pivot step j (first, so
+                    // its addresses fit the LDS instructions' immediate offset)
   float S[NB][SP];  // A, overwritten by L (lower triangle)
   float X[NB][SP];  // L^-1
   float T[64][65];  // product scratch
-  float C[BS][BS];  // column j of the base block's L at pivot step j
   double ldp[NB / BS];
   int bad;
 };
