@@ -118,6 +118,37 @@ __device__ __forceinline__ void mfma_slot(const Frags& f, f32x16 (&acc)[4][4]) {
                        : __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[kk][i], f[kk][4 + j], acc[i][j], 0, 0, 0);
 }
 
+// Single pieces of a step, for the explicitly interleaved steady state:
+// product m (k half m / 16, tile pair ((m / 4) % 4, m % 4)), fragment read q
+// (k half q / 8; A tiles for q % 8 < 4, B tiles above) and copy q (operand
+// q % 2, chunk group q / 2) of one stage.
+template <bool SW>
+__device__ __forceinline__ void mfma_one(const Frags& f, f32x16 (&acc)[4][4], int m) {
+  const int kk = m >> 4, i = (m >> 2) & 3, j = m & 3;
+  acc[i][j] = SW ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[kk][4 + j], f[kk][i], acc[i][j], 0, 0, 0)
+                 : __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[kk][i], f[kk][4 + j], acc[i][j], 0, 0, 0);
+}
+
+__device__ __forceinline__ void read_frag_one(const Ring& sm, int buf, int wave, int lane, Frags& f,
+                                              int q) {
+  const int kk = q >> 3, t = q & 7;
+  const int c = kk * 2 + (lane >> 5);
+  const int row = (t < 4 ? (wave >> 1) : (wave & 1)) * 128 + (t & 3) * 32 + (lane & 31);
+  f[kk][t] = __builtin_bit_cast(bf16x8, t < 4 ? sm.a[buf][chunk_pos(row, c)] : sm.b[buf][chunk_pos(row, c)]);
+}
+
+__device__ __forceinline__ void issue_one(Ring& sm, int buf, const bf16_t* pa, const bf16_t* pb,
+                                          const uint32_t (&oa)[4], const uint32_t (&ob)[4], int wave,
+                                          int q) {
+  const int g = q >> 1;
+  if (q & 1)
+    __builtin_amdgcn_global_load_lds((const void*)(pb + ob[g]), (lds_void*)&sm.b[buf][(g * 4 + wave) * 64],
+                                     16, 0, 0);
+  else
+    __builtin_amdgcn_global_load_lds((const void*)(pa + oa[g]), (lds_void*)&sm.a[buf][(g * 4 + wave) * 64],
+                                     16, 0, 0);
+}
+
 // Slices requested but not yet known to have landed may number at most
 // `pending` (0..4) when this returns (eight copies per slice and lane).
 __device__ __forceinline__ void wait_pending(int pending) {
@@ -132,26 +163,46 @@ __device__ __forceinline__ void wait_pending(int pending) {
 // its fragments: wait for slice i + 1, barrier (every wave has slice i in
 // registers, so its slot is free), request slice i + 5 into that slot, then
 // read slice i + 1 into the other register set interleaved with the 32
-// products of slice i.
-template <bool SW, int CUR, class Addr>
+// products of slice i.  STEADY steps (i + 5 < n, so slice i + 5 exists and
+// exactly three slices besides i + 1 are in flight) are branch-free, and
+// their eight copies are spread over the first half of the products instead
+// of being issued in one burst behind the barrier, where they would hold up
+// the first product while the four waves' copies queue at the address unit.
+template <bool SW, int CUR, bool STEADY, class Addr>
 __device__ __forceinline__ void loop_step(Ring& sm, int i, int n, int kt0, const Addr& addr,
                                           const uint32_t (&oa)[4], const uint32_t (&ob)[4],
                                           int wave, int lane, Frags (&F)[2],
                                           f32x16 (&acc)[4][4]) {
-  wait_pending(min(n, i + NSTAGE) - (i + 2));
+  if constexpr (STEADY) wait_vmem<(NSTAGE - 2) * 8>();
+  else wait_pending(min(n, i + NSTAGE) - (i + 2));
   wait_lds();  // this wave's reads of slice i (issued one step ago) are complete
   __builtin_amdgcn_s_barrier();
-  if (i + NSTAGE < n) {
+  if constexpr (STEADY) {
     const bf16_t *pa, *pb;
     addr(kt0 + i + NSTAGE, pa, pb);
-    issue_stage(sm, (i + NSTAGE) % NSTAGE, pa, pb, oa, ob, wave);
-  }
-  read_frags(sm, (i + 1) % NSTAGE, wave, lane, F[CUR ^ 1]);
-  mfma_slot<SW>(F[CUR], acc);
+    const int wbuf = (i + NSTAGE) % NSTAGE, rbuf = (i + 1) % NSTAGE;
+    // in program order, fenced: product, LDS read, product, copy (first half)
 #pragma unroll
-  for (int q = 0; q < 16; ++q) {
-    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
-    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // two matrix-core products
+    for (int q = 0; q < 16; ++q) {
+      mfma_one<SW>(F[CUR], acc, 2 * q);
+      read_frag_one(sm, rbuf, wave, lane, F[CUR ^ 1], q);
+      mfma_one<SW>(F[CUR], acc, 2 * q + 1);
+      if (q < 8) issue_one(sm, wbuf, pa, pb, oa, ob, wave, q);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  } else {
+    if (i + NSTAGE < n) {
+      const bf16_t *pa, *pb;
+      addr(kt0 + i + NSTAGE, pa, pb);
+      issue_stage(sm, (i + NSTAGE) % NSTAGE, pa, pb, oa, ob, wave);
+    }
+    read_frags(sm, (i + 1) % NSTAGE, wave, lane, F[CUR ^ 1]);
+    mfma_slot<SW>(F[CUR], acc);
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // two matrix-core products
+    }
   }
 }
 
@@ -179,12 +230,16 @@ __device__ __forceinline__ void mainloop(Ring& sm, int kt0, int kt1, uint32_t ld
   Frags F[2];
   read_frags(sm, 0, wave, lane, F[0]);
   int i = 0;
+  for (; i + NSTAGE + 1 < n; i += 2) {  // both steps of the pair request a slice
+    loop_step<SW, 0, true>(sm, i, n, kt0, addr, oa, ob, wave, lane, F, acc);
+    loop_step<SW, 1, true>(sm, i + 1, n, kt0, addr, oa, ob, wave, lane, F, acc);
+  }
   for (; i + 2 < n; i += 2) {
-    loop_step<SW, 0>(sm, i, n, kt0, addr, oa, ob, wave, lane, F, acc);
-    loop_step<SW, 1>(sm, i + 1, n, kt0, addr, oa, ob, wave, lane, F, acc);
+    loop_step<SW, 0, false>(sm, i, n, kt0, addr, oa, ob, wave, lane, F, acc);
+    loop_step<SW, 1, false>(sm, i + 1, n, kt0, addr, oa, ob, wave, lane, F, acc);
   }
   if (n - i == 2) {
-    loop_step<SW, 0>(sm, i, n, kt0, addr, oa, ob, wave, lane, F, acc);
+    loop_step<SW, 0, false>(sm, i, n, kt0, addr, oa, ob, wave, lane, F, acc);
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
