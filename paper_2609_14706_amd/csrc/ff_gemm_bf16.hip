@@ -181,13 +181,17 @@ __device__ __forceinline__ void loop_step(Ring& sm, int i, int n, int kt0, const
     const bf16_t *pa, *pb;
     addr(kt0 + i + NSTAGE, pa, pb);
     const int wbuf = (i + NSTAGE) % NSTAGE, rbuf = (i + 1) % NSTAGE;
-    // in program order, fenced: product, LDS read, product, copy (first half)
+    // products in program order, fenced; the 16 LDS reads of the next slice
+    // follow products 0, 1, 3, 4, ..., 22 (read q after product 3q/2), so
+    // the last one has nine products to land before the next step's wait,
+    // and the eight copies follow products 2, 5, ..., 23
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      mfma_one<SW>(F[CUR], acc, 2 * q);
-      read_frag_one(sm, rbuf, wave, lane, F[CUR ^ 1], q);
-      mfma_one<SW>(F[CUR], acc, 2 * q + 1);
-      if (q < 8) issue_one(sm, wbuf, pa, pb, oa, ob, wave, q);
+    for (int m = 0; m < 32; ++m) {
+      mfma_one<SW>(F[CUR], acc, m);
+      if (m < 24) {
+        if (m % 3 == 2) issue_one(sm, wbuf, pa, pb, oa, ob, wave, m / 3);
+        else read_frag_one(sm, rbuf, wave, lane, F[CUR ^ 1], (2 * m + (m % 3)) / 3);
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
   } else {
@@ -258,37 +262,41 @@ __device__ __forceinline__ void zero_acc(f32x16 (&acc)[4][4]) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 }
 
-__global__ __launch_bounds__(NTHR, 1) void k_whiten_bf16(const bf16_t* __restrict__ X,
-                                                         const bf16_t* __restrict__ Y,
-                                                         const bf16_t* __restrict__ Y2,
-                                                         bf16_t* __restrict__ C, uint32_t Kp,
-                                                         const int* st) {
-  if (ff_halted(st)) return;
-  __shared__ Ring sm;
-  const uint32_t ncol = Kp / TM;
-  const uint32_t t = xcd_remap(blockIdx.x, gridDim.x);
-  const uint32_t rb = t / ncol;
-  const uint32_t cj = ncol - 1 - t % ncol;  // heaviest column tiles first
+// Tiles of the whitening products.  Output tile (rb, cj) needs k in
+// [0, 256 (cj + 1)) (Y is lower triangular), so tile lengths range from 8 to
+// 8 ncol slices.  One workgroup takes the pair cj = c and cj = ncol - 1 - c
+// of one row block: c with k ascending, then its partner with k descending.
+// Every workgroup then runs 8 (ncol + 1) slices, and at slice step t of the
+// workgroup all pairs of a row block sit at k slice t or 8 (ncol + 1) - 1 - t,
+// so the workgroups that run together on an XCD (consecutive pairs of a few
+// row blocks) stay in step and share their operand slices in its L2.
+template <bool SW, bool REV>
+__device__ __forceinline__ void whiten_tile(Ring& sm, const bf16_t* xa, const bf16_t* Y, const bf16_t* Y2,
+                                            uint32_t cj, uint32_t Kp, f32x16 (&acc)[4][4]) {
   const int kt1 = (int)((cj + 1) * (TM / TK));
-  const bf16_t* xa = X + (size_t)rb * TM * Kp;
-  f32x16 acc[4][4];
   zero_acc(acc);
   {
     const bf16_t* yb = Y + (size_t)cj * TM * Kp;
     auto addr = [&](int kt, const bf16_t*& pa, const bf16_t*& pb) {
-      pa = xa + kt * TK;
-      pb = yb + kt * TK;
+      const int k = REV ? kt1 - 1 - kt : kt;
+      pa = xa + k * TK;
+      pb = yb + k * TK;
     };
-    mainloop(sm, 0, kt1, Kp, Kp, addr, acc);
+    mainloop<SW>(sm, 0, kt1, Kp, Kp, addr, acc);
   }
   if (Y2 != nullptr) {
     const bf16_t* yb = Y2 + (size_t)cj * TM * Kp;
     auto addr = [&](int kt, const bf16_t*& pa, const bf16_t*& pb) {
-      pa = xa + kt * TK;
-      pb = yb + kt * TK;
+      const int k = REV ? kt1 - 1 - kt : kt;
+      pa = xa + k * TK;
+      pb = yb + k * TK;
     };
-    mainloop(sm, 0, kt1, Kp, Kp, addr, acc);
+    mainloop<SW>(sm, 0, kt1, Kp, Kp, addr, acc);
   }
+}
+
+__device__ __forceinline__ void store_whitened(const f32x16 (&acc)[4][4], bf16_t* C, uint32_t rb,
+                                               uint32_t cj, uint32_t Kp) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
   bf16_t* cb = C + (size_t)rb * TM * Kp + (size_t)cj * TM;
@@ -304,43 +312,34 @@ __global__ __launch_bounds__(NTHR, 1) void k_whiten_bf16(const bf16_t* __restric
       }
 }
 
-// Row norms of the whitened rows, for the rank-one (per-token) form of the
-// updates (Section 5: the weight of token t in one half step is x_t^T A^-1 x_t
-// = ||L^-1 x_t||^2).  Same tiles and k ranges as k_whiten_bf16, with the
-// operands swapped so that every lane holds values of one row; the whitened
-// values are never stored.  part[row][2 cj + wn] receives the sum of squares
-// over the 128 columns of wave column wn of tile column cj.
-__global__ __launch_bounds__(NTHR, 1) void k_whiten_norm_bf16(const bf16_t* __restrict__ X,
-                                                              const bf16_t* __restrict__ Y,
-                                                              const bf16_t* __restrict__ Y2,
-                                                              float* __restrict__ part, uint32_t Kp,
-                                                              const int* st) {
+__global__ __launch_bounds__(NTHR, 1) void k_whiten_bf16(const bf16_t* __restrict__ X,
+                                                         const bf16_t* __restrict__ Y,
+                                                         const bf16_t* __restrict__ Y2,
+                                                         bf16_t* __restrict__ C, uint32_t Kp,
+                                                         const int* st) {
   if (ff_halted(st)) return;
   __shared__ Ring sm;
-  const uint32_t ncol = Kp / TM;
+  const uint32_t ncol = Kp / TM, npair = (ncol + 1) / 2;
   const uint32_t t = xcd_remap(blockIdx.x, gridDim.x);
-  const uint32_t rb = t / ncol;
-  const uint32_t cj = ncol - 1 - t % ncol;
-  const int kt1 = (int)((cj + 1) * (TM / TK));
+  const uint32_t rb = t / npair, c = t % npair;
   const bf16_t* xa = X + (size_t)rb * TM * Kp;
   f32x16 acc[4][4];
-  zero_acc(acc);
-  {
-    const bf16_t* yb = Y + (size_t)cj * TM * Kp;
-    auto addr = [&](int kt, const bf16_t*& pa, const bf16_t*& pb) {
-      pa = xa + kt * TK;
-      pb = yb + kt * TK;
-    };
-    mainloop<true>(sm, 0, kt1, Kp, Kp, addr, acc);
+  whiten_tile<false, false>(sm, xa, Y, Y2, c, Kp, acc);
+  store_whitened(acc, C, rb, c, Kp);
+  if (ncol - 1 - c != c) {
+    whiten_tile<false, true>(sm, xa, Y, Y2, ncol - 1 - c, Kp, acc);
+    store_whitened(acc, C, rb, ncol - 1 - c, Kp);
   }
-  if (Y2 != nullptr) {
-    const bf16_t* yb = Y2 + (size_t)cj * TM * Kp;
-    auto addr = [&](int kt, const bf16_t*& pa, const bf16_t*& pb) {
-      pa = xa + kt * TK;
-      pb = yb + kt * TK;
-    };
-    mainloop<true>(sm, 0, kt1, Kp, Kp, addr, acc);
-  }
+}
+
+// Row norms of the whitened rows, for the rank-one (per-token) form of the
+// updates (Section 5: the weight of token t in one half step is x_t^T A^-1 x_t
+// = ||L^-1 x_t||^2).  Same tiles, pairs and k ranges as k_whiten_bf16, with
+// the operands swapped so that every lane holds values of one row; the
+// whitened values are never stored.  part[row][2 cj + wn] receives the sum of
+// squares over the 128 columns of wave column wn of tile column cj.
+__device__ __forceinline__ void store_norms(const f32x16 (&acc)[4][4], float* part, uint32_t rb,
+                                            uint32_t cj, uint32_t ncol) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
   const uint32_t npart = 2 * ncol;
@@ -356,6 +355,26 @@ __global__ __launch_bounds__(NTHR, 1) void k_whiten_norm_bf16(const bf16_t* __re
       const size_t row = (size_t)rb * TM + wm * 128 + i * 32 + lane;
       part[row * npart + 2 * cj + wn] = s;
     }
+  }
+}
+
+__global__ __launch_bounds__(NTHR, 1) void k_whiten_norm_bf16(const bf16_t* __restrict__ X,
+                                                              const bf16_t* __restrict__ Y,
+                                                              const bf16_t* __restrict__ Y2,
+                                                              float* __restrict__ part, uint32_t Kp,
+                                                              const int* st) {
+  if (ff_halted(st)) return;
+  __shared__ Ring sm;
+  const uint32_t ncol = Kp / TM, npair = (ncol + 1) / 2;
+  const uint32_t t = xcd_remap(blockIdx.x, gridDim.x);
+  const uint32_t rb = t / npair, c = t % npair;
+  const bf16_t* xa = X + (size_t)rb * TM * Kp;
+  f32x16 acc[4][4];
+  whiten_tile<true, false>(sm, xa, Y, Y2, c, Kp, acc);
+  store_norms(acc, part, rb, c, ncol);
+  if (ncol - 1 - c != c) {
+    whiten_tile<true, true>(sm, xa, Y, Y2, ncol - 1 - c, Kp, acc);
+    store_norms(acc, part, rb, ncol - 1 - c, ncol);
   }
 }
 
@@ -444,7 +463,7 @@ __global__ __launch_bounds__(256) void k_reduce_frag(const float* __restrict__ P
 hipError_t launch_whiten_bf16(const bf16_t* X, const bf16_t* Y, const bf16_t* Y2, bf16_t* C,
                               int64_t rows, int64_t Kp, const int* st, hipStream_t s) {
   if (rows <= 0 || Kp <= 0 || rows % TM || Kp % TM || Kp > (1 << 20)) return hipErrorInvalidValue;
-  const int64_t tiles = (rows / TM) * (Kp / TM);
+  const int64_t tiles = (rows / TM) * ((Kp / TM + 1) / 2);  // one workgroup per tile pair
   if (tiles > 0x7fffffff) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_whiten_bf16, dim3((uint32_t)tiles), dim3(NTHR), 0, s, X, Y, Y2, C,
                      (uint32_t)Kp, st);
@@ -454,7 +473,7 @@ hipError_t launch_whiten_bf16(const bf16_t* X, const bf16_t* Y, const bf16_t* Y2
 hipError_t launch_whiten_norm_bf16(const bf16_t* X, const bf16_t* Y, const bf16_t* Y2, float* part,
                                    int64_t rows, int64_t Kp, const int* st, hipStream_t s) {
   if (rows <= 0 || Kp <= 0 || rows % TM || Kp % TM || Kp > (1 << 20)) return hipErrorInvalidValue;
-  const int64_t tiles = (rows / TM) * (Kp / TM);
+  const int64_t tiles = (rows / TM) * ((Kp / TM + 1) / 2);  // one workgroup per tile pair
   if (tiles > 0x7fffffff) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_whiten_norm_bf16, dim3((uint32_t)tiles), dim3(NTHR), 0, s, X, Y, Y2, part,
                      (uint32_t)Kp, st);
