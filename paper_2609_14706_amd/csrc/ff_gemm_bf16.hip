@@ -13,11 +13,12 @@
 //    deterministic partial sums that a second kernel adds in fixed order.
 //
 // Operands move global -> LDS with the direct-to-LDS loads of gfx950
-// (global_load_lds_dwordx4, no register staging) in 32-wide k slices through
-// a 5-slot ring (160 KB), four slices in flight ahead of the matrix cores, which
-// covers the memory latency with one workgroup of four waves per CU.  The
-// 16-byte chunks of each 64-byte row are XOR-swizzled so that fragment
-// reads of consecutive rows hit distinct banks.
+// (global_load_lds_dwordx4, no register staging) in 64-wide k pairs, so that
+// every copy request is a whole 128-byte line (half-line requests cost about
+// 15% of the symmetric product's time in L2 traffic), through two pair slots
+// (128 KB), one pair in flight ahead of the matrix cores.  The 16-byte chunks
+// of each 128-byte row are XOR-swizzled so that fragment reads of
+// consecutive rows hit distinct banks.
 #include "ff_common.hpp"
 #include "ff_kernels.hpp"
 
@@ -25,29 +26,31 @@ namespace ff {
 namespace {
 
 constexpr int TM = 256;       // tile rows (and columns)
-constexpr int TK = 32;        // k per LDS stage
-constexpr int NSTAGE = 5;     // LDS ring depth (four slices in flight, 160 KB)
+constexpr int TK = 32;        // k per matrix-core step (two 16-wide products)
+constexpr int PK = 64;        // k per copied pair of steps: 128-byte row segments
+constexpr int NPAIR = 2;      // LDS pair slots (128 KB)
 constexpr int NTHR = 256;     // four waves
 constexpr int TILE_FLOATS = TM * TM;
-constexpr int CHUNKS = TM * TK / 8;  // 16-byte chunks per operand per stage (1024)
+constexpr int PCH = TM * PK / 8;  // 16-byte chunks per operand per pair (2048)
 
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 typedef __attribute__((address_space(3))) void lds_void;
 
-// Stage layout: chunk position P = 4 row + slot; slot s of row r holds the
-// 16-byte k chunk c = s ^ swz(r).  A fragment read moves one chunk of each
-// of 32 consecutive rows; the LDS serves it 16 lanes (16 rows, 256 bytes) at
-// a time across its 64 banks, so the 16 chunks must cover all 16 positions
-// modulo 16, i.e. (r mod 4, slot) must differ across 16 consecutive rows.
-// swz(r) = ((r >> 1) & 3) ^ ((r >> 3) & 1) gives that, and also keeps any 8
-// consecutive rows on distinct 128-byte bank groups.
+// Pair layout: each operand row holds the 8 chunks (16 bytes, 8 k) of a 64-k
+// pair, chunk c at position 8 row + (c ^ swz(row)).  A fragment read moves
+// one chunk of each of 32 consecutive rows; the LDS serves it 16 lanes (16
+// rows, 256 bytes) at a time across its 64 four-byte banks.  With 128-byte
+// rows, position p of row r starts at bank 32 (r & 1) + 4 p, so the read is
+// conflict-free when its 16 rows cover all 16 pairs (r & 1, p); swz(row) =
+// (row >> 1) & 7 gives that.  A copy instruction fills 1 KB of consecutive
+// positions, i.e. eight whole rows: eight complete 128-byte lines.
 struct __align__(16) Ring {
-  u32x4 a[NSTAGE][CHUNKS];
-  u32x4 b[NSTAGE][CHUNKS];
+  u32x4 a[NPAIR][PCH];
+  u32x4 b[NPAIR][PCH];
 };
 
-__device__ __forceinline__ int swz(int row) { return ((row >> 1) & 3) ^ ((row >> 3) & 1); }
-__device__ __forceinline__ int chunk_pos(int row, int c) { return row * 4 + (c ^ swz(row)); }
+__device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
+__device__ __forceinline__ int chunk_pos(int row, int c) { return row * 8 + (c ^ swz(row)); }
 
 // vmcnt(N) with the other counters left alone (gfx9 encoding).
 template <int N>
@@ -58,70 +61,56 @@ __device__ __forceinline__ void wait_vmem() {
 // lgkmcnt(0) with the other counters left alone.
 __device__ __forceinline__ void wait_lds() { __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4)); }
 
-// Per-lane element offsets of the four chunks this lane moves per operand and
-// stage: instruction q of wave w fills positions (4 q + w) 64 + lane.
-__device__ __forceinline__ void chunk_offsets(int wave, int lane, uint32_t ld, uint32_t (&off)[4]) {
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int P = (q * 4 + wave) * 64 + lane;
-    const int row = P >> 2, slot = P & 3;
-    const int c = slot ^ swz(row);
-    off[q] = (uint32_t)row * ld + (uint32_t)c * 8u;
-  }
+// Element offset of the chunk this lane copies with instruction 0 of a pair;
+// instruction q (0..7) of wave w fills positions (4 q + w) 64 + lane, which
+// lie 32 q rows further down with the same swizzle, so its offset is
+// off + 32 q ld.
+__device__ __forceinline__ uint32_t chunk_offset(int wave, int lane, uint32_t ld) {
+  const int P = wave * 64 + lane;
+  const int row = P >> 3, c = (P & 7) ^ swz(row);
+  return (uint32_t)row * ld + (uint32_t)c * 8u;
 }
 
-// Asynchronous global -> LDS copy of one k slice of both operands.
-__device__ __forceinline__ void issue_stage(Ring& sm, int buf, const bf16_t* pa, const bf16_t* pb,
-                                            const uint32_t (&oa)[4], const uint32_t (&ob)[4],
-                                            int wave) {
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    __builtin_amdgcn_global_load_lds((const void*)(pa + oa[q]),
-                                     (lds_void*)&sm.a[buf][(q * 4 + wave) * 64], 16, 0, 0);
-    __builtin_amdgcn_global_load_lds((const void*)(pb + ob[q]),
-                                     (lds_void*)&sm.b[buf][(q * 4 + wave) * 64], 16, 0, 0);
-  }
+// Copy q (0..15) of a pair: operand q % 2, instruction q / 2.
+__device__ __forceinline__ void issue_one(Ring& sm, int slot, const bf16_t* pa, const bf16_t* pb,
+                                          uint32_t oa, uint32_t ob, uint32_t lda, uint32_t ldb,
+                                          int wave, int q) {
+  const int g = q >> 1;
+  if (q & 1)
+    __builtin_amdgcn_global_load_lds((const void*)(pb + ob + (size_t)g * 32 * ldb),
+                                     (lds_void*)&sm.b[slot][(g * 4 + wave) * 64], 16, 0, 0);
+  else
+    __builtin_amdgcn_global_load_lds((const void*)(pa + oa + (size_t)g * 32 * lda),
+                                     (lds_void*)&sm.a[slot][(g * 4 + wave) * 64], 16, 0, 0);
 }
 
-// Matrix-core fragments of one LDS slot: for each of the two 16-wide k
-// steps, the rows (A side) and columns (B side) of this wave's 128 x 128
+__device__ __forceinline__ void issue_pair(Ring& sm, int slot, const bf16_t* pa, const bf16_t* pb,
+                                           uint32_t oa, uint32_t ob, uint32_t lda, uint32_t ldb,
+                                           int wave) {
+#pragma unroll
+  for (int q = 0; q < 16; ++q) issue_one(sm, slot, pa, pb, oa, ob, lda, ldb, wave, q);
+}
+
+// Matrix-core fragments of one 32-k step: for each of its two 16-wide k
+// halves, the rows (A side) and columns (B side) of this wave's 128 x 128
 // quadrant, 8 consecutive k per lane.  f[kk][0..3] = A, f[kk][4..7] = B.
 typedef bf16x8 Frags[2][8];
 
-__device__ __forceinline__ void read_frags(const Ring& sm, int buf, int wave, int lane, Frags& f) {
-  const int wm = wave >> 1, wn = wave & 1;
-  const int lrow = lane & 31;
-#pragma unroll
-  for (int kk = 0; kk < 2; ++kk) {
-    const int c = kk * 2 + (lane >> 5);
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      f[kk][t] = __builtin_bit_cast(bf16x8, sm.a[buf][chunk_pos(wm * 128 + t * 32 + lrow, c)]);
-      f[kk][4 + t] = __builtin_bit_cast(bf16x8, sm.b[buf][chunk_pos(wn * 128 + t * 32 + lrow, c)]);
-    }
-  }
+// Fragment read q (0..15) of step `half` (0, 1) of the pair in `slot`:
+// k half q / 8, A tiles for q % 8 < 4, B tiles above.
+__device__ __forceinline__ void read_frag_one(const Ring& sm, int slot, int half, int wave, int lane,
+                                              Frags& f, int q) {
+  const int kk = q >> 3, t = q & 7;
+  const int c = half * 4 + kk * 2 + (lane >> 5);
+  const int row = (t < 4 ? (wave >> 1) : (wave & 1)) * 128 + (t & 3) * 32 + (lane & 31);
+  f[kk][t] = __builtin_bit_cast(bf16x8, t < 4 ? sm.a[slot][chunk_pos(row, c)] : sm.b[slot][chunk_pos(row, c)]);
 }
 
+// Product m (0..31) of a step: k half m / 16, tile pair ((m / 4) % 4, m % 4).
 // SW = false: acc[i][j] = A rows of tile i x B rows of tile j (element r of
 // lane l: row 8 (r/4) + 4 (l/32) + r%4, column l%32).  SW = true: the
 // operands swapped, acc[i][j] holds the transposed tile (row l%32, column
 // 8 (r/4) + 4 (l/32) + r%4), so each lane holds 16 values of one row.
-template <bool SW = false>
-__device__ __forceinline__ void mfma_slot(const Frags& f, f32x16 (&acc)[4][4]) {
-#pragma unroll
-  for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc[i][j] = SW ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[kk][4 + j], f[kk][i], acc[i][j], 0, 0, 0)
-                       : __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[kk][i], f[kk][4 + j], acc[i][j], 0, 0, 0);
-}
-
-// Single pieces of a step, for the explicitly interleaved steady state:
-// product m (k half m / 16, tile pair ((m / 4) % 4, m % 4)), fragment read q
-// (k half q / 8; A tiles for q % 8 < 4, B tiles above) and copy q (operand
-// q % 2, chunk group q / 2) of one stage.
 template <bool SW>
 __device__ __forceinline__ void mfma_one(const Frags& f, f32x16 (&acc)[4][4], int m) {
   const int kk = m >> 4, i = (m >> 2) & 3, j = m & 3;
@@ -129,127 +118,77 @@ __device__ __forceinline__ void mfma_one(const Frags& f, f32x16 (&acc)[4][4], in
                  : __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[kk][i], f[kk][4 + j], acc[i][j], 0, 0, 0);
 }
 
-__device__ __forceinline__ void read_frag_one(const Ring& sm, int buf, int wave, int lane, Frags& f,
-                                              int q) {
-  const int kk = q >> 3, t = q & 7;
-  const int c = kk * 2 + (lane >> 5);
-  const int row = (t < 4 ? (wave >> 1) : (wave & 1)) * 128 + (t & 3) * 32 + (lane & 31);
-  f[kk][t] = __builtin_bit_cast(bf16x8, t < 4 ? sm.a[buf][chunk_pos(row, c)] : sm.b[buf][chunk_pos(row, c)]);
-}
-
-__device__ __forceinline__ void issue_one(Ring& sm, int buf, const bf16_t* pa, const bf16_t* pb,
-                                          const uint32_t (&oa)[4], const uint32_t (&ob)[4], int wave,
-                                          int q) {
-  const int g = q >> 1;
-  if (q & 1)
-    __builtin_amdgcn_global_load_lds((const void*)(pb + ob[g]), (lds_void*)&sm.b[buf][(g * 4 + wave) * 64],
-                                     16, 0, 0);
-  else
-    __builtin_amdgcn_global_load_lds((const void*)(pa + oa[g]), (lds_void*)&sm.a[buf][(g * 4 + wave) * 64],
-                                     16, 0, 0);
-}
-
-// Slices requested but not yet known to have landed may number at most
-// `pending` (0..4) when this returns (eight copies per slice and lane).
-__device__ __forceinline__ void wait_pending(int pending) {
-  if (pending >= 4) wait_vmem<32>();
-  else if (pending == 3) wait_vmem<24>();
-  else if (pending == 2) wait_vmem<16>();
-  else if (pending == 1) wait_vmem<8>();
-  else wait_vmem<0>();
-}
-
-// One k slice i (not the last) of the main loop, register set CUR holding
-// its fragments: wait for slice i + 1, barrier (every wave has slice i in
-// registers, so its slot is free), request slice i + 5 into that slot, then
-// read slice i + 1 into the other register set interleaved with the 32
-// products of slice i.  STEADY steps (i + 5 < n, so slice i + 5 exists and
-// exactly three slices besides i + 1 are in flight) are branch-free, and
-// their eight copies are spread over the first half of the products instead
-// of being issued in one burst behind the barrier, where they would hold up
-// the first product while the four waves' copies queue at the address unit.
-template <bool SW, int CUR, bool STEADY, class Addr>
-__device__ __forceinline__ void loop_step(Ring& sm, int i, int n, int kt0, const Addr& addr,
-                                          const uint32_t (&oa)[4], const uint32_t (&ob)[4],
-                                          int wave, int lane, Frags (&F)[2],
-                                          f32x16 (&acc)[4][4]) {
-  if constexpr (STEADY) wait_vmem<(NSTAGE - 2) * 8>();
-  else wait_pending(min(n, i + NSTAGE) - (i + 2));
-  wait_lds();  // this wave's reads of slice i (issued one step ago) are complete
-  __builtin_amdgcn_s_barrier();
-  if constexpr (STEADY) {
-    const bf16_t *pa, *pb;
-    addr(kt0 + i + NSTAGE, pa, pb);
-    const int wbuf = (i + NSTAGE) % NSTAGE, rbuf = (i + 1) % NSTAGE;
-    // products in program order, fenced; the 16 LDS reads of the next slice
-    // follow products 0, 1, 3, 4, ..., 22 (read q after product 3q/2), so
-    // the last one has nine products to land before the next step's wait,
-    // and the eight copies follow products 2, 5, ..., 23
+// One step: the 32 products of `cur` in program order, fenced one by one.
+// If READ, the 16 fragment reads of step `rhalf` of the pair in `rslot` go
+// into `nxt` after products 0, 1, 3, 4, ..., 22 (read q after product 3q/2),
+// so the last one has nine products to land; if LOADS, the 16 copies of the
+// pair at (pa, pb) into `lslot` follow the even products.
+template <bool SW, bool READ, bool LOADS>
+__device__ __forceinline__ void step(Ring& sm, const Frags& cur, Frags& nxt, int rslot, int rhalf,
+                                     int lslot, const bf16_t* pa, const bf16_t* pb, uint32_t oa,
+                                     uint32_t ob, uint32_t lda, uint32_t ldb, int wave, int lane,
+                                     f32x16 (&acc)[4][4]) {
 #pragma unroll
-    for (int m = 0; m < 32; ++m) {
-      mfma_one<SW>(F[CUR], acc, m);
-      if (m < 24) {
-        if (m % 3 == 2) issue_one(sm, wbuf, pa, pb, oa, ob, wave, m / 3);
-        else read_frag_one(sm, rbuf, wave, lane, F[CUR ^ 1], (2 * m + (m % 3)) / 3);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  } else {
-    if (i + NSTAGE < n) {
-      const bf16_t *pa, *pb;
-      addr(kt0 + i + NSTAGE, pa, pb);
-      issue_stage(sm, (i + NSTAGE) % NSTAGE, pa, pb, oa, ob, wave);
-    }
-    read_frags(sm, (i + 1) % NSTAGE, wave, lane, F[CUR ^ 1]);
-    mfma_slot<SW>(F[CUR], acc);
-#pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // two matrix-core products
-    }
+  for (int m = 0; m < 32; ++m) {
+    mfma_one<SW>(cur, acc, m);
+    if (READ && m < 24 && m % 3 != 2)
+      read_frag_one(sm, rslot, rhalf, wave, lane, nxt, (2 * m + (m % 3)) / 3);
+    if (LOADS && m % 2 == 0) issue_one(sm, lslot, pa, pb, oa, ob, lda, ldb, wave, m / 2);
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
-// acc += sum over k slices [kt0, kt1) of Aslice(kt) Bslice(kt)^T, where
-// addr(kt, pa, pb) yields the slice base pointers (row 0, k = 32 kt).
-// Slices are copied global -> LDS five slots ahead; fragments are read one
-// slice ahead into a second register set.
+// acc += sum over k pairs [p0, p1) of Apair(p) Bpair(p)^T, where
+// addr(p, pa, pb) yields the pair's base pointers (row 0, k = 64 p).  Pairs
+// are copied global -> LDS one ahead, into two slots.  Per pair, step A
+// multiplies the pair's first 32 k from registers while reading its second
+// half; step B waits for the next pair, takes the pair's one barrier (every
+// wave has finished reading this pair's slot and sees the next pair), then
+// multiplies the second half while reading the next pair's first half and
+// copying the pair after next into the slot just freed.
 template <bool SW = false, class Addr>
-__device__ __forceinline__ void mainloop(Ring& sm, int kt0, int kt1, uint32_t lda, uint32_t ldb,
+__device__ __forceinline__ void mainloop(Ring& sm, int p0, int p1, uint32_t lda, uint32_t ldb,
                                          const Addr& addr, f32x16 (&acc)[4][4]) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS bases in SGPRs
-  const int n = kt1 - kt0;
+  const int n = p1 - p0;
   if (n <= 0) return;
-  uint32_t oa[4], ob[4];
-  chunk_offsets(wave, lane, lda, oa);
-  chunk_offsets(wave, lane, ldb, ob);
-  for (int s = 0; s < NSTAGE && s < n; ++s) {
-    const bf16_t *pa, *pb;
-    addr(kt0 + s, pa, pb);
-    issue_stage(sm, s, pa, pb, oa, ob, wave);
+  const uint32_t oa = chunk_offset(wave, lane, lda), ob = chunk_offset(wave, lane, ldb);
+  const bf16_t *pa, *pb;
+  addr(p0, pa, pb);
+  issue_pair(sm, 0, pa, pb, oa, ob, lda, ldb, wave);
+  if (n > 1) {
+    addr(p0 + 1, pa, pb);
+    issue_pair(sm, 1, pa, pb, oa, ob, lda, ldb, wave);
+    wait_vmem<16>();
+  } else {
+    wait_vmem<0>();
   }
-  wait_pending(min(n, NSTAGE) - 1);
   __builtin_amdgcn_s_barrier();
   Frags F[2];
-  read_frags(sm, 0, wave, lane, F[0]);
-  int i = 0;
-  for (; i + NSTAGE + 1 < n; i += 2) {  // both steps of the pair request a slice
-    loop_step<SW, 0, true>(sm, i, n, kt0, addr, oa, ob, wave, lane, F, acc);
-    loop_step<SW, 1, true>(sm, i + 1, n, kt0, addr, oa, ob, wave, lane, F, acc);
-  }
-  for (; i + 2 < n; i += 2) {
-    loop_step<SW, 0, false>(sm, i, n, kt0, addr, oa, ob, wave, lane, F, acc);
-    loop_step<SW, 1, false>(sm, i + 1, n, kt0, addr, oa, ob, wave, lane, F, acc);
-  }
-  if (n - i == 2) {
-    loop_step<SW, 0, false>(sm, i, n, kt0, addr, oa, ob, wave, lane, F, acc);
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-      for (int t = 0; t < 8; ++t) F[0][kk][t] = F[1][kk][t];
+  for (int q = 0; q < 16; ++q) read_frag_one(sm, 0, 0, wave, lane, F[0], q);
+  int j = 0;
+  for (; j + 2 < n; ++j) {  // steady: step B also copies pair j + 2
+    const int slot = j & 1;
+    step<SW, true, false>(sm, F[0], F[1], slot, 1, 0, nullptr, nullptr, 0, 0, lda, ldb, wave, lane, acc);
+    wait_vmem<0>();  // pair j + 1 (the only pair in flight)
+    wait_lds();      // this wave's reads of pair j are complete
+    __builtin_amdgcn_s_barrier();
+    addr(p0 + j + 2, pa, pb);
+    step<SW, true, true>(sm, F[1], F[0], slot ^ 1, 0, slot, pa, pb, oa, ob, lda, ldb, wave, lane, acc);
   }
-  mfma_slot<SW>(F[0], acc);
+  if (j + 1 < n) {
+    const int slot = j & 1;
+    step<SW, true, false>(sm, F[0], F[1], slot, 1, 0, nullptr, nullptr, 0, 0, lda, ldb, wave, lane, acc);
+    wait_vmem<0>();
+    wait_lds();
+    __builtin_amdgcn_s_barrier();
+    step<SW, true, false>(sm, F[1], F[0], slot ^ 1, 0, 0, nullptr, nullptr, 0, 0, lda, ldb, wave, lane, acc);
+    ++j;
+  }
+  step<SW, true, false>(sm, F[0], F[1], j & 1, 1, 0, nullptr, nullptr, 0, 0, lda, ldb, wave, lane, acc);
+  step<SW, false, false>(sm, F[1], F[0], 0, 0, 0, nullptr, nullptr, 0, 0, lda, ldb, wave, lane, acc);
   __syncthreads();
 }
 
@@ -270,45 +209,43 @@ __device__ __forceinline__ void zero_acc(f32x16 (&acc)[4][4]) {
 // workgroup all pairs of a row block sit at k slice t or 8 (ncol + 1) - 1 - t,
 // so the workgroups that run together on an XCD (consecutive pairs of a few
 // row blocks) stay in step and share their operand slices in its L2.
-template <bool SW, bool REV>
+template <bool SW>
 __device__ __forceinline__ void whiten_tile(Ring& sm, const bf16_t* xa, const bf16_t* Y, const bf16_t* Y2,
-                                            uint32_t cj, uint32_t Kp, f32x16 (&acc)[4][4]) {
-  const int kt1 = (int)((cj + 1) * (TM / TK));
+                                            uint32_t cj, bool rev, uint32_t Kp, f32x16 (&acc)[4][4]) {
+  const int np = (int)((cj + 1) * (TM / PK));
   zero_acc(acc);
-  {
-    const bf16_t* yb = Y + (size_t)cj * TM * Kp;
-    auto addr = [&](int kt, const bf16_t*& pa, const bf16_t*& pb) {
-      const int k = REV ? kt1 - 1 - kt : kt;
-      pa = xa + k * TK;
-      pb = yb + k * TK;
+  for (int pass = 0; pass < (Y2 != nullptr ? 2 : 1); ++pass) {
+    const bf16_t* yb = (pass ? Y2 : Y) + (size_t)cj * TM * Kp;
+    auto addr = [&](int p, const bf16_t*& pa, const bf16_t*& pb) {
+      const int k = rev ? np - 1 - p : p;
+      pa = xa + k * PK;
+      pb = yb + k * PK;
     };
-    mainloop<SW>(sm, 0, kt1, Kp, Kp, addr, acc);
-  }
-  if (Y2 != nullptr) {
-    const bf16_t* yb = Y2 + (size_t)cj * TM * Kp;
-    auto addr = [&](int kt, const bf16_t*& pa, const bf16_t*& pb) {
-      const int k = REV ? kt1 - 1 - kt : kt;
-      pa = xa + k * TK;
-      pb = yb + k * TK;
-    };
-    mainloop<SW>(sm, 0, kt1, Kp, Kp, addr, acc);
+    mainloop<SW>(sm, 0, np, Kp, Kp, addr, acc);
   }
 }
 
 __device__ __forceinline__ void store_whitened(const f32x16 (&acc)[4][4], bf16_t* C, uint32_t rb,
                                                uint32_t cj, uint32_t Kp) {
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
-  bf16_t* cb = C + (size_t)rb * TM * Kp + (size_t)cj * TM;
+  // per-lane base (row 4 (l / 32), column l % 32 of the wave's quadrant);
+  // the offsets of the accumulator elements below are wave-uniform.  The
+  // opaque copy of the row pitch keeps the compiler from computing those
+  // offsets once ahead of the tile loop and holding them across the main loop.
+  uint32_t ldc = Kp;
+  asm volatile("" : "+s"(ldc));
+  bf16_t* lp = C + ((size_t)rb * TM + wm * 128 + 4 * (lane >> 5)) * ldc + (size_t)cj * TM + wn * 128 +
+               (lane & 31);
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int row = wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        const int col = wn * 128 + j * 32 + (lane & 31);
-        cb[(size_t)row * Kp + col] = f32_to_bf16(acc[i][j][r]);
+        const uint32_t row = i * 32 + 8 * (r >> 2) + (r & 3);
+        lp[row * ldc + j * 32] = f32_to_bf16(acc[i][j][r]);
       }
 }
 
@@ -324,11 +261,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_whiten_bf16(const bf16_t* __restric
   const uint32_t rb = t / npair, c = t % npair;
   const bf16_t* xa = X + (size_t)rb * TM * Kp;
   f32x16 acc[4][4];
-  whiten_tile<false, false>(sm, xa, Y, Y2, c, Kp, acc);
-  store_whitened(acc, C, rb, c, Kp);
-  if (ncol - 1 - c != c) {
-    whiten_tile<false, true>(sm, xa, Y, Y2, ncol - 1 - c, Kp, acc);
-    store_whitened(acc, C, rb, ncol - 1 - c, Kp);
+  for (uint32_t h = 0; h < (ncol - 1 - c != c ? 2u : 1u); ++h) {
+    const uint32_t cj = h ? ncol - 1 - c : c;
+    whiten_tile<false>(sm, xa, Y, Y2, cj, h != 0, Kp, acc);
+    store_whitened(acc, C, rb, cj, Kp);
   }
 }
 
@@ -370,11 +306,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_whiten_norm_bf16(const bf16_t* __re
   const uint32_t rb = t / npair, c = t % npair;
   const bf16_t* xa = X + (size_t)rb * TM * Kp;
   f32x16 acc[4][4];
-  whiten_tile<true, false>(sm, xa, Y, Y2, c, Kp, acc);
-  store_norms(acc, part, rb, c, ncol);
-  if (ncol - 1 - c != c) {
-    whiten_tile<true, true>(sm, xa, Y, Y2, ncol - 1 - c, Kp, acc);
-    store_norms(acc, part, rb, ncol - 1 - c, ncol);
+  for (uint32_t h = 0; h < (ncol - 1 - c != c ? 2u : 1u); ++h) {
+    const uint32_t cj = h ? ncol - 1 - c : c;
+    whiten_tile<true>(sm, xa, Y, Y2, cj, h != 0, Kp, acc);
+    store_norms(acc, part, rb, cj, ncol);
   }
 }
 
@@ -400,20 +335,20 @@ __global__ __launch_bounds__(NTHR, 1) void k_syrk_bf16(const bf16_t* __restrict_
   const uint32_t z = t / ntiles, tile = t % ntiles;
   uint32_t ti, tj;
   upper_tile(tile, T, ti, tj);
-  const uint32_t kps = ld / TK;  // k slices per segment
-  const uint64_t ktot = (uint64_t)kps * nseg;
-  const int kt0 = (int)(ktot * z / splits), kt1 = (int)(ktot * (z + 1) / splits);
+  const uint32_t pps = ld / PK;  // k pairs per segment
+  const uint64_t ptot = (uint64_t)pps * nseg;
+  const int p0 = (int)(ptot * z / splits), p1 = (int)(ptot * (z + 1) / splits);
   const bf16_t* xa = X + (size_t)ti * TM * ld;
   const bf16_t* xb = X + (size_t)tj * TM * ld;
   f32x16 acc[4][4];
   zero_acc(acc);
-  auto addr = [&](int kt, const bf16_t*& pa, const bf16_t*& pb) {
-    const uint32_t s = (uint32_t)kt / kps, o = (uint32_t)kt % kps;
-    const size_t base = (size_t)s * seg_stride + (size_t)o * TK;
+  auto addr = [&](int p, const bf16_t*& pa, const bf16_t*& pb) {
+    const uint32_t s = (uint32_t)p / pps, o = (uint32_t)p % pps;
+    const size_t base = (size_t)s * seg_stride + (size_t)o * PK;
     pa = xa + base;
     pb = xb + base;
   };
-  mainloop(sm, kt0, kt1, ld, ld, addr, acc);
+  mainloop(sm, p0, p1, ld, ld, addr, acc);
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   float* pt = P + ((size_t)z * ntiles + tile) * TILE_FLOATS;
 #pragma unroll
@@ -482,10 +417,10 @@ hipError_t launch_whiten_norm_bf16(const bf16_t* X, const bf16_t* Y, const bf16_
 
 hipError_t launch_syrk_bf16(const bf16_t* X, int64_t dim_p, int64_t ld, int64_t seg_stride,
                             int64_t nseg, int splits, float* P, const int* st, hipStream_t s) {
-  if (dim_p <= 0 || dim_p % TM || ld <= 0 || ld % TK || nseg <= 0 || splits <= 0)
+  if (dim_p <= 0 || dim_p % TM || ld <= 0 || ld % PK || nseg <= 0 || splits <= 0)
     return hipErrorInvalidValue;
   const int64_t T = dim_p / TM, ntiles = T * (T + 1) / 2;
-  if ((int64_t)splits > (ld / TK) * nseg) return hipErrorInvalidValue;
+  if ((int64_t)splits > (ld / PK) * nseg) return hipErrorInvalidValue;
   if (ntiles * splits > 0x7fffffff) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_syrk_bf16, dim3((uint32_t)(ntiles * splits)), dim3(NTHR), 0, s, X,
                      (uint32_t)ld, (uint64_t)seg_stride, (uint32_t)nseg, (uint32_t)T,
