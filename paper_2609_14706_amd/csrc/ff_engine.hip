@@ -64,6 +64,7 @@ struct Side {
   int splits = 1;                    // k-splits of the symmetric product producing this side
   size_t partial_floats = 0;
   bool lw_valid = false;             // Lw holds the inverse factor of F[cur]
+  bool start_identity = false;       // the starting factor is I (no A0 / B0 given)
   int code = 0;                      // 1 = A, 2 = B
   // streams of the blocked factorisation (created on first use): the helper
   // runs the bulk of each trailing update, istream builds the inverse
@@ -525,23 +526,28 @@ ff_status update_rank1(ff_handle_s* h, Side& s, Side& p, int slot, bool finish,
 }
 
 // s.F[slot] = (1/(N p.dim)) sum_i X_i Li_p^T Li_p X_i^T  (+ damping), trace into
-// s.tr; with finish = false, without damping and trace.
-ff_status update(ff_handle_s* h, Side& s, Side& p, int slot, bool finish = true) {
+// s.tr; with finish = false, without damping and trace.  p_identity: p's
+// factor is exactly I (the default start), so Li_p = I and the whitened
+// samples are the samples themselves (bitwise: a product with I is exact);
+// the symmetric product then reads X directly.
+ff_status update(ff_handle_s* h, Side& s, Side& p, int slot, bool finish = true,
+                 bool p_identity = false) {
   if (h->lay.rank1) return update_rank1(h, s, p, slot, finish);
   const void* X = (&s == &h->B) ? h->Gx : h->Gt;
   const int64_t N = h->N, rows = N * s.dim_p, Kp = p.dim_p;
   const double scale = 1.0 / ((double)N * (double)p.dim);
   const double wflop = (double)N * s.dim * p.dim * p.dim;
   const double sflop = (double)N * p.dim * s.dim * s.dim;
+  const void* Wsrc = p_identity ? X : (const void*)h->W;
   if (h->bf16) {
-    {
+    if (!p_identity) {
       Timed t(h, 0, wflop);
       FF_HIP(launch_whiten_bf16((const bf16_t*)X, (const bf16_t*)p.Lw, (const bf16_t*)p.Lw2,
                                 (bf16_t*)h->W, rows, Kp, h->st, h->stream));
     }
     {
       Timed t(h, 1, sflop);
-      FF_HIP(launch_syrk_bf16((const bf16_t*)h->W, s.dim_p, Kp, s.dim_p * Kp, N, s.splits, h->P,
+      FF_HIP(launch_syrk_bf16((const bf16_t*)Wsrc, s.dim_p, Kp, s.dim_p * Kp, N, s.splits, h->P,
                               h->st, h->stream));
     }
     {
@@ -553,7 +559,7 @@ ff_status update(ff_handle_s* h, Side& s, Side& p, int slot, bool finish = true)
     GemmF32 g{};
     g.st = h->st;
     g.ksplit = 1;
-    {
+    if (!p_identity) {
       Timed t(h, 0, wflop);
       g.A = (const float*)X; g.lda = Kp; g.transA = 0;
       g.B = (const float*)p.Lw; g.ldb = Kp; g.transB = 1;
@@ -566,8 +572,8 @@ ff_status update(ff_handle_s* h, Side& s, Side& p, int slot, bool finish = true)
       Timed t(h, 1, sflop);
       GemmF32 q{};
       q.st = h->st;
-      q.A = (const float*)h->W; q.lda = Kp; q.transA = 0;
-      q.B = (const float*)h->W; q.ldb = Kp; q.transB = 1;
+      q.A = (const float*)Wsrc; q.lda = Kp; q.transA = 0;
+      q.B = (const float*)Wsrc; q.ldb = Kp; q.transB = 1;
       q.C = h->P; q.ldc = s.dim_p; q.sC = s.dim_p * s.dim_p;
       q.M = s.dim_p; q.N = s.dim_p; q.K = N * Kp;
       q.kseg = Kp; q.segA = q.segB = s.dim_p * Kp;
@@ -641,14 +647,17 @@ ff_status iterate_chunk(ff_handle_s* h, int iters, int* done, double* loglik) {
   Side& second = bfirst ? h->A : h->B;
   const int64_t base = h->iters_total;
   ff_status rc;
-  if (!second.lw_valid) {
+  // Before the first iteration the factor updated second may still be the
+  // default start I: its whitening operand is I, nothing to factorise or apply.
+  const bool start_id = base == 0 && second.start_identity && !h->lay.rank1;
+  if (!second.lw_valid && !start_id) {
     rc = operand(h, second, h->cur, (int)(base + 1));
     if (rc != FF_OK) return rc;
   }
   for (int k = 1; k <= iters; ++k) {
     const int64_t g = base + k;
     const int slot = (int)(g & 1);
-    if ((rc = update(h, first, second, slot)) != FF_OK) return rc;
+    if ((rc = update(h, first, second, slot, true, start_id && k == 1)) != FF_OK) return rc;
     if ((rc = operand(h, first, slot, (int)g)) != FF_OK) return rc;
     if ((rc = update(h, second, first, slot)) != FF_OK) return rc;
     FF_HIP(launch_normalise(h->A.F[slot], h->n, h->B.F[slot], h->m, h->A.tr, h->c, h->st,
@@ -859,6 +868,8 @@ ff_status ff_init(const ff_config* cfg, ff_handle* out) {
   };
   side(h->A, lay.off_A, h->n, lay.n_p, lay.splitsA, 1);
   side(h->B, lay.off_B, h->m, lay.m_p, lay.splitsB, 2);
+  h->A.start_identity = cfg->A0 == nullptr;
+  h->B.start_identity = cfg->B0 == nullptr;
 
   auto setup = [&]() -> ff_status {
     FF_HIP(launch_set_int(h->st, 4, 0, h->stream));
