@@ -18,6 +18,7 @@
 // the identity.
 #include <math.h>
 
+#include <algorithm>
 #include <type_traits>
 
 #include "ff_common.hpp"
@@ -212,12 +213,71 @@ __device__ __forceinline__ int cholinv_lds(LeafLDS& sm, int o, int wave, int lan
   return -1;
 }
 
-__global__ __launch_bounds__(256) void k_chol_leaf(const float* Lblk, float* __restrict__ Liblk,
-                                                   int64_t ld, int b, int64_t pivot_base,
-                                                   double* logdet, int slot, int iteration,
-                                                   int side, int* st, float* Lout) {
-  if (ff_halted(st)) return;
-  __shared__ LeafLDS sm;
+// 128 x 128 x 128 product of two LDS operands held as rows (pitch SP):
+// acc[a][b] = P[rows of tile a] Q[rows of tile b]^T over all 128 k, for the
+// 64 x 64 quadrant (wm, wn) of this wave (2 x 2 tiles of 32 x 32).
+__device__ __forceinline__ void quad_product(const float (*P)[SP], const float (*Q)[SP], int wave,
+                                             int lane, f32x16 (&acc)[2][2]) {
+  const int wm = wave >> 1, wn = wave & 1, li = lane & 31, lk = lane >> 5;
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][c][r] = 0.0f;
+#pragma unroll 4
+  for (int k = 0; k < NB; k += 2) {
+    const float p0 = P[wm * 64 + li][k + lk], p1 = P[wm * 64 + 32 + li][k + lk];
+    const float q0 = Q[wn * 64 + li][k + lk], q1 = Q[wn * 64 + 32 + li][k + lk];
+    acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(p0, q0, acc[0][0], 0, 0, 0);
+    acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(p0, q1, acc[0][1], 0, 0, 0);
+    acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(p1, q0, acc[1][0], 0, 0, 0);
+    acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(p1, q1, acc[1][1], 0, 0, 0);
+  }
+}
+// Quadrant-relative row / column of element r of this lane in tile (a, c).
+__device__ __forceinline__ int quad_row(int wave, int a, int r, int lane) {
+  return (wave >> 1) * 64 + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+}
+__device__ __forceinline__ int quad_col(int wave, int c, int lane) {
+  return (wave & 1) * 64 + c * 32 + (lane & 31);
+}
+
+// rows [0, 128) x 128 columns of M (ld) from row r0 / column c0 into T
+// (pitch SP); rows at or beyond rlim are zero.  16-byte loads when aligned.
+__device__ __forceinline__ void load_rows(float (*T)[SP], const float* M, int64_t ld, int64_t r0,
+                                          int64_t c0, int64_t rlim, int tid) {
+  if ((ld & 3) == 0 && ((reinterpret_cast<uintptr_t>(M + c0) & 15) == 0)) {
+    const int q = tid & 31, r = tid >> 5;
+    float4 v[NB / 8];
+#pragma unroll
+    for (int t = 0; t < NB / 8; ++t) {
+      const int64_t i = r0 + r + 8 * t;
+      v[t] = i < rlim ? *reinterpret_cast<const float4*>(M + i * ld + c0 + 4 * q)
+                      : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int t = 0; t < NB / 8; ++t) {
+      float* d = &T[r + 8 * t][4 * q];
+      d[0] = v[t].x;
+      d[1] = v[t].y;
+      d[2] = v[t].z;
+      d[3] = v[t].w;
+    }
+  } else {
+    const int j = tid & (NB - 1), i0 = tid >> 7;
+    for (int i = i0; i < NB; i += 2) T[i][j] = r0 + i < rlim ? M[(r0 + i) * ld + c0 + j] : 0.0f;
+  }
+}
+
+// Cholesky + inverse of one diagonal block by one workgroup (see
+// launch_chol_leaf).  Lpre (optional): the block row of the last panel to
+// the left (b rows x 128, leading dimension ld), whose update
+// A -= Lpre Lpre^T is applied to the block first.
+__device__ __forceinline__ void leaf_body(LeafLDS& sm, const float* Lblk, float* __restrict__ Liblk,
+                                          int64_t ld, int b, int64_t pivot_base, double* logdet,
+                                          int slot, int iteration, int side, int* st, float* Lout,
+                                          const float* Lpre) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int j = tid & (NB - 1), i0 = tid >> 7;
   if (b == NB && (ld & 3) == 0 && (reinterpret_cast<uintptr_t>(Lblk) & 15) == 0) {
@@ -260,6 +320,25 @@ __global__ __launch_bounds__(256) void k_chol_leaf(const float* Lblk, float* __r
   }
   if (tid == 0) sm.bad = -1;
   __syncthreads();
+  if (Lpre != nullptr) {
+    // A -= Lpre Lpre^T (Lpre staged in X, cleared again afterwards)
+    load_rows(sm.X, Lpre, ld, 0, 0, b, tid);
+    __syncthreads();
+    f32x16 u[2][2];
+    quad_product(sm.X, sm.X, wave, lane, u);
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int i = quad_row(wave, a, r, lane), jj = quad_col(wave, c, lane);
+          if (jj <= i) sm.S[i][jj] -= u[a][c][r];
+        }
+    __syncthreads();
+    for (int i = tid >> 7; i < NB; i += 2) sm.X[i][tid & (NB - 1)] = 0.0f;
+    __syncthreads();
+  }
   const int bad = cholinv_lds<NB>(sm, 0, wave, lane);
   if (bad >= 0) {
     if (tid == 0) {
@@ -285,6 +364,137 @@ __global__ __launch_bounds__(256) void k_chol_leaf(const float* Lblk, float* __r
   }
 }
 
+__global__ __launch_bounds__(256) void k_chol_leaf(const float* Lblk, float* __restrict__ Liblk,
+                                                   int64_t ld, int b, int64_t pivot_base,
+                                                   double* logdet, int slot, int iteration,
+                                                   int side, int* st, float* Lout) {
+  if (ff_halted(st)) return;
+  __shared__ LeafLDS sm;
+  leaf_body(sm, Lblk, Liblk, ld, b, pivot_base, logdet, slot, iteration, side, st, Lout, nullptr);
+}
+
+// Trailing-update tile of a right-looking step: the two 128-row blocks of
+// the panel (columns ok.., rows i0.. and j0..) in LDS.
+struct TrailLDS {
+  float a[NB][SP];
+  float b[NB][SP];
+};
+union StepLDS {
+  LeafLDS leaf;
+  TrailLDS trail;
+};
+
+// One step of the blocked factorisation after panel k (columns ok..ok+127)
+// has been solved: workgroup 0 factors and inverts the next diagonal block
+// (d0 = ok + 128) after applying the panel's update to it; workgroups
+// 1..gridDim.x-1 apply the panel's update A_ij -= L_ik L_jk^T to every other
+// 128 x 128 block of the trailing lower triangle (block rows >= block
+// columns >= d0 / 128, the diagonal block excluded), round robin.  With
+// ok < 0 there is no panel yet: the kernel factors block 0 only.
+__global__ __launch_bounds__(256) void k_chol_step(float* __restrict__ L, float* __restrict__ Li,
+                                                   int64_t dim, int64_t ok, double* logdet,
+                                                   int iteration, int side, int* st) {
+  if (ff_halted(st)) return;
+  __shared__ StepLDS sm;
+  const int64_t d0 = ok + NB;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  if (blockIdx.x == 0) {
+    const int b = (int)min<int64_t>(NB, dim - d0);
+    float* Akk = L + d0 * dim + d0;
+    leaf_body(sm.leaf, Akk, Li + d0 * dim + d0, dim, b, d0, logdet, (int)(d0 / NB), iteration, side,
+              st, Akk, ok >= 0 ? L + d0 * dim + ok : nullptr);
+    return;
+  }
+  const int64_t T = (dim - d0 + NB - 1) / NB;  // trailing blocks per side
+  const int64_t ntiles = T * (T + 1) / 2 - 1;
+  for (int64_t t = blockIdx.x - 1; t < ntiles; t += gridDim.x - 1) {
+    // lower-triangle index t + 1 (index 0 is the diagonal block) -> (bi >= bj)
+    const int64_t u = t + 1;
+    int64_t bi = 0;
+    while ((bi + 1) * (bi + 2) / 2 <= u) ++bi;
+    const int64_t bj = u - bi * (bi + 1) / 2;
+    const int64_t i0 = d0 + bi * NB, j0 = d0 + bj * NB;
+    load_rows(sm.trail.a, L, dim, i0, ok, dim, tid);
+    if (bi != bj) load_rows(sm.trail.b, L, dim, j0, ok, dim, tid);
+    __syncthreads();
+    f32x16 u4[2][2];
+    quad_product(sm.trail.a, bi != bj ? sm.trail.b : sm.trail.a, wave, lane, u4);
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int64_t i = i0 + quad_row(wave, a, r, lane), j = j0 + quad_col(wave, c, lane);
+          if (i < dim && j < dim && (bi != bj || j <= i)) L[i * dim + j] -= u4[a][c][r];
+        }
+    __syncthreads();  // before the next tile's rows overwrite LDS
+  }
+}
+
+// Panel of the blocked factorisation: L_ik = A_ik L_kk^-T for the rows
+// below a diagonal block, in place.  One workgroup per 64 rows holds its rows
+// (64 x 128) and the block's inverse (128 x 128, zero above the diagonal) in
+// LDS; wave w computes output columns 32 w .. 32 w + 31 (two 32 x 32 tiles).
+struct PanelLDS {
+  float a[64][SP];
+  float x[NB][SP];
+};
+
+__global__ __launch_bounds__(256) void k_panel_solve(float* __restrict__ P, const float* __restrict__ Xkk,
+                                                     int64_t ld, int64_t rows, const int* st) {
+  if (ff_halted(st)) return;
+  __shared__ PanelLDS sm;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int64_t r0 = (int64_t)blockIdx.x * 64;
+  const bool vec = (ld & 3) == 0 && (reinterpret_cast<uintptr_t>(P) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(Xkk) & 15) == 0;
+  if (vec) {
+    const int q = tid & 31, r = tid >> 5;
+    float4 va[8], vx[16];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const int64_t i = r0 + r + 8 * t;
+      va[t] = i < rows ? *reinterpret_cast<const float4*>(P + i * ld + 4 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int t = 0; t < 16; ++t) vx[t] = *reinterpret_cast<const float4*>(Xkk + (int64_t)(r + 8 * t) * ld + 4 * q);
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      float* d = &sm.a[r + 8 * t][4 * q];
+      d[0] = va[t].x; d[1] = va[t].y; d[2] = va[t].z; d[3] = va[t].w;
+    }
+#pragma unroll
+    for (int t = 0; t < 16; ++t) {
+      float* d = &sm.x[r + 8 * t][4 * q];
+      d[0] = vx[t].x; d[1] = vx[t].y; d[2] = vx[t].z; d[3] = vx[t].w;
+    }
+  } else {
+    const int j = tid & (NB - 1), i0 = tid >> 7;
+    for (int i = i0; i < 64; i += 2) sm.a[i][j] = r0 + i < rows ? P[(r0 + i) * ld + j] : 0.0f;
+    for (int i = i0; i < NB; i += 2) sm.x[i][j] = Xkk[(int64_t)i * ld + j];
+  }
+  __syncthreads();
+  // out(i, j) = sum_k a[i][k] x[j][k], k <= j (x lower triangular)
+  const int li = lane & 31, lk = lane >> 5, j0 = wave * 32;
+  f32x16 acc0, acc1;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc0[r] = acc1[r] = 0.0f;
+#pragma unroll 4
+  for (int k = 0; k < j0 + 32; k += 2) {
+    const float xb = sm.x[j0 + li][k + lk];
+    acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.a[li][k + lk], xb, acc0, 0, 0, 0);
+    acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.a[32 + li][k + lk], xb, acc1, 0, 0, 0);
+  }
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int i = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+    const int64_t g0 = r0 + i, g1 = r0 + 32 + i;
+    if (g0 < rows) P[g0 * ld + j0 + li] = acc0[r];
+    if (g1 < rows) P[g1 * ld + j0 + li] = acc1[r];
+  }
+}
+
 }  // namespace
 
 hipError_t launch_chol_leaf(const float* Lblk, float* Liblk, int64_t ld, int b, int64_t pivot_base,
@@ -294,6 +504,28 @@ hipError_t launch_chol_leaf(const float* Lblk, float* Liblk, int64_t ld, int b, 
   if (Lout != nullptr && Lout != Lblk) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_chol_leaf, dim3(1), dim3(256), 0, s, Lblk, Liblk, ld, b, pivot_base, logdet,
                      slot, iteration, side, st, Lout);
+  return hipGetLastError();
+}
+
+hipError_t launch_chol_step(float* L, float* Li, int64_t dim, int64_t ok, double* logdet,
+                            int iteration, int side, int* st, hipStream_t s) {
+  if (dim < 1 || ok < -kLeaf || ok % kLeaf != 0 || ok + kLeaf >= dim) return hipErrorInvalidValue;
+  const int64_t d0 = ok + kLeaf;
+  const int64_t T = (dim - d0 + kLeaf - 1) / kLeaf;
+  const int64_t ntiles = ok < 0 ? 0 : T * (T + 1) / 2 - 1;
+  const int64_t grid = 1 + std::min<int64_t>(ntiles, kStepWorkers);
+  hipLaunchKernelGGL(k_chol_step, dim3((uint32_t)grid), dim3(256), 0, s, L, Li, dim, ok, logdet,
+                     iteration, side, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_panel_solve(float* P, const float* Xkk, int64_t ld, int64_t rows, const int* st,
+                              hipStream_t s) {
+  if (rows < 0 || ld < kLeaf) return hipErrorInvalidValue;
+  if (rows == 0) return hipSuccess;
+  const int64_t grid = (rows + 63) / 64;
+  if (grid > 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_panel_solve, dim3((uint32_t)grid), dim3(256), 0, s, P, Xkk, ld, rows, st);
   return hipGetLastError();
 }
 

@@ -66,10 +66,8 @@ struct Side {
   bool lw_valid = false;             // Lw holds the inverse factor of F[cur]
   bool start_identity = false;       // the starting factor is I (no A0 / B0 given)
   int code = 0;                      // 1 = A, 2 = B
-  // streams of the blocked factorisation (created on first use): the helper
-  // runs the bulk of each trailing update, istream builds the inverse
-  hipStream_t helper = nullptr;
-  hipEvent_t hfork = nullptr, hjoin = nullptr;
+  // second stream of the blocked factorisation (created on first use): it
+  // builds the off-diagonal blocks of the inverse
   hipStream_t istream = nullptr;
   hipEvent_t ev_leaf = nullptr, ev_inv = nullptr;
 };
@@ -287,11 +285,6 @@ void collect_timing(ff_handle_s* h) {
 
 // ------------------------------------------------------- factorisation
 ff_status side_streams(Side& s) {
-  if (s.helper == nullptr) {
-    FF_HIP(hipStreamCreateWithFlags(&s.helper, hipStreamNonBlocking));
-    FF_HIP(hipEventCreateWithFlags(&s.hfork, hipEventDisableTiming));
-    FF_HIP(hipEventCreateWithFlags(&s.hjoin, hipEventDisableTiming));
-  }
   if (s.istream == nullptr) {
     FF_HIP(hipStreamCreateWithFlags(&s.istream, hipStreamNonBlocking));
     FF_HIP(hipEventCreateWithFlags(&s.ev_leaf, hipEventDisableTiming));
@@ -301,109 +294,139 @@ ff_status side_streams(Side& s) {
 }
 
 // Off-diagonal blocks of L^-1 for the node [o, o + sz) of the leaf tree, on
-// stream st: Li21 = -Li22 (L21 Li11), with (L21 Li11)^T parked in the node's
-// block above the diagonal of s.L.  The children are done before (in order
-// on the same stream).
-ff_status inverse_node(ff_handle_s* h, Side& s, int64_t o, int64_t sz, hipStream_t st) {
+// stream st, in two products: P1, T^T = (L21 Li11)^T, parked in the node's
+// block above the diagonal of s.L, needs the left half done (its inverse and
+// the panels below it); P2, Li21 = -Li22 T, needs the right half's inverse
+// too.  64 x 64 tiles: with one operand triangular, 128 x 128 tiles leave a
+// few long workgroups to finish alone.
+struct TreeNode {
+  int64_t hh, r;
+  float *L21, *Li11, *Li21, *Li22, *Tt;
+};
+
+TreeNode tree_node(Side& s, int64_t o, int64_t sz) {
   const int64_t d = s.dim;
   const int64_t nl = (sz + kLeaf - 1) / kLeaf;
-  const int64_t hh = (nl + 1) / 2 * kLeaf, r = sz - hh;
-  float* L21 = s.L + (o + hh) * d + o;
-  float* Li11 = s.Li + o * d + o;
-  float* Li21 = s.Li + (o + hh) * d + o;
-  float* Li22 = s.Li + (o + hh) * d + (o + hh);
-  float* Tt = s.L + o * d + (o + hh);
+  TreeNode t;
+  t.hh = (nl + 1) / 2 * kLeaf;
+  t.r = sz - t.hh;
+  t.L21 = s.L + (o + t.hh) * d + o;
+  t.Li11 = s.Li + o * d + o;
+  t.Li21 = s.Li + (o + t.hh) * d + o;
+  t.Li22 = s.Li + (o + t.hh) * d + (o + t.hh);
+  t.Tt = s.L + o * d + (o + t.hh);
+  return t;
+}
+
+GemmF32 tree_gemm(ff_handle_s* h, Side& s) {
   GemmF32 g{};
-  g.lda = g.ldb = g.ldc = d;
+  g.lda = g.ldb = g.ldc = s.dim;
   g.kseg = INT64_MAX / 4;
   g.ksplit = 1;
   g.st = h->st;
+  g.tile = 64;
+  return g;
+}
+
+ff_status inverse_p1(ff_handle_s* h, Side& s, int64_t o, int64_t sz, hipStream_t st) {
+  const TreeNode t = tree_node(s, o, sz);
+  GemmF32 g = tree_gemm(h, s);
   // T^T = (L21 Li11)^T = Li11^T L21^T  (hh x r)
-  g.A = Li11; g.B = L21; g.C = Tt; g.M = hh; g.N = r; g.K = hh;
+  g.A = t.Li11; g.B = t.L21; g.C = t.Tt; g.M = t.hh; g.N = t.r; g.K = t.hh;
   g.transA = 1; g.transB = 1; g.alpha = 1.f; g.beta = 0.f; g.flags = kKLoRow;
   FF_HIP(launch_gemm_f32(g, 1, st));
+  return FF_OK;
+}
+
+ff_status inverse_p2(ff_handle_s* h, Side& s, int64_t o, int64_t sz, hipStream_t st) {
+  const TreeNode t = tree_node(s, o, sz);
+  GemmF32 g = tree_gemm(h, s);
   // Li21 = -Li22 T
-  g.A = Li22; g.B = Tt; g.C = Li21; g.M = r; g.N = hh; g.K = r;
+  g.A = t.Li22; g.B = t.Tt; g.C = t.Li21; g.M = t.r; g.N = t.hh; g.K = t.r;
   g.transA = 0; g.transB = 1; g.alpha = -1.f; g.beta = 0.f; g.flags = kKHiRow;
   FF_HIP(launch_gemm_f32(g, 1, st));
   return FF_OK;
 }
 
-// Enqueue, in post order, the inverse of every node of [o, o + sz) whose last
-// leaf is leaf `last` (children first).
-ff_status inverse_nodes_ending(ff_handle_s* h, Side& s, int64_t o, int64_t sz, int64_t last,
-                               hipStream_t st) {
+// Enqueue, in post order, P2 of every node of [o, o + sz) whose last leaf is
+// leaf `last` (children first).
+ff_status inverse_p2_ending(ff_handle_s* h, Side& s, int64_t o, int64_t sz, int64_t last,
+                            hipStream_t st) {
   if (sz <= kLeaf) return FF_OK;
   const int64_t nl = (sz + kLeaf - 1) / kLeaf;
   const int64_t hh = (nl + 1) / 2 * kLeaf;
   const int64_t end_leaf = (o + sz - 1) / kLeaf;
   ff_status rc;
-  if (last < (o + hh) / kLeaf) return inverse_nodes_ending(h, s, o, hh, last, st);
-  if ((rc = inverse_nodes_ending(h, s, o + hh, sz - hh, last, st)) != FF_OK) return rc;
-  if (end_leaf == last) return inverse_node(h, s, o, sz, st);
+  if (last < (o + hh) / kLeaf) return inverse_p2_ending(h, s, o, hh, last, st);
+  if ((rc = inverse_p2_ending(h, s, o + hh, sz - hh, last, st)) != FF_OK) return rc;
+  if (end_leaf == last) return inverse_p2(h, s, o, sz, st);
   return FF_OK;
 }
 
+// Enqueue P1 of the node of [o, o + sz) whose left half ends with leaf k
+// (every leaf but the last ends the left half of exactly one node).
+ff_status inverse_p1_split(ff_handle_s* h, Side& s, int64_t o, int64_t sz, int64_t k,
+                           hipStream_t st) {
+  if (sz <= kLeaf) return FF_OK;
+  const int64_t nl = (sz + kLeaf - 1) / kLeaf;
+  const int64_t hh = (nl + 1) / 2 * kLeaf;
+  const int64_t split = (o + hh) / kLeaf - 1;
+  if (k == split) return inverse_p1(h, s, o, sz, st);
+  if (k < split) return inverse_p1_split(h, s, o, hh, k, st);
+  return inverse_p1_split(h, s, o + hh, sz - hh, k, st);
+}
+
 // Cholesky factor L (lower, in place in s.L) and its inverse (s.Li) of the
-// matrix in s.L: right-looking over 128-column panels.  Main stream, per
-// panel k: the leaf (L_kk and its inverse), the panel L_ik = A_ik L_kk^-T
-// (in place), the update of the next column block; the rest of the trailing
-// update runs on the helper stream, overlapping the next leaf; the
-// off-diagonal blocks of L^-1 are built on a third stream, each node of the
-// binary tree of leaves as soon as its last leaf is done.  The upper
-// triangle of s.L is scratch.
+// matrix in s.L: right-looking over 128-column panels, two launches per
+// panel k on the main stream: the panel L_ik = A_ik L_kk^-T (in place), then
+// one step kernel in which one workgroup factors and inverts diagonal block
+// k + 1 (after applying the panel's update to it) while the others apply the
+// panel's update to the rest of the trailing lower triangle.  (Trailing
+// updates on a second stream, overlapping the diagonal blocks, delayed the
+// small kernels on the critical path instead: concurrent kernels share the
+// CUs.)  The off-diagonal blocks of L^-1 are built on a second stream from
+// the binary tree of leaves, each node's first product as soon as its left
+// half and its panels are done, its second when its last leaf is; the work
+// is handed over every kInvEvery panels (an event on the main stream costs a
+// few microseconds there).  The upper triangle of s.L is scratch.
+constexpr int64_t kInvEvery = 4;
+
 ff_status chol_blocked(ff_handle_s* h, Side& s, int iteration) {
   ff_status rc = side_streams(s);
   if (rc != FF_OK) return rc;
   const int64_t d = s.dim;
   const int64_t nb = (d + kLeaf - 1) / kLeaf;
   hipStream_t ms = h->stream;
-  GemmF32 g{};
-  g.lda = g.ldb = g.ldc = d;
-  g.kseg = INT64_MAX / 4;
-  g.ksplit = 1;
-  g.st = h->st;
   // the inverse stream starts after the work already on the main stream
   FF_HIP(hipEventRecord(s.ev_leaf, ms));
   FF_HIP(hipStreamWaitEvent(s.istream, s.ev_leaf, 0));
-  FF_HIP(hipStreamWaitEvent(s.helper, s.ev_leaf, 0));
-  for (int64_t k = 0; k < nb; ++k) {
-    const int64_t o = k * kLeaf, bk = std::min<int64_t>(kLeaf, d - o), rest = d - o - bk;
-    float* Akk = s.L + o * d + o;
-    FF_HIP(launch_chol_leaf(Akk, s.Li + o * d + o, d, (int)bk, o, s.slots, (int)k, iteration,
-                            s.code, h->st, ms, Akk));
+  FF_HIP(launch_chol_step(s.L, s.Li, d, -kLeaf, s.slots, iteration, s.code, h->st, ms));
+  int64_t handed = 0;  // leaves whose inverse products are enqueued
+  // Leaves [handed, upto] are done, and the panel below leaf upto too when
+  // panel_done (all earlier panels are).
+  auto hand_over = [&](int64_t upto, bool panel_done) -> ff_status {
     FF_HIP(hipEventRecord(s.ev_leaf, ms));
     FF_HIP(hipStreamWaitEvent(s.istream, s.ev_leaf, 0));
-    if ((rc = inverse_nodes_ending(h, s, 0, d, k, s.istream)) != FF_OK) return rc;
-    if (rest == 0) break;
-    // the panel L_ik = A_ik Li_kk^T, in place (128-row tiles: each workgroup
-    // reads its rows before it writes them)
-    float* Pk = s.L + (o + bk) * d + o;
-    g.A = Pk; g.B = s.Li + o * d + o; g.C = Pk; g.M = rest; g.N = bk; g.K = bk;
-    g.transA = 0; g.transB = 1; g.alpha = 1.f; g.beta = 0.f; g.flags = kKHiCol; g.tile = 128;
-    FF_HIP(launch_gemm_f32(g, 1, ms));
-    g.tile = 0;
-    const int64_t b1 = std::min<int64_t>(kLeaf, rest);
-    // the next column block now (after the helper's update of it from panel k - 1),
-    // before the helper is released, so that it runs alone
-    if (k > 0) FF_HIP(hipStreamWaitEvent(ms, s.hjoin, 0));
-    g.A = Pk; g.B = Pk; g.C = s.L + (o + bk) * d + (o + bk); g.M = rest; g.N = b1; g.K = bk;
-    g.transA = 0; g.transB = 1; g.alpha = -1.f; g.beta = 1.f; g.flags = kCLower;
-    FF_HIP(launch_gemm_f32(g, 1, ms));
-    // rest of the trailing update on the helper: columns beyond the next block
-    if (rest > b1) {
-      FF_HIP(hipEventRecord(s.hfork, ms));
-      FF_HIP(hipStreamWaitEvent(s.helper, s.hfork, 0));
+    for (int64_t j = handed; j <= upto; ++j) {
+      ff_status r2 = inverse_p2_ending(h, s, 0, d, j, s.istream);
+      if (r2 != FF_OK) return r2;
+      if (j + 1 < nb && (panel_done || j < upto)) {
+        r2 = inverse_p1_split(h, s, 0, d, j, s.istream);
+        if (r2 != FF_OK) return r2;
+      }
     }
-    if (rest > b1) {
-      const int64_t q = o + bk + b1;
-      g.A = Pk + b1 * d; g.B = Pk + b1 * d; g.C = s.L + q * d + q;
-      g.M = rest - b1; g.N = rest - b1; g.K = bk;
-      g.transA = 0; g.transB = 1; g.alpha = -1.f; g.beta = 1.f; g.flags = kCLower;
-      FF_HIP(launch_gemm_f32(g, 1, s.helper));
-      FF_HIP(hipEventRecord(s.hjoin, s.helper));
-    }
+    handed = upto + 1;
+    return FF_OK;
+  };
+  for (int64_t k = 0; k + 1 < nb; ++k) {
+    const int64_t o = k * kLeaf, rest = d - o - kLeaf;
+    // the panel L_ik = A_ik Li_kk^T, in place
+    FF_HIP(launch_panel_solve(s.L + (o + kLeaf) * d + o, s.Li + o * d + o, d, rest, h->st, ms));
+    if ((k + 1) % kInvEvery == 0 && (rc = hand_over(k, true)) != FF_OK) return rc;
+    // diagonal block k + 1 and the trailing update of panel k
+    FF_HIP(launch_chol_step(s.L, s.Li, d, o, s.slots, iteration, s.code, h->st, ms));
   }
+  if ((rc = hand_over(nb - 1, false)) != FF_OK) return rc;
   FF_HIP(hipEventRecord(s.ev_inv, s.istream));
   FF_HIP(hipStreamWaitEvent(ms, s.ev_inv, 0));
   return FF_OK;
@@ -1209,12 +1232,6 @@ ff_status ff_destroy(ff_handle h) {
     hipEventDestroy(h->join);
   }
   for (Side* sd : {&h->A, &h->B}) {
-    if (sd->helper != nullptr) {
-      hipStreamSynchronize(sd->helper);
-      hipStreamDestroy(sd->helper);
-      hipEventDestroy(sd->hfork);
-      hipEventDestroy(sd->hjoin);
-    }
     if (sd->istream != nullptr) {
       hipStreamSynchronize(sd->istream);
       hipStreamDestroy(sd->istream);

@@ -274,6 +274,7 @@ hipError_t launch_gemm_f32(const GemmF32& p, int batch, hipStream_t s) {
                             (p.ksplit > 1 ? p.ksplit : batch);
   GemmF32 q = p;
   if (!segmented) q.kseg = 0;  // plain k axis: the kernels skip the segment arithmetic
+  if (p.tile == 64) return launch_tiles<64>(q, batch, vec, s);
   if (p.tile == 128 || big_tiles >= 256) return launch_tiles<128>(q, batch, vec, s);
   return launch_tiles<64>(q, batch, vec, s);
 }

@@ -65,8 +65,9 @@ struct GemmF32 {
   int64_t segA, segB;
   int ksplit;          // > 1: grid z splits k, C += z * sC, beta ignored
   const int* st;
-  int tile;            // 0: chosen by size; 128: 128 x 128 tiles (a workgroup reads all of
-                       // its rows of op(A) before it writes, so C may alias A when N <= 128)
+  int tile;            // 0: chosen by size; 64: 64 x 64 tiles; 128: 128 x 128 tiles (a
+                       // workgroup reads all of its rows of op(A) before it writes, so C
+                       // may alias A when N <= 128)
 };
 // C = alpha * op(A) op(B) + beta * C on the fp32 matrix cores (64 x 64 tiles).
 hipError_t launch_gemm_f32(const GemmF32& p, int batch, hipStream_t s);
@@ -87,6 +88,23 @@ constexpr int kLeaf = 128;  // diagonal block factorised inside one workgroup
 hipError_t launch_chol_leaf(const float* Lblk, float* Liblk, int64_t ld, int b, int64_t pivot_base,
                             double* logdet, int slot, int iteration, int side, int* st,
                             hipStream_t s, float* Lout = nullptr);
+
+// One step of the right-looking blocked factorisation of the dim x dim
+// matrix L (row-major, lower triangle; L^-1 blocks into Li).  With ok >= 0
+// the panel columns [ok, ok + 128) already hold L (rows below ok + 128):
+// diagonal block d0 = ok + 128 gets the panel's update and is factored and
+// inverted as by launch_chol_leaf (pivots d0.., log-determinant share into
+// logdet[d0 / 128], factor written in place), and the panel's update is
+// applied to every other 128 x 128 block of the trailing lower triangle by up
+// to kStepWorkers further workgroups.  ok = -128: block 0 only.
+constexpr int kStepWorkers = 255;
+// Panel of the blocked factorisation, in place: P (rows x 128, leading
+// dimension ld) <- P Xkk^T with Xkk the 128 x 128 inverse of the diagonal
+// block (lower, zeros above; leading dimension ld).
+hipError_t launch_panel_solve(float* P, const float* Xkk, int64_t ld, int64_t rows, const int* st,
+                              hipStream_t s);
+hipError_t launch_chol_step(float* L, float* Li, int64_t dim, int64_t ok, double* logdet,
+                            int iteration, int side, int* st, hipStream_t s);
 
 // out[s][r][c] (rows_p x cols_p) from G[s] (m x n): copy (transpose = 0,
 // rows_p >= m, cols_p >= n) or transpose (transpose = 1, rows_p >= n,
