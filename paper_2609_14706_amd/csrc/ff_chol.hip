@@ -384,19 +384,18 @@ union StepLDS {
   TrailLDS trail;
 };
 
-// One step of the blocked factorisation after panel k (columns ok..ok+127)
-// has been solved: workgroup 0 factors and inverts the next diagonal block
-// (d0 = ok + 128) after applying the panel's update to it; workgroups
-// 1..gridDim.x-1 apply the panel's update A_ij -= L_ik L_jk^T to every other
-// 128 x 128 block of the trailing lower triangle (block rows >= block
-// columns >= d0 / 128, the diagonal block excluded), round robin.  With
-// ok < 0 there is no panel yet: the kernel factors block 0 only.
+// One step of the blocked factorisation: workgroup 0 factors and inverts
+// the diagonal block at d0, after applying to it the update of the panel in
+// columns ok..ok+127 (already holding L) when ok >= 0; workgroups
+// 1..gridDim.x-1 apply that panel's update A_ij -= L_i,ok L_j,ok^T to every
+// other 128 x 128 block of the trailing lower triangle at or below d0 whose
+// block column starts before jend (the diagonal block excluded), round robin
+// over block columns then rows.
 __global__ __launch_bounds__(256) void k_chol_step(float* __restrict__ L, float* __restrict__ Li,
-                                                   int64_t dim, int64_t ok, double* logdet,
-                                                   int iteration, int side, int* st) {
+                                                   int64_t dim, int64_t d0, int64_t ok, int64_t jend,
+                                                   double* logdet, int iteration, int side, int* st) {
   if (ff_halted(st)) return;
   __shared__ StepLDS sm;
-  const int64_t d0 = ok + NB;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   if (blockIdx.x == 0) {
     const int b = (int)min<int64_t>(NB, dim - d0);
@@ -405,14 +404,17 @@ __global__ __launch_bounds__(256) void k_chol_step(float* __restrict__ L, float*
               st, Akk, ok >= 0 ? L + d0 * dim + ok : nullptr);
     return;
   }
-  const int64_t T = (dim - d0 + NB - 1) / NB;  // trailing blocks per side
-  const int64_t ntiles = T * (T + 1) / 2 - 1;
+  const int64_t R = (dim - d0 + NB - 1) / NB;   // block rows at or below d0
+  const int64_t T = (jend - d0 + NB - 1) / NB;  // block columns updated
+  // tiles: block column bj < T holds block rows bj..R-1; skip (0, 0)
+  const int64_t ntiles = T * R - T * (T - 1) / 2 - 1;
   for (int64_t t = blockIdx.x - 1; t < ntiles; t += gridDim.x - 1) {
-    // lower-triangle index t + 1 (index 0 is the diagonal block) -> (bi >= bj)
-    const int64_t u = t + 1;
-    int64_t bi = 0;
-    while ((bi + 1) * (bi + 2) / 2 <= u) ++bi;
-    const int64_t bj = u - bi * (bi + 1) / 2;
+    int64_t u = t + 1, bj = 0;
+    while (u >= R - bj) {
+      u -= R - bj;
+      ++bj;
+    }
+    const int64_t bi = bj + u;
     const int64_t i0 = d0 + bi * NB, j0 = d0 + bj * NB;
     load_rows(sm.trail.a, L, dim, i0, ok, dim, tid);
     if (bi != bj) load_rows(sm.trail.b, L, dim, j0, ok, dim, tid);
@@ -507,15 +509,19 @@ hipError_t launch_chol_leaf(const float* Lblk, float* Liblk, int64_t ld, int b, 
   return hipGetLastError();
 }
 
-hipError_t launch_chol_step(float* L, float* Li, int64_t dim, int64_t ok, double* logdet,
-                            int iteration, int side, int* st, hipStream_t s) {
-  if (dim < 1 || ok < -kLeaf || ok % kLeaf != 0 || ok + kLeaf >= dim) return hipErrorInvalidValue;
-  const int64_t d0 = ok + kLeaf;
-  const int64_t T = (dim - d0 + kLeaf - 1) / kLeaf;
-  const int64_t ntiles = ok < 0 ? 0 : T * (T + 1) / 2 - 1;
+hipError_t launch_chol_step(float* L, float* Li, int64_t dim, int64_t d0, int64_t ok, int64_t jend,
+                            double* logdet, int iteration, int side, int* st, hipStream_t s) {
+  if (dim < 1 || d0 < 0 || d0 >= dim || d0 % kLeaf != 0) return hipErrorInvalidValue;
+  if (ok >= 0 && (ok % kLeaf != 0 || ok + kLeaf > d0 || jend <= d0 || jend > dim))
+    return hipErrorInvalidValue;
+  int64_t ntiles = 0;
+  if (ok >= 0) {
+    const int64_t R = (dim - d0 + kLeaf - 1) / kLeaf, T = (jend - d0 + kLeaf - 1) / kLeaf;
+    ntiles = T * R - T * (T - 1) / 2 - 1;
+  }
   const int64_t grid = 1 + std::min<int64_t>(ntiles, kStepWorkers);
-  hipLaunchKernelGGL(k_chol_step, dim3((uint32_t)grid), dim3(256), 0, s, L, Li, dim, ok, logdet,
-                     iteration, side, st);
+  hipLaunchKernelGGL(k_chol_step, dim3((uint32_t)grid), dim3(256), 0, s, L, Li, dim, d0,
+                     ok >= 0 ? ok : (int64_t)-1, jend, logdet, iteration, side, st);
   return hipGetLastError();
 }
 

@@ -297,8 +297,8 @@ ff_status side_streams(Side& s) {
 // stream st, in two products: P1, T^T = (L21 Li11)^T, parked in the node's
 // block above the diagonal of s.L, needs the left half done (its inverse and
 // the panels below it); P2, Li21 = -Li22 T, needs the right half's inverse
-// too.  64 x 64 tiles: with one operand triangular, 128 x 128 tiles leave a
-// few long workgroups to finish alone.
+// too.  64 x 64 tiles below 2048 rows: with one operand triangular, 128 x 128
+// tiles leave a few long workgroups to finish alone.
 struct TreeNode {
   int64_t hh, r;
   float *L21, *Li11, *Li21, *Li22, *Tt;
@@ -318,19 +318,19 @@ TreeNode tree_node(Side& s, int64_t o, int64_t sz) {
   return t;
 }
 
-GemmF32 tree_gemm(ff_handle_s* h, Side& s) {
+GemmF32 tree_gemm(ff_handle_s* h, Side& s, const TreeNode& t) {
   GemmF32 g{};
+  g.tile = t.hh < 2048 ? 64 : 0;
   g.lda = g.ldb = g.ldc = s.dim;
   g.kseg = INT64_MAX / 4;
   g.ksplit = 1;
   g.st = h->st;
-  g.tile = 64;
   return g;
 }
 
 ff_status inverse_p1(ff_handle_s* h, Side& s, int64_t o, int64_t sz, hipStream_t st) {
   const TreeNode t = tree_node(s, o, sz);
-  GemmF32 g = tree_gemm(h, s);
+  GemmF32 g = tree_gemm(h, s, t);
   // T^T = (L21 Li11)^T = Li11^T L21^T  (hh x r)
   g.A = t.Li11; g.B = t.L21; g.C = t.Tt; g.M = t.hh; g.N = t.r; g.K = t.hh;
   g.transA = 1; g.transB = 1; g.alpha = 1.f; g.beta = 0.f; g.flags = kKLoRow;
@@ -340,7 +340,7 @@ ff_status inverse_p1(ff_handle_s* h, Side& s, int64_t o, int64_t sz, hipStream_t
 
 ff_status inverse_p2(ff_handle_s* h, Side& s, int64_t o, int64_t sz, hipStream_t st) {
   const TreeNode t = tree_node(s, o, sz);
-  GemmF32 g = tree_gemm(h, s);
+  GemmF32 g = tree_gemm(h, s, t);
   // Li21 = -Li22 T
   g.A = t.Li22; g.B = t.Tt; g.C = t.Li21; g.M = t.r; g.N = t.hh; g.K = t.r;
   g.transA = 0; g.transB = 1; g.alpha = -1.f; g.beta = 0.f; g.flags = kKHiRow;
@@ -384,23 +384,29 @@ ff_status inverse_p1_split(ff_handle_s* h, Side& s, int64_t o, int64_t sz, int64
 // panel's update to the rest of the trailing lower triangle.  (Trailing
 // updates on a second stream, overlapping the diagonal blocks, delayed the
 // small kernels on the critical path instead: concurrent kernels share the
-// CUs.)  The off-diagonal blocks of L^-1 are built on a second stream from
-// the binary tree of leaves, each node's first product as soon as its left
-// half and its panels are done, its second when its last leaf is; the work
-// is handed over every kInvEvery panels (an event on the main stream costs a
-// few microseconds there).  The upper triangle of s.L is scratch.
+// CUs.)  Factors wider than kTwoLevel go in outer panels of kOuter columns:
+// the steps update only the outer panel's columns, and one large product
+// applies the outer panel's rank-kOuter update to the rest (rank-128 updates
+// of a large matrix are bound by its reads and writes).  The off-diagonal
+// blocks of L^-1 are built on a second stream from the binary tree of
+// leaves, each node's first product as soon as its left half and its panels
+// are done, its second when its last leaf is; the work is handed over every
+// kInvEvery panels (an event on the main stream costs a few microseconds
+// there).  The upper triangle of s.L is scratch.
 constexpr int64_t kInvEvery = 4;
+constexpr int64_t kTwoLevel = 6144;
+constexpr int64_t kOuter = 1024;
 
 ff_status chol_blocked(ff_handle_s* h, Side& s, int iteration) {
   ff_status rc = side_streams(s);
   if (rc != FF_OK) return rc;
   const int64_t d = s.dim;
   const int64_t nb = (d + kLeaf - 1) / kLeaf;
+  const int64_t outer = d > kTwoLevel ? kOuter : nb * kLeaf;
   hipStream_t ms = h->stream;
   // the inverse stream starts after the work already on the main stream
   FF_HIP(hipEventRecord(s.ev_leaf, ms));
   FF_HIP(hipStreamWaitEvent(s.istream, s.ev_leaf, 0));
-  FF_HIP(launch_chol_step(s.L, s.Li, d, -kLeaf, s.slots, iteration, s.code, h->st, ms));
   int64_t handed = 0;  // leaves whose inverse products are enqueued
   // Leaves [handed, upto] are done, and the panel below leaf upto too when
   // panel_done (all earlier panels are).
@@ -418,13 +424,31 @@ ff_status chol_blocked(ff_handle_s* h, Side& s, int iteration) {
     handed = upto + 1;
     return FF_OK;
   };
-  for (int64_t k = 0; k + 1 < nb; ++k) {
-    const int64_t o = k * kLeaf, rest = d - o - kLeaf;
-    // the panel L_ik = A_ik Li_kk^T, in place
-    FF_HIP(launch_panel_solve(s.L + (o + kLeaf) * d + o, s.Li + o * d + o, d, rest, h->st, ms));
-    if ((k + 1) % kInvEvery == 0 && (rc = hand_over(k, true)) != FF_OK) return rc;
-    // diagonal block k + 1 and the trailing update of panel k
-    FF_HIP(launch_chol_step(s.L, s.Li, d, o, s.slots, iteration, s.code, h->st, ms));
+  for (int64_t p = 0; p < d; p += outer) {
+    const int64_t pe = std::min(p + outer, d);
+    // the outer panel's first diagonal block has every earlier update
+    FF_HIP(launch_chol_step(s.L, s.Li, d, p, -1, 0, s.slots, iteration, s.code, h->st, ms));
+    for (int64_t o = p; o + kLeaf < pe || (o + kLeaf < d && o + kLeaf == pe); o += kLeaf) {
+      const int64_t k = o / kLeaf, rest = d - o - kLeaf;
+      // the panel L_ik = A_ik Li_kk^T, in place
+      FF_HIP(launch_panel_solve(s.L + (o + kLeaf) * d + o, s.Li + o * d + o, d, rest, h->st, ms));
+      if ((k + 1) % kInvEvery == 0 && (rc = hand_over(k, true)) != FF_OK) return rc;
+      if (o + kLeaf == pe) break;  // the last panel of the outer panel
+      // diagonal block k + 1 and the panel's update of the outer panel's columns
+      FF_HIP(launch_chol_step(s.L, s.Li, d, o + kLeaf, o, pe, s.slots, iteration, s.code, h->st, ms));
+    }
+    if (pe < d) {
+      // A_22 -= L_21 L_21^T over the outer panel's columns
+      GemmF32 g{};
+      g.lda = g.ldb = g.ldc = d;
+      g.kseg = INT64_MAX / 4;
+      g.ksplit = 1;
+      g.st = h->st;
+      g.A = s.L + pe * d + p; g.B = g.A; g.C = s.L + pe * d + pe;
+      g.M = d - pe; g.N = d - pe; g.K = pe - p;
+      g.transA = 0; g.transB = 1; g.alpha = -1.f; g.beta = 1.f; g.flags = kCLower;
+      FF_HIP(launch_gemm_f32(g, 1, ms));
+    }
   }
   if ((rc = hand_over(nb - 1, false)) != FF_OK) return rc;
   FF_HIP(hipEventRecord(s.ev_inv, s.istream));

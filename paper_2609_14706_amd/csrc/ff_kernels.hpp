@@ -90,21 +90,22 @@ hipError_t launch_chol_leaf(const float* Lblk, float* Liblk, int64_t ld, int b, 
                             hipStream_t s, float* Lout = nullptr);
 
 // One step of the right-looking blocked factorisation of the dim x dim
-// matrix L (row-major, lower triangle; L^-1 blocks into Li).  With ok >= 0
-// the panel columns [ok, ok + 128) already hold L (rows below ok + 128):
-// diagonal block d0 = ok + 128 gets the panel's update and is factored and
-// inverted as by launch_chol_leaf (pivots d0.., log-determinant share into
-// logdet[d0 / 128], factor written in place), and the panel's update is
-// applied to every other 128 x 128 block of the trailing lower triangle by up
-// to kStepWorkers further workgroups.  ok = -128: block 0 only.
+// matrix L (row-major, lower triangle; L^-1 blocks into Li): the diagonal
+// block at d0 (a multiple of 128) is factored and inverted as by
+// launch_chol_leaf (pivots d0.., log-determinant share into logdet[d0 / 128],
+// factor written in place), after the update of panel ok (columns
+// [ok, ok + 128), already holding L below ok + 128) when ok >= 0; that panel's
+// update is also applied to every other 128 x 128 block of the trailing lower
+// triangle at or below d0 with block column below jend, by up to
+// kStepWorkers further workgroups.  ok < 0: the diagonal block only.
 constexpr int kStepWorkers = 255;
 // Panel of the blocked factorisation, in place: P (rows x 128, leading
 // dimension ld) <- P Xkk^T with Xkk the 128 x 128 inverse of the diagonal
 // block (lower, zeros above; leading dimension ld).
 hipError_t launch_panel_solve(float* P, const float* Xkk, int64_t ld, int64_t rows, const int* st,
                               hipStream_t s);
-hipError_t launch_chol_step(float* L, float* Li, int64_t dim, int64_t ok, double* logdet,
-                            int iteration, int side, int* st, hipStream_t s);
+hipError_t launch_chol_step(float* L, float* Li, int64_t dim, int64_t d0, int64_t ok, int64_t jend,
+                            double* logdet, int iteration, int side, int* st, hipStream_t s);
 
 // out[s][r][c] (rows_p x cols_p) from G[s] (m x n): copy (transpose = 0,
 // rows_p >= m, cols_p >= n) or transpose (transpose = 1, rows_p >= n,

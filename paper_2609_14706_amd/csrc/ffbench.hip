@@ -1,6 +1,6 @@
 // ffbench: native driver of the C ABI for timing and hardware-counter runs.
 //
-//   ffbench [m n N iters dtype(bf16|f32)]        (default 4096 4096 128 10 bf16)
+//   ffbench [m n N iters dtype(bf16|f32) damping]   (default 4096 4096 128 10 bf16 0)
 //
 // Before the job it runs one plain device-to-device copy of 1 GiB, a
 // reference of known size for scaling the FETCH_SIZE / WRITE_SIZE counters.
@@ -48,6 +48,8 @@ int main(int argc, char** argv) {
   if (argc > 3) N = atoll(argv[3]);
   if (argc > 4) iters = atoi(argv[4]);
   if (argc > 5) bf16 = strcmp(argv[5], "f32") != 0;
+  double damping = 0.0;
+  if (argc > 6) damping = atof(argv[6]);
   const size_t elem = bf16 ? 2 : 4;
   void* G = nullptr;
   CHECK(hipMalloc(&G, (size_t)N * m * n * elem));
@@ -65,6 +67,7 @@ int main(int argc, char** argv) {
   cfg.stream = s;
   cfg.order = FF_ORDER_B_FIRST;
   cfg.whiten_split = 1;
+  cfg.damping = damping;
   size_t ws = 0;
   if (ff_workspace_size(&cfg, &ws) != FF_OK) {
     fprintf(stderr, "ff_workspace_size: %s\n", ff_last_error());
