@@ -30,7 +30,7 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2609_14706_amd", "csrc", "ff_gemm_bf16.hi
 
 def recorded_traffic(kernel: str, workload: str):
     """HBM bytes per launch of `kernel` from the committed counter summary, or
-    None when it was taken for another kernel/workload or the kernel source
+    None when none was taken for that kernel/workload or the kernel source
     has changed since."""
     import hashlib
     if workload != "attn-4096x4096-N128" or not os.path.exists(TRAFFIC_FILE):
@@ -41,9 +41,12 @@ def recorded_traffic(kernel: str, workload: str):
             k, v = line.strip().split("=", 1)
             kv[k] = v
     src = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
-    if kv.get("traffic_kernel") != kernel or kv.get("traffic_source_sha256") != src:
+    key = f"traffic_{kernel}_bytes_per_launch"
+    if key not in kv or kv.get("traffic_source_sha256") != src:
         return None
-    return int(kv["traffic_bytes_per_launch"])
+    return int(kv[key])
+
+
 PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 
 
@@ -339,8 +342,12 @@ def main():
         roofline["traffic"] = recorded_traffic(roofline["kernel"], w.name)
     flipflop = args.estimator == "flipflop"
     if flipflop:
-        metric = (METRIC if not tokens else
-                  f"flip-flop iter/s + TFLOP/s, per-token form, m={w.m} n={w.n} T={w.T}")
+        if tokens:
+            metric = f"flip-flop iter/s + TFLOP/s, per-token form, m={w.m} n={w.n} T={w.T}"
+        elif w.name == "attn-4096x4096-N128":
+            metric = METRIC
+        else:
+            metric = f"flip-flop iter/s + TFLOP/s (% bf16 MFMA peak), m={w.m}, n={w.n}, N={N}"
     else:
         metric = (f"{args.estimator} estimator iter/s, m={w.m} n={w.n} " +
                   (f"T={w.T}" if tokens else f"N={N}"))

@@ -165,6 +165,29 @@ def test_kron_apply_matches_oracle(gpu):
     assert np.linalg.norm(Yi - refi) / np.linalg.norm(refi) < 1e-4
 
 
+@pytest.mark.parametrize("m,n,tol", [(300, 1000, 1e-5), (64, 6600, 1e-5)])
+def test_kron_apply_inverse_blocked_factorisation(gpu, m, n, tol):
+    """The inverse application at widths that take the blocked factorisation
+    (1000: eight 128-column panels with a ragged last block; 6600: outer
+    panels of 1024 columns and a ragged last outer panel), against fp64
+    solves with the same start factors."""
+    import torch
+    import paper_2609_14706_amd as ffe
+    rng = np.random.default_rng(12)
+    QA, QB = synth.haar_orthogonal(n, rng), synth.haar_orthogonal(m, rng)
+    A0 = ((QA * np.geomspace(2.0, 0.2, n)) @ QA.T).astype(np.float32)
+    B0 = ((QB * np.geomspace(4.0, 0.5, m)) @ QB.T).astype(np.float32)
+    G = rng.standard_normal((1, m, n)).astype(np.float32)
+    f = ffe.FlipFlop(to_device(G, gpu), A0=torch.from_numpy(A0), B0=torch.from_numpy(B0))
+    X = rng.standard_normal((2, m, n)).astype(np.float32)
+    Yi = f.kron_apply(torch.from_numpy(X), inverse=True).double().cpu().numpy()
+    f.close()
+    refi = oracle.kron_apply(A0.astype(np.float64), B0.astype(np.float64), X, inverse=True)
+    err = np.linalg.norm(Yi - refi) / np.linalg.norm(refi)
+    print(f"m={m} n={n}: inverse application rel err {err:.2e}")
+    assert err < tol
+
+
 # --------------------------------------------------------- failure handling
 
 def test_rank_deficient_samples_report_not_spd(gpu):
