@@ -264,6 +264,9 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
+    if args.gpus == 1 and not args.no_cpu_baseline:
+        import oracle  # noqa: F401  (its set-up starts a child process: before the GPU is in use)
+
     if args.workload.startswith("quant"):
         return main_quant(args)
 

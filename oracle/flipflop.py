@@ -39,9 +39,14 @@ import contextlib
 
 import numpy as np
 import scipy.linalg as sla
-from threadpoolctl import threadpool_limits
+from threadpoolctl import threadpool_info, threadpool_limits
 
 LOG_2PI = float(np.log(2.0 * np.pi))
+
+# threadpoolctl finds the C library once per process, by running `ldconfig` in
+# a child process.  Do it when the oracle is imported, so that it never has to
+# start a child process later, from a process that already drives a GPU.
+threadpool_info()
 
 
 def blas_threads(m, n):

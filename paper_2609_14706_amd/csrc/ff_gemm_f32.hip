@@ -19,6 +19,8 @@ namespace ff {
 namespace {
 
 constexpr int LDPMAX = 128 + 4;
+// k range per workgroup above which products use two-level accumulation
+constexpr int64_t kDeepK = 16384;
 
 // k per LDS slice: 32 for 128 x 128 tiles, 64 for 64 x 64 tiles (the small
 // products of the factorisation are latency bound: fewer, larger slices).
@@ -93,7 +95,9 @@ struct TileLDS {
 
 // acc += op(A)[i0.., klo..khi) op(B)[klo..khi), j0..) for one BT x BT tile
 // (each wave a (BT/2) x (BT/2) quadrant of MT x MT 32 x 32 matrix-core tiles).
-template <int BT, bool AK, bool BKM, bool FAST>
+// DEEP: two-level accumulation (see below), for long k ranges only: its
+// second set of accumulators halves the waves a CU can hold.
+template <int BT, bool AK, bool BKM, bool FAST, bool DEEP>
 __device__ __forceinline__ void tile_product(const GemmF32& p, const float* A, const float* B,
                                              int64_t i0, int64_t j0, int64_t klo, int64_t khi,
                                              TileLDS<BT>& sm, f32x16 (&acc)[BT / 64][BT / 64]) {
@@ -128,22 +132,35 @@ __device__ __forceinline__ void tile_product(const GemmF32& p, const float* A, c
       lb.load(B, p.ldb, j0, p.N, k0 + BK, khi, p.kseg, p.segB, tid);
     }
     __builtin_amdgcn_sched_barrier(0);
+    // operands of k-step s + 1 are read while the products of step s run
+    float fa[2][MT], fb[2][MT];
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+      fa[0][t] = sm.a[cur][lane >> 5][wm * (BT / 2) + t * 32 + (lane & 31)];
+      fb[0][t] = sm.b[cur][lane >> 5][wn * (BT / 2) + t * 32 + (lane & 31)];
+    }
 #pragma unroll
     for (int s = 0; s < BK / 2; ++s) {
-      const int kr = 2 * s + (lane >> 5);
-      float fa[MT], fb[MT];
+      if (s + 1 < BK / 2) {
+        const int kr = 2 * (s + 1) + (lane >> 5);
 #pragma unroll
-      for (int t = 0; t < MT; ++t) {
-        fa[t] = sm.a[cur][kr][wm * (BT / 2) + t * 32 + (lane & 31)];
-        fb[t] = sm.b[cur][kr][wn * (BT / 2) + t * 32 + (lane & 31)];
+        for (int t = 0; t < MT; ++t) {
+          fa[(s + 1) & 1][t] = sm.a[cur][kr][wm * (BT / 2) + t * 32 + (lane & 31)];
+          fb[(s + 1) & 1][t] = sm.b[cur][kr][wn * (BT / 2) + t * 32 + (lane & 31)];
+        }
       }
+      __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of the products
 #pragma unroll
       for (int a = 0; a < MT; ++a)
 #pragma unroll
-        for (int b = 0; b < MT; ++b)
-          loc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[a], fb[b], loc[a][b], 0, 0, 0);
+        for (int b = 0; b < MT; ++b) {
+          if constexpr (DEEP)
+            loc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[s & 1][a], fb[s & 1][b], loc[a][b], 0, 0, 0);
+          else
+            acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[s & 1][a], fb[s & 1][b], acc[a][b], 0, 0, 0);
+        }
     }
-    if (++cnt == CHUNK || !more) {
+    if (DEEP && (++cnt == CHUNK || !more)) {
 #pragma unroll
       for (int a = 0; a < MT; ++a)
 #pragma unroll
@@ -164,7 +181,7 @@ __device__ __forceinline__ void tile_product(const GemmF32& p, const float* A, c
   }
 }
 
-template <int BT, int TA, int TBT, bool VEC>
+template <int BT, int TA, int TBT, bool VEC, bool DEEP>
 __global__ __launch_bounds__(256) void k_gemm_f32(GemmF32 p) {
   constexpr int MT = BT / 64, BK = slice_k<BT>();
   if (ff_halted(p.st)) return;
@@ -201,8 +218,8 @@ __global__ __launch_bounds__(256) void k_gemm_f32(GemmF32 p) {
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
   if (klo < khi) {
     const bool fast = VEC && i0 + BT <= p.M && j0 + BT <= p.N && (khi - klo) % BK == 0;
-    if (fast) tile_product<BT, TA == 0, TBT != 0, VEC>(p, A, B, i0, j0, klo, khi, sm, acc);
-    else tile_product<BT, TA == 0, TBT != 0, false>(p, A, B, i0, j0, klo, khi, sm, acc);
+    if (fast) tile_product<BT, TA == 0, TBT != 0, VEC, DEEP>(p, A, B, i0, j0, klo, khi, sm, acc);
+    else tile_product<BT, TA == 0, TBT != 0, false, DEEP>(p, A, B, i0, j0, klo, khi, sm, acc);
   }
   const bool lower = (p.flags & kCLower) != 0;
   const bool use_beta = p.ksplit <= 1 && p.beta != 0.0f;
@@ -247,16 +264,30 @@ hipError_t launch_tiles(const GemmF32& p, int batch, bool vec, hipStream_t s) {
   const int gz = p.ksplit > 1 ? p.ksplit : batch;
   if (gx > 0x7fffffff || gy > 65535 || gz > 65535) return hipErrorInvalidValue;
   const dim3 grid((uint32_t)gx, (uint32_t)gy, (uint32_t)gz);
-  const int sel = (p.transA ? 1 : 0) | (p.transB ? 2 : 0) | (vec ? 4 : 0);
+  // two-level accumulation when a workgroup's k range is long (the stacked samples)
+  const int64_t kwg = p.ksplit > 1 ? (p.K + p.ksplit - 1) / p.ksplit : p.K;
+  const bool deep = kwg > kDeepK;
+  const int sel = (p.transA ? 1 : 0) | (p.transB ? 2 : 0) | (vec ? 4 : 0) | (deep ? 8 : 0);
   switch (sel) {
-    case 0: hipLaunchKernelGGL((k_gemm_f32<BT, 0, 0, false>), grid, dim3(256), 0, s, p); break;
-    case 1: hipLaunchKernelGGL((k_gemm_f32<BT, 1, 0, false>), grid, dim3(256), 0, s, p); break;
-    case 2: hipLaunchKernelGGL((k_gemm_f32<BT, 0, 1, false>), grid, dim3(256), 0, s, p); break;
-    case 3: hipLaunchKernelGGL((k_gemm_f32<BT, 1, 1, false>), grid, dim3(256), 0, s, p); break;
-    case 4: hipLaunchKernelGGL((k_gemm_f32<BT, 0, 0, true>), grid, dim3(256), 0, s, p); break;
-    case 5: hipLaunchKernelGGL((k_gemm_f32<BT, 1, 0, true>), grid, dim3(256), 0, s, p); break;
-    case 6: hipLaunchKernelGGL((k_gemm_f32<BT, 0, 1, true>), grid, dim3(256), 0, s, p); break;
-    default: hipLaunchKernelGGL((k_gemm_f32<BT, 1, 1, true>), grid, dim3(256), 0, s, p); break;
+#define FF_GEMM_CASE(c, ta, tb, v, dp) \
+    case c: hipLaunchKernelGGL((k_gemm_f32<BT, ta, tb, v, dp>), grid, dim3(256), 0, s, p); break;
+    FF_GEMM_CASE(0, 0, 0, false, false)
+    FF_GEMM_CASE(1, 1, 0, false, false)
+    FF_GEMM_CASE(2, 0, 1, false, false)
+    FF_GEMM_CASE(3, 1, 1, false, false)
+    FF_GEMM_CASE(4, 0, 0, true, false)
+    FF_GEMM_CASE(5, 1, 0, true, false)
+    FF_GEMM_CASE(6, 0, 1, true, false)
+    FF_GEMM_CASE(7, 1, 1, true, false)
+    FF_GEMM_CASE(8, 0, 0, false, true)
+    FF_GEMM_CASE(9, 1, 0, false, true)
+    FF_GEMM_CASE(10, 0, 1, false, true)
+    FF_GEMM_CASE(11, 1, 1, false, true)
+    FF_GEMM_CASE(12, 0, 0, true, true)
+    FF_GEMM_CASE(13, 1, 0, true, true)
+    FF_GEMM_CASE(14, 0, 1, true, true)
+    default: hipLaunchKernelGGL((k_gemm_f32<BT, 1, 1, true, true>), grid, dim3(256), 0, s, p); break;
+#undef FF_GEMM_CASE
   }
   return hipGetLastError();
 }
