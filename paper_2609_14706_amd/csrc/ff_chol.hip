@@ -324,18 +324,43 @@ __device__ __forceinline__ void leaf_body(LeafLDS& sm, const float* Lblk, float*
     // A -= Lpre Lpre^T (Lpre staged in X, cleared again afterwards)
     load_rows(sm.X, Lpre, ld, 0, 0, b, tid);
     __syncthreads();
-    f32x16 u[2][2];
-    quad_product(sm.X, sm.X, wave, lane, u);
+    // only the 10 lower 32 x 32 tiles (ti >= tj): tiles w, w + 4, w + 8 of
+    // (0,0) (1,0) (1,1) (2,0) (2,1) (2,2) (3,0) (3,1) (3,2) (3,3) on wave w
+    {
+      const int li = lane & 31, lk = lane >> 5;
+      const int nt = wave < 2 ? 3 : 2;
+      int ti[3], tj[3];
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+      for (int q = 0; q < 3; ++q) {
+        const int t = min(wave + 4 * q, 9);
+        ti[q] = t < 1 ? 0 : t < 3 ? 1 : t < 6 ? 2 : 3;
+        tj[q] = t - ti[q] * (ti[q] + 1) / 2;
+      }
+      f32x16 u[3];
 #pragma unroll
-      for (int c = 0; c < 2; ++c)
+      for (int q = 0; q < 3; ++q)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int i = quad_row(wave, a, r, lane), jj = quad_col(wave, c, lane);
-          if (jj <= i) sm.S[i][jj] -= u[a][c][r];
+        for (int r = 0; r < 16; ++r) u[q][r] = 0.0f;
+#pragma unroll 4
+      for (int k = 0; k < NB; k += 2) {
+#pragma unroll
+        for (int q = 0; q < 3; ++q)
+          if (q < nt)
+            u[q] = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.X[ti[q] * 32 + li][k + lk],
+                                                        sm.X[tj[q] * 32 + li][k + lk], u[q], 0, 0, 0);
+      }
+#pragma unroll
+      for (int q = 0; q < 3; ++q)
+        if (q < nt) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int i = ti[q] * 32 + 8 * (r >> 2) + 4 * lk + (r & 3), jj = tj[q] * 32 + li;
+            if (jj <= i) sm.S[i][jj] -= u[q][r];
+          }
         }
+    }
     __syncthreads();
+
     for (int i = tid >> 7; i < NB; i += 2) sm.X[i][tid & (NB - 1)] = 0.0f;
     __syncthreads();
   }
@@ -477,23 +502,31 @@ __global__ __launch_bounds__(256) void k_panel_solve(float* __restrict__ P, cons
     for (int i = i0; i < NB; i += 2) sm.x[i][j] = Xkk[(int64_t)i * ld + j];
   }
   __syncthreads();
-  // out(i, j) = sum_k a[i][k] x[j][k], k <= j (x lower triangular)
-  const int li = lane & 31, lk = lane >> 5, j0 = wave * 32;
+  // out(i, j) = sum_k a[i][k] x[j][k], k <= j (x lower triangular): column
+  // block c needs k < 32 (c + 1).  Wave w takes row half w % 2 and column
+  // blocks 3 and 0 (waves 0, 1) or 2 and 1 (waves 2, 3): 160 k each.
+  const int li = lane & 31, lk = lane >> 5;
+  const int h = wave & 1, cA = wave < 2 ? 3 : 2, cB = 3 - cA;
   f32x16 acc0, acc1;
 #pragma unroll
   for (int r = 0; r < 16; ++r) acc0[r] = acc1[r] = 0.0f;
 #pragma unroll 4
-  for (int k = 0; k < j0 + 32; k += 2) {
-    const float xb = sm.x[j0 + li][k + lk];
-    acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.a[li][k + lk], xb, acc0, 0, 0, 0);
-    acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.a[32 + li][k + lk], xb, acc1, 0, 0, 0);
+  for (int k = 0; k < 32 * (cB + 1); k += 2) {
+    const float av = sm.a[h * 32 + li][k + lk];
+    acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(av, sm.x[cA * 32 + li][k + lk], acc0, 0, 0, 0);
+    acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(av, sm.x[cB * 32 + li][k + lk], acc1, 0, 0, 0);
   }
+#pragma unroll 4
+  for (int k = 32 * (cB + 1); k < 32 * (cA + 1); k += 2)
+    acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.a[h * 32 + li][k + lk], sm.x[cA * 32 + li][k + lk], acc0,
+                                                0, 0, 0);
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
-    const int i = 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-    const int64_t g0 = r0 + i, g1 = r0 + 32 + i;
-    if (g0 < rows) P[g0 * ld + j0 + li] = acc0[r];
-    if (g1 < rows) P[g1 * ld + j0 + li] = acc1[r];
+    const int64_t g = r0 + h * 32 + 8 * (r >> 2) + 4 * lk + (r & 3);
+    if (g < rows) {
+      P[g * ld + cA * 32 + li] = acc0[r];
+      P[g * ld + cB * 32 + li] = acc1[r];
+    }
   }
 }
 

@@ -185,7 +185,19 @@ template <int BT, int TA, int TBT, bool VEC, bool DEEP>
 __global__ __launch_bounds__(256) void k_gemm_f32(GemmF32 p) {
   constexpr int MT = BT / 64, BK = slice_k<BT>();
   if (ff_halted(p.st)) return;
-  const int64_t i0 = (int64_t)blockIdx.x * BT, j0 = (int64_t)blockIdx.y * BT;
+  // With a triangular operand the k range, hence the work, of a tile grows
+  // along one tile index: walk the tiles with that index slowest and from the
+  // long end, so that the longest workgroups start first.
+  int64_t bx = blockIdx.x, by = blockIdx.y;
+  if (p.flags & (kKHiRow | kKLoRow)) {
+    const int64_t lin = bx + (int64_t)gridDim.x * by;
+    bx = lin / gridDim.y;
+    by = lin % gridDim.y;
+    if (p.flags & kKHiRow) bx = gridDim.x - 1 - bx;
+  } else if (p.flags & (kKHiCol | kKLoCol)) {
+    if (p.flags & kKHiCol) by = gridDim.y - 1 - by;
+  }
+  const int64_t i0 = bx * BT, j0 = by * BT;
   if ((p.flags & kCLower) && j0 > i0 + BT - 1) return;
   const float* A = p.A;
   const float* B = p.B;
