@@ -270,8 +270,11 @@ __device__ __forceinline__ void load_rows(float (*T)[SP], const float* M, int64_
   }
 }
 
-// Cholesky + inverse of one diagonal block by one workgroup (see
-// launch_chol_leaf).  Lpre (optional): the block row of the last panel to
+// Cholesky + inverse of one diagonal block of size b <= 128 by one
+// workgroup: reads the lower triangle of Lblk (ld), writes the block of L^-1
+// (lower, zeros above) to Liblk and, when Lout is not null, L itself over the
+// block; sum(log diag L) into logdet[slot]; on a non-positive or NaN pivot
+// sets st = {iteration, side, pivot_base + j} and returns.  Lpre (optional): the block row of the last panel to
 // the left (b rows x 128, leading dimension ld), whose update
 // A -= Lpre Lpre^T is applied to the block first.
 __device__ __forceinline__ void leaf_body(LeafLDS& sm, const float* Lblk, float* __restrict__ Liblk,
@@ -387,15 +390,6 @@ __device__ __forceinline__ void leaf_body(LeafLDS& sm, const float* Lblk, float*
       for (int i = i0; i < b; i += 2) Lout[(int64_t)i * ld + j] = j <= i ? sm.S[i][j] : 0.0f;
     }
   }
-}
-
-__global__ __launch_bounds__(256) void k_chol_leaf(const float* Lblk, float* __restrict__ Liblk,
-                                                   int64_t ld, int b, int64_t pivot_base,
-                                                   double* logdet, int slot, int iteration,
-                                                   int side, int* st, float* Lout) {
-  if (ff_halted(st)) return;
-  __shared__ LeafLDS sm;
-  leaf_body(sm, Lblk, Liblk, ld, b, pivot_base, logdet, slot, iteration, side, st, Lout, nullptr);
 }
 
 // Trailing-update tile of a right-looking step: the two 128-row blocks of
@@ -531,16 +525,6 @@ __global__ __launch_bounds__(256) void k_panel_solve(float* __restrict__ P, cons
 }
 
 }  // namespace
-
-hipError_t launch_chol_leaf(const float* Lblk, float* Liblk, int64_t ld, int b, int64_t pivot_base,
-                            double* logdet, int slot, int iteration, int side, int* st,
-                            hipStream_t s, float* Lout) {
-  if (b < 1 || b > kLeaf || ld < b) return hipErrorInvalidValue;
-  if (Lout != nullptr && Lout != Lblk) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_chol_leaf, dim3(1), dim3(256), 0, s, Lblk, Liblk, ld, b, pivot_base, logdet,
-                     slot, iteration, side, st, Lout);
-  return hipGetLastError();
-}
 
 hipError_t launch_chol_step(float* L, float* Li, int64_t dim, int64_t d0, int64_t ok, int64_t jend,
                             double* logdet, int iteration, int side, int* st, hipStream_t s) {

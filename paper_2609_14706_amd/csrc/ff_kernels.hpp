@@ -80,20 +80,12 @@ hipError_t launch_reduce_rowmajor(const float* P, int splits, int64_t dim_p, flo
 // ------------------------------------------------------ factorisation / misc
 constexpr int kLeaf = 128;  // diagonal block factorised inside one workgroup
 
-// Cholesky + inverse of a diagonal block of size b <= kLeaf.  Reads the lower
-// triangle of Lblk (ld), writes Li block (lower, zeros above), writes
-// sum(log diag L) to logdet[slot]; on a non-positive/NaN pivot sets
-// st = {iteration, side, pivot_base + j}.  Lout (null, or equal to Lblk):
-// the factor L is also written over the block (lower, zeros above).
-hipError_t launch_chol_leaf(const float* Lblk, float* Liblk, int64_t ld, int b, int64_t pivot_base,
-                            double* logdet, int slot, int iteration, int side, int* st,
-                            hipStream_t s, float* Lout = nullptr);
-
 // One step of the right-looking blocked factorisation of the dim x dim
 // matrix L (row-major, lower triangle; L^-1 blocks into Li): the diagonal
-// block at d0 (a multiple of 128) is factored and inverted as by
-// launch_chol_leaf (pivots d0.., log-determinant share into logdet[d0 / 128],
-// factor written in place), after the update of panel ok (columns
+// block at d0 (a multiple of 128) is factored and inverted in one workgroup
+// (pivots d0.., log-determinant share into logdet[d0 / 128], factor written
+// in place, L^-1 block into Li; a non-positive or NaN pivot sets the status
+// word to {iteration, side, pivot}), after the update of panel ok (columns
 // [ok, ok + 128), already holding L below ok + 128) when ok >= 0; that panel's
 // update is also applied to every other 128 x 128 block of the trailing lower
 // triangle at or below d0 with block column below jend, by up to
