@@ -43,6 +43,41 @@ __global__ __launch_bounds__(256) void k_pack(const T* __restrict__ G, T* __rest
   }
 }
 
+// Transposing bf16 copy with 8-byte accesses: out[s][r][c] = G[s][c][r] (r < n,
+// c < m), zero padding; a 64 x 64 tile per workgroup, rows of 16 four-element
+// chunks.  Requires n % 4 == 0 and cols_p % 4 == 0 (the caller checks).
+__global__ __launch_bounds__(256) void k_pack_t16(const bf16_t* __restrict__ G, bf16_t* __restrict__ out,
+                                                  int64_t m, int64_t n, int64_t rows_p, int64_t cols_p) {
+  __shared__ bf16_t tile[64][72];
+  const int64_t s = blockIdx.z;
+  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+  const bf16_t* g = G + s * m * n;
+  bf16_t* o = out + s * rows_p * cols_p;
+  const int tid = threadIdx.x, q = tid & 15, y0 = tid >> 4;
+  // source rows c0.. (m side), 4 consecutive source columns r0 + 4 q .. (n side)
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int y = y0 + 16 * t;
+    const int64_t sr = c0 + y, sc = r0 + 4 * q;
+    uint2 v = {0u, 0u};
+    if (sr < m && sc < n) v = *reinterpret_cast<const uint2*>(g + sr * n + sc);
+    *reinterpret_cast<uint2*>(&tile[y][4 * q]) = v;
+  }
+  __syncthreads();
+  // output rows r0.. , 4 consecutive output columns c0 + 4 q ..
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int y = y0 + 16 * t;
+    const int64_t r = r0 + y, c = c0 + 4 * q;
+    if (r < rows_p && c < cols_p) {
+      const uint32_t a = tile[4 * q][y], b = tile[4 * q + 1][y], d = tile[4 * q + 2][y],
+                     e = tile[4 * q + 3][y];
+      const uint2 v = {a | (b << 16), d | (e << 16)};
+      *reinterpret_cast<uint2*>(o + r * cols_p + c) = v;
+    }
+  }
+}
+
 // ------------------------------------------- rank-one (per-token) weights
 // w[r] = sum_j v(r, j) over cols entries of row r (square = 0: v = P[r][j];
 // square = 1: v = P[r][j]^2), one wave per row, fixed reduction order.
@@ -273,7 +308,11 @@ hipError_t launch_pack(const void* G, void* out, int64_t N, int64_t m, int64_t n
   if (transpose ? (rows_p < n || cols_p < m) : (rows_p < m || cols_p < n))
     return hipErrorInvalidValue;
   dim3 grid((uint32_t)((cols_p + 63) / 64), (uint32_t)((rows_p + 63) / 64), (uint32_t)N);
-  if (elem_bytes == 2)
+  if (elem_bytes == 2 && transpose && n % 4 == 0 && cols_p % 4 == 0 &&
+      (reinterpret_cast<uintptr_t>(G) & 7) == 0 && (reinterpret_cast<uintptr_t>(out) & 7) == 0) {
+    hipLaunchKernelGGL(k_pack_t16, grid, dim3(256), 0, s, (const bf16_t*)G, (bf16_t*)out, m, n,
+                       rows_p, cols_p);
+  } else if (elem_bytes == 2)
     hipLaunchKernelGGL(k_pack<bf16_t>, grid, dim3(256), 0, s, (const bf16_t*)G, (bf16_t*)out, m, n,
                        rows_p, cols_p, transpose);
   else if (elem_bytes == 4)
