@@ -128,6 +128,48 @@ __global__ __launch_bounds__(256) void k_scale_transpose(const T* __restrict__ M
   }
 }
 
+// The same for bf16 with 8-byte accesses (four consecutive elements per
+// thread on both sides; the tile lies within one segment since 64 | seg).
+// Requires cols_p % 4 == 0.
+__global__ __launch_bounds__(256) void k_scale_transpose_16(const bf16_t* __restrict__ M,
+                                                            const float* __restrict__ w,
+                                                            int64_t rows_p, int64_t cols_p, int64_t seg,
+                                                            bf16_t* __restrict__ out, const int* st) {
+  if (ff_halted(st)) return;
+  __shared__ float tile[64][65];
+  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+  const int tid = threadIdx.x, q = tid & 15, y0 = tid >> 4;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int y = y0 + 16 * t;
+    const int64_t r = r0 + y, c = c0 + 4 * q;
+    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    if (r < rows_p && c < cols_p) {
+      const uint2 u = *reinterpret_cast<const uint2*>(M + r * cols_p + c);
+      const float sw = sqrtf(w[r]);
+      v[0] = sw * bf16_to_f32((bf16_t)(u.x & 0xffffu));
+      v[1] = sw * bf16_to_f32((bf16_t)(u.x >> 16));
+      v[2] = sw * bf16_to_f32((bf16_t)(u.y & 0xffffu));
+      v[3] = sw * bf16_to_f32((bf16_t)(u.y >> 16));
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) tile[y][4 * q + e] = v[e];
+  }
+  __syncthreads();
+  bf16_t* o = out + (r0 / seg) * cols_p * seg + (r0 % seg);
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int y = y0 + 16 * t;
+    const int64_t c = c0 + y, r = r0 + 4 * q;
+    if (c < cols_p && r < rows_p) {
+      const uint32_t a = f32_to_bf16(tile[4 * q][y]), b = f32_to_bf16(tile[4 * q + 1][y]),
+                     d = f32_to_bf16(tile[4 * q + 2][y]), e = f32_to_bf16(tile[4 * q + 3][y]);
+      const uint2 v = {a | (b << 16), d | (e << 16)};
+      *reinterpret_cast<uint2*>(o + c * seg + 4 * q) = v;
+    }
+  }
+}
+
 // --------------------------------------------------------- inverse convert
 template <typename T>
 __global__ __launch_bounds__(256) void k_convert_inverse(const float* __restrict__ Li, int64_t dim,
@@ -341,7 +383,11 @@ hipError_t launch_scale_transpose(const void* M, const float* w, int64_t rows_p,
   const int64_t gx = (cols_p + 63) / 64, gy = (rows_p + 63) / 64;
   if (gx > 0x7fffffff || gy > 65535) return hipErrorInvalidValue;
   const dim3 grid((uint32_t)gx, (uint32_t)gy);
-  if (elem_bytes == 2)
+  if (elem_bytes == 2 && cols_p % 4 == 0 && (reinterpret_cast<uintptr_t>(M) & 7) == 0 &&
+      (reinterpret_cast<uintptr_t>(out) & 7) == 0)
+    hipLaunchKernelGGL(k_scale_transpose_16, grid, dim3(256), 0, s, (const bf16_t*)M, w, rows_p,
+                       cols_p, seg, (bf16_t*)out, st);
+  else if (elem_bytes == 2)
     hipLaunchKernelGGL(k_scale_transpose<bf16_t>, grid, dim3(256), 0, s, (const bf16_t*)M, w,
                        rows_p, cols_p, seg, (bf16_t*)out, st);
   else if (elem_bytes == 4)
