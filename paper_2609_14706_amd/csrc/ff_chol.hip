@@ -283,14 +283,22 @@ __device__ __forceinline__ void leaf_body(LeafLDS& sm, const float* Lblk, float*
                                           const float* Lpre) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int j = tid & (NB - 1), i0 = tid >> 7;
+  bool pre_loaded = false;  // Lpre already staged in X
   if (b == NB && (ld & 3) == 0 && (reinterpret_cast<uintptr_t>(Lblk) & 15) == 0) {
     // full block: thread (r, q) moves float4 q of rows r, r + 8, ...; all
-    // sixteen loads are in flight before the first is used
+    // sixteen loads (thirty-two with the panel's block row) are in flight
+    // before the first is used
     const int q = tid & 31, r = tid >> 5;
-    float4 v[NB / 8];
+    const bool pre = Lpre != nullptr && (reinterpret_cast<uintptr_t>(Lpre) & 15) == 0;
+    float4 v[NB / 8], u[NB / 8];
 #pragma unroll
     for (int t = 0; t < NB / 8; ++t)
       v[t] = *reinterpret_cast<const float4*>(Lblk + (int64_t)(r + 8 * t) * ld + 4 * q);
+    if (pre) {
+#pragma unroll
+      for (int t = 0; t < NB / 8; ++t)
+        u[t] = *reinterpret_cast<const float4*>(Lpre + (int64_t)(r + 8 * t) * ld + 4 * q);
+    }
 #pragma unroll
     for (int t = 0; t < NB / 8; ++t) {
       const int i = r + 8 * t, c = 4 * q;
@@ -298,9 +306,17 @@ __device__ __forceinline__ void leaf_body(LeafLDS& sm, const float* Lblk, float*
       sm.S[i][c + 1] = c + 1 <= i ? v[t].y : 0.0f;
       sm.S[i][c + 2] = c + 2 <= i ? v[t].z : 0.0f;
       sm.S[i][c + 3] = c + 3 <= i ? v[t].w : 0.0f;
+      if (pre) {
+        sm.X[i][c + 0] = u[t].x;
+        sm.X[i][c + 1] = u[t].y;
+        sm.X[i][c + 2] = u[t].z;
+        sm.X[i][c + 3] = u[t].w;
+      } else {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) sm.X[i][c + e] = 0.0f;
+        for (int e = 0; e < 4; ++e) sm.X[i][c + e] = 0.0f;
+      }
     }
+    pre_loaded = pre;
   } else {
     // ragged block (b < 128), padded with the identity: thread (i0, j) moves
     // rows i0, i0 + 2, ... of column j, from clamped (always valid) addresses
@@ -325,8 +341,10 @@ __device__ __forceinline__ void leaf_body(LeafLDS& sm, const float* Lblk, float*
   __syncthreads();
   if (Lpre != nullptr) {
     // A -= Lpre Lpre^T (Lpre staged in X, cleared again afterwards)
-    load_rows(sm.X, Lpre, ld, 0, 0, b, tid);
-    __syncthreads();
+    if (!pre_loaded) {
+      load_rows(sm.X, Lpre, ld, 0, 0, b, tid);
+      __syncthreads();
+    }
     // only the 10 lower 32 x 32 tiles (ti >= tj): tiles w, w + 4, w + 8 of
     // (0,0) (1,0) (1,1) (2,0) (2,1) (2,2) (3,0) (3,1) (3,2) (3,3) on wave w
     {

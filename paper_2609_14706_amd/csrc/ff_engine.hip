@@ -393,7 +393,7 @@ ff_status inverse_p1_split(ff_handle_s* h, Side& s, int64_t o, int64_t sz, int64
 // are done, its second when its last leaf is; the work is handed over every
 // kInvEvery panels (an event on the main stream costs a few microseconds
 // there).  The upper triangle of s.L is scratch.
-constexpr int64_t kInvEvery = 4;
+constexpr int64_t kInvEvery = 8;
 constexpr int64_t kTwoLevel = 6144;
 constexpr int64_t kOuter = 1024;
 
