@@ -65,6 +65,21 @@ def test_frobenius_fp32_ragged(gpu, m, n, N):
     assert done == 3 and err < TOL_F32
 
 
+def test_frobenius_fp32_two_level_factorisation(gpu):
+    """A 6600-wide input factor: the factorisation that keeps the factor (its
+    reversed Cholesky factor is the whitening operand) runs in 1024-column
+    outer panels, the last one ragged.  With N m = 96 < n the update is
+    singular; the paper's damping makes it positive definite."""
+    rng = np.random.default_rng(6600)
+    m, n, N = 48, 6600, 2
+    G = (rng.standard_normal((N, m, n)) * np.linspace(0.5, 2.0, n)[None, None, :]).astype(np.float32)
+    A, B, ll, done = run(gpu, 2, G=G, estimator="frobenius", damping=0.1)
+    ref = oracle.frobenius(G, 2, damping=0.1)
+    err = oracle.kron_rel_error(A, B, ref.A, ref.B)
+    print(f"frobenius fp32 {m}x{n} N={N}: rel err {err:.3e}")
+    assert done == 2 and err < TOL_F32
+
+
 def test_frobenius_damping_and_order(gpu):
     import paper_2609_14706_amd as ffe
     d = synth.generate(synth.workload("tiny").scaled(m=48, n=80, N=40))
