@@ -252,6 +252,30 @@ def test_resume_and_bitwise_determinism(gpu):
     f2.close()
 
 
+@pytest.mark.parametrize("key,m,n,N", [("attn", 512, 768, 4), ("tiny", 64, 128, 32)])
+@pytest.mark.parametrize("order", ["B_FIRST", "A_FIRST"])
+def test_identity_start_is_exact(gpu, key, m, n, N, order):
+    """Without A0 / B0 the first half step skips the whitening by the inverse
+    factor of I and the factorisation of I; with the identity passed
+    explicitly both run.  A product with I is exact in every precision, so the
+    iterates must agree bitwise (bf16 and fp32 paths, both orders)."""
+    import torch
+    import paper_2609_14706_amd as ffe
+    d = synth.generate(small_workload(key, m=m, n=n, N=N))
+    G = to_device(d.G, gpu)
+    kw = {"A0": torch.eye(n)} if order == "B_FIRST" else {"B0": torch.eye(m)}
+    f1 = ffe.FlipFlop(G, order=order)
+    ll1 = f1.iterate(3)
+    A1, B1 = f1.factors()
+    f2 = ffe.FlipFlop(G, order=order, **kw)
+    ll2 = f2.iterate(3)
+    A2, B2 = f2.factors()
+    f1.close()
+    f2.close()
+    assert bool((A1 == A2).all()) and bool((B1 == B2).all())
+    assert ll1 == ll2
+
+
 # ------------------------------------------------------- mismatch objective
 
 def _spd(dim, rng, cond):
