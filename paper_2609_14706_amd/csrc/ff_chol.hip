@@ -1,11 +1,13 @@
-// Cholesky factorisation and inverse of one diagonal block (fp32).
+// Kernels of the blocked Cholesky factorisation and inverse (fp32).
 //
 // The factors' inverses enter every flip-flop update (Section 5: A^-1 and
 // B^-1 in the two half steps); the iteration whitens with the inverse of the
 // lower Cholesky factor, L^-1 (Section 2 notation: Cholesky(M) is the lower
-// L with positive diagonal and L L^T = M).  Blocks of up to 128 rows are
-// handled here by one workgroup; larger factors are assembled by the host's
-// blocked factorisation from these blocks and fp32 matrix-core products.
+// L with positive diagonal and L L^T = M).  The host factors right-looking
+// over 128-column panels with two kernels per panel: k_panel_solve (the
+// panel L_ik = A_ik L_kk^-T) and k_chol_step, in which one workgroup factors
+// and inverts the next 128 x 128 diagonal block while the others apply the
+// panel's update to the trailing lower triangle.
 //
 // Inside the block a recursion runs in LDS: for a block [[A11, .],
 // [A21, A22]] of size s (halves h = s/2)
