@@ -59,9 +59,11 @@ __device__ __forceinline__ float bcast(float v, int lane) {
 // column goes through LDS (sm.C[j][.], read back as uniform vectors) and is
 // applied one step later, off that path.  Row-lane entries above the
 // diagonal are never read for the lower triangle and are cleared at the end.
-// Returns the block-relative failing column or -1.
-__device__ __forceinline__ int base_block(LeafLDS& sm, int o, int lane) {
-  float v[BS], col[BS], nxt[BS];
+// base_factor leaves the lane's row of L or column of X in v (and L[r][r]
+// in diag) and returns the block-relative failing column or -1;
+// base_store writes them to S and X and the log-determinant share.
+__device__ __forceinline__ int base_factor(LeafLDS& sm, int o, int lane, float (&v)[BS], float& diag) {
+  float col[BS], nxt[BS];
   const int r = lane & 31;
   const bool rowlane = lane < BS;
 #pragma unroll
@@ -71,7 +73,7 @@ __device__ __forceinline__ int base_block(LeafLDS& sm, int o, int lane) {
     nxt[c] = 0.0f;
   }
   int bad = -1;
-  float diag = 1.0f;           // L[r][r] (row lanes)
+  diag = 1.0f;                 // L[r][r] (row lanes)
   float vp = 0.0f, lp = 0.0f;  // previous step's multiplier v[j-1] and L[j][j-1]
 #pragma unroll
   for (int j = 0; j < BS; ++j) {
@@ -104,6 +106,12 @@ __device__ __forceinline__ int base_block(LeafLDS& sm, int o, int lane) {
     vp = vj;
     lp = ln;
   }
+  return bad;
+}
+
+__device__ __forceinline__ void base_store(LeafLDS& sm, int o, int lane, const float (&v)[BS], float diag) {
+  const int r = lane & 31;
+  const bool rowlane = lane < BS;
 #pragma unroll
   for (int c = 0; c < BS; ++c) {
     if (rowlane) sm.S[o + r][o + c] = c <= r ? v[c] : 0.0f;
@@ -114,7 +122,6 @@ __device__ __forceinline__ int base_block(LeafLDS& sm, int o, int lane) {
 #pragma unroll
   for (int w = 16; w >= 1; w >>= 1) ls += __shfl_xor(ls, w, 32);
   if (lane == 0) sm.ldp[o / BS] = ls;
-  return bad;
 }
 
 // The products of a recursion level are h x h (h = 64 or 32) with k running
@@ -158,10 +165,26 @@ struct LevelTile {
   }
 };
 
+template <int NT>
+__device__ __forceinline__ void pre_update(LeafLDS& sm, int lane, int first, int stride);
+__device__ __forceinline__ void zero_upper(LeafLDS& sm, int tid);
+
 // Base block at (o, o) by wave 0; everyone waits.  Records the first failure.
-__device__ __forceinline__ void base_step(LeafLDS& sm, int o, int wave, int lane) {
+// pre: the first base block of a leaf whose update A -= P P^T (P staged in
+// X) has been applied to the tile (0, 0) only: waves 1..3 apply it to the
+// other nine lower tiles meanwhile, and the base block's own writes to X wait
+// until they have read P.
+__device__ __forceinline__ void base_step(LeafLDS& sm, int o, int wave, int lane, bool pre) {
+  float v[BS], diag = 1.0f;
+  int b = -1;
+  if (wave == 0) b = base_factor(sm, o, lane, v, diag);
+  else if (pre) pre_update<3>(sm, lane, wave, 3);
+  if (pre) {
+    __syncthreads();
+    zero_upper(sm, threadIdx.x);
+  }
   if (wave == 0) {
-    const int b = base_block(sm, o, lane);
+    base_store(sm, o, lane, v, diag);
     if (lane == 0 && b >= 0 && sm.bad < 0) sm.bad = o + b;
   }
   __syncthreads();
@@ -169,13 +192,13 @@ __device__ __forceinline__ void base_step(LeafLDS& sm, int o, int wave, int lane
 
 // Recursive cholinv of the block at (o, o) of size S (64 or 128, unrolled at
 // compile time); every wave takes every barrier.  Returns the failing column
-// or -1.
+// or -1.  pre: see base_step (passed on to the first base block).
 template <int S>
-__device__ __forceinline__ int cholinv_lds(LeafLDS& sm, int o, int wave, int lane) {
+__device__ __forceinline__ int cholinv_lds(LeafLDS& sm, int o, int wave, int lane, bool pre = false) {
   constexpr int h = S / 2;
   typedef LevelTile<h> LT;
-  if constexpr (h == BS) base_step(sm, o, wave, lane);
-  else cholinv_lds<h>(sm, o, wave, lane);
+  if constexpr (h == BS) base_step(sm, o, wave, lane, pre);
+  else cholinv_lds<h>(sm, o, wave, lane, pre);
   if (sm.bad >= 0) return sm.bad;
   const int o2 = o + h;
   const int oc = LT::col(wave, lane);
@@ -194,7 +217,7 @@ __device__ __forceinline__ int cholinv_lds(LeafLDS& sm, int o, int wave, int lan
     for (int r = 0; r < LT::NACC; ++r) sm.S[o2 + LT::row(wave, r, lane)][o2 + oc] -= u[r];
   }
   __syncthreads();
-  if constexpr (h == BS) base_step(sm, o2, wave, lane);
+  if constexpr (h == BS) base_step(sm, o2, wave, lane, false);
   else cholinv_lds<h>(sm, o2, wave, lane);
   if (sm.bad >= 0) return sm.bad;
   // Y = L21 X11 -> T;  X21 = -X22 Y
@@ -272,6 +295,82 @@ __device__ __forceinline__ void load_rows(float (*T)[SP], const float* M, int64_
   }
 }
 
+// A -= P P^T on the lower triangle of the block in S, with P (128 x 128)
+// staged in X, for NT of the ten lower 32 x 32 tiles (ti >= tj) in the
+// order (0,0) (1,0) (1,1) (2,0) (2,1) (2,2) (3,0) (3,1) (3,2) (3,3): tiles
+// first, first + stride, ...  The operands of eight k steps are read before
+// their products are issued.
+template <int NT>
+__device__ __forceinline__ void pre_update(LeafLDS& sm, int lane, int first, int stride) {
+  const int li = lane & 31, lk = lane >> 5;
+  const float* pa[NT];
+  const float* pb[NT];
+  int ti[NT], tj[NT];
+#pragma unroll
+  for (int q = 0; q < NT; ++q) {
+    const int t = first + stride * q;
+    ti[q] = t < 1 ? 0 : t < 3 ? 1 : t < 6 ? 2 : 3;
+    tj[q] = t - ti[q] * (ti[q] + 1) / 2;
+    pa[q] = &sm.X[ti[q] * 32 + li][lk];
+    pb[q] = &sm.X[tj[q] * 32 + li][lk];
+  }
+  f32x16 u[NT];
+#pragma unroll
+  for (int q = 0; q < NT; ++q)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) u[q][r] = 0.0f;
+#pragma unroll
+  for (int k = 0; k < NB; k += 16) {
+    float a[NT][8], b[NT][8];
+#pragma unroll
+    for (int q = 0; q < NT; ++q)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        a[q][e] = pa[q][k + 2 * e];
+        b[q][e] = pb[q][k + 2 * e];
+      }
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+#pragma unroll
+      for (int q = 0; q < NT; ++q) u[q] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[q][e], b[q][e], u[q], 0, 0, 0);
+  }
+  // all reads before the first write (entries above the diagonal of a
+  // diagonal tile are written back unchanged; no other wave touches the tile)
+  float sv[NT][16];
+#pragma unroll
+  for (int q = 0; q < NT; ++q)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sv[q][r] = sm.S[ti[q] * 32 + 8 * (r >> 2) + 4 * lk + (r & 3)][tj[q] * 32 + li];
+#pragma unroll
+  for (int q = 0; q < NT; ++q)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int i = ti[q] * 32 + 8 * (r >> 2) + 4 * lk + (r & 3), j = tj[q] * 32 + li;
+      sm.S[i][j] = j <= i ? sv[q][r] - u[q][r] : sv[q][r];
+    }
+}
+
+// The recursion reads X only where it has written it, except the blocks
+// above the diagonal inside X11 and X22 of the top level (the base blocks
+// write theirs in full): zero those two 32 x 32 blocks.
+__device__ __forceinline__ void zero_upper(LeafLDS& sm, int tid) {
+  const int r = tid >> 3, c = 4 * (tid & 7);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    sm.X[r][32 + c + e] = 0.0f;
+    sm.X[64 + r][96 + c + e] = 0.0f;
+  }
+}
+
+// Thread tid's share of a 128 x 128 block moved as float4: rows
+// row0 + 8 t (t < 16), columns col..col+3.  The 32 lanes of a half wave
+// cover 4 rows x 32 columns, so that with the odd LDS pitch their entries
+// fall in distinct banks, and each row's 128 bytes form one global segment.
+__device__ __forceinline__ void quad4_map(int tid, int& row0, int& col) {
+  row0 = ((tid >> 7) << 2) + ((tid >> 3) & 3);
+  col = 32 * ((tid >> 5) & 3) + 4 * (tid & 7);
+}
+
 // Cholesky + inverse of one diagonal block of size b <= 128 by one
 // workgroup: reads the lower triangle of Lblk (ld), writes the block of L^-1
 // (lower, zeros above) to Liblk and, when Lout is not null, L itself over the
@@ -287,23 +386,23 @@ __device__ __forceinline__ void leaf_body(LeafLDS& sm, const float* Lblk, float*
   const int j = tid & (NB - 1), i0 = tid >> 7;
   bool pre_loaded = false;  // Lpre already staged in X
   if (b == NB && (ld & 3) == 0 && (reinterpret_cast<uintptr_t>(Lblk) & 15) == 0) {
-    // full block: thread (r, q) moves float4 q of rows r, r + 8, ...; all
-    // sixteen loads (thirty-two with the panel's block row) are in flight
-    // before the first is used
-    const int q = tid & 31, r = tid >> 5;
+    // full block, float4 moves (quad4_map); all sixteen loads (thirty-two
+    // with the panel's block row) are in flight before the first is used
+    int r, c;
+    quad4_map(tid, r, c);
     const bool pre = Lpre != nullptr && (reinterpret_cast<uintptr_t>(Lpre) & 15) == 0;
     float4 v[NB / 8], u[NB / 8];
 #pragma unroll
     for (int t = 0; t < NB / 8; ++t)
-      v[t] = *reinterpret_cast<const float4*>(Lblk + (int64_t)(r + 8 * t) * ld + 4 * q);
+      v[t] = *reinterpret_cast<const float4*>(Lblk + (int64_t)(r + 8 * t) * ld + c);
     if (pre) {
 #pragma unroll
       for (int t = 0; t < NB / 8; ++t)
-        u[t] = *reinterpret_cast<const float4*>(Lpre + (int64_t)(r + 8 * t) * ld + 4 * q);
+        u[t] = *reinterpret_cast<const float4*>(Lpre + (int64_t)(r + 8 * t) * ld + c);
     }
 #pragma unroll
     for (int t = 0; t < NB / 8; ++t) {
-      const int i = r + 8 * t, c = 4 * q;
+      const int i = r + 8 * t;
       sm.S[i][c + 0] = c + 0 <= i ? v[t].x : 0.0f;
       sm.S[i][c + 1] = c + 1 <= i ? v[t].y : 0.0f;
       sm.S[i][c + 2] = c + 2 <= i ? v[t].z : 0.0f;
@@ -342,52 +441,16 @@ __device__ __forceinline__ void leaf_body(LeafLDS& sm, const float* Lblk, float*
   if (tid == 0) sm.bad = -1;
   __syncthreads();
   if (Lpre != nullptr) {
-    // A -= Lpre Lpre^T (Lpre staged in X, cleared again afterwards)
+    // A -= Lpre Lpre^T (Lpre staged in X)
     if (!pre_loaded) {
       load_rows(sm.X, Lpre, ld, 0, 0, b, tid);
       __syncthreads();
     }
-    // only the 10 lower 32 x 32 tiles (ti >= tj): tiles w, w + 4, w + 8 of
-    // (0,0) (1,0) (1,1) (2,0) (2,1) (2,2) (3,0) (3,1) (3,2) (3,3) on wave w
-    {
-      const int li = lane & 31, lk = lane >> 5;
-      const int nt = wave < 2 ? 3 : 2;
-      int ti[3], tj[3];
-#pragma unroll
-      for (int q = 0; q < 3; ++q) {
-        const int t = min(wave + 4 * q, 9);
-        ti[q] = t < 1 ? 0 : t < 3 ? 1 : t < 6 ? 2 : 3;
-        tj[q] = t - ti[q] * (ti[q] + 1) / 2;
-      }
-      f32x16 u[3];
-#pragma unroll
-      for (int q = 0; q < 3; ++q)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) u[q][r] = 0.0f;
-#pragma unroll 4
-      for (int k = 0; k < NB; k += 2) {
-#pragma unroll
-        for (int q = 0; q < 3; ++q)
-          if (q < nt)
-            u[q] = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.X[ti[q] * 32 + li][k + lk],
-                                                        sm.X[tj[q] * 32 + li][k + lk], u[q], 0, 0, 0);
-      }
-#pragma unroll
-      for (int q = 0; q < 3; ++q)
-        if (q < nt) {
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int i = ti[q] * 32 + 8 * (r >> 2) + 4 * lk + (r & 3), jj = tj[q] * 32 + li;
-            if (jj <= i) sm.S[i][jj] -= u[q][r];
-          }
-        }
-    }
-    __syncthreads();
-
-    for (int i = tid >> 7; i < NB; i += 2) sm.X[i][tid & (NB - 1)] = 0.0f;
+    // tile (0, 0) now, the other nine during the first base block
+    if (wave == 0) pre_update<1>(sm, lane, 0, 1);
     __syncthreads();
   }
-  const int bad = cholinv_lds<NB>(sm, 0, wave, lane);
+  const int bad = cholinv_lds<NB>(sm, 0, wave, lane, Lpre != nullptr);
   if (bad >= 0) {
     if (tid == 0) {
       st[1] = side;
@@ -402,7 +465,32 @@ __device__ __forceinline__ void leaf_body(LeafLDS& sm, const float* Lblk, float*
     for (int p = 0; p < NB / BS; ++p) s += sm.ldp[p];
     logdet[slot] = s;
   }
-  if (j < b) {
+  const bool vec_out = b == NB && (ld & 3) == 0 && (reinterpret_cast<uintptr_t>(Liblk) & 15) == 0 &&
+                       (reinterpret_cast<uintptr_t>(Lout) & 15) == 0;
+  if (vec_out) {
+    // float4 stores (quad4_map), lower triangle, zeros above
+    int r, c;
+    quad4_map(tid, r, c);
+    float4 w[NB / 8];
+#pragma unroll
+    for (int t = 0; t < NB / 8; ++t) {
+      const int i = r + 8 * t;
+      w[t] = make_float4(c + 0 <= i ? sm.X[i][c + 0] : 0.0f, c + 1 <= i ? sm.X[i][c + 1] : 0.0f,
+                         c + 2 <= i ? sm.X[i][c + 2] : 0.0f, c + 3 <= i ? sm.X[i][c + 3] : 0.0f);
+    }
+#pragma unroll
+    for (int t = 0; t < NB / 8; ++t) *reinterpret_cast<float4*>(Liblk + (int64_t)(r + 8 * t) * ld + c) = w[t];
+    if (Lout != nullptr) {  // the factor itself, over the block it was read from
+#pragma unroll
+      for (int t = 0; t < NB / 8; ++t) {
+        const int i = r + 8 * t;
+        w[t] = make_float4(c + 0 <= i ? sm.S[i][c + 0] : 0.0f, c + 1 <= i ? sm.S[i][c + 1] : 0.0f,
+                           c + 2 <= i ? sm.S[i][c + 2] : 0.0f, c + 3 <= i ? sm.S[i][c + 3] : 0.0f);
+      }
+#pragma unroll
+      for (int t = 0; t < NB / 8; ++t) *reinterpret_cast<float4*>(Lout + (int64_t)(r + 8 * t) * ld + c) = w[t];
+    }
+  } else if (j < b) {
 #pragma unroll 8
     for (int i = i0; i < b; i += 2) Liblk[(int64_t)i * ld + j] = j <= i ? sm.X[i][j] : 0.0f;
     if (Lout != nullptr) {  // the factor itself, over the block it was read from
@@ -458,6 +546,19 @@ __global__ __launch_bounds__(256) void k_chol_step(float* __restrict__ L, float*
     load_rows(sm.trail.a, L, dim, i0, ok, dim, tid);
     if (bi != bj) load_rows(sm.trail.b, L, dim, j0, ok, dim, tid);
     __syncthreads();
+    // this lane's 64 entries of the block, read (from clamped addresses)
+    // before the product so that their latency overlaps it
+    float cv[2][2][16];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int64_t i = min<int64_t>(i0 + quad_row(wave, a, r, lane), dim - 1);
+          const int64_t j = min<int64_t>(j0 + quad_col(wave, c, lane), dim - 1);
+          cv[a][c][r] = L[i * dim + j];
+        }
     f32x16 u4[2][2];
     quad_product(sm.trail.a, bi != bj ? sm.trail.b : sm.trail.a, wave, lane, u4);
 #pragma unroll
@@ -467,7 +568,7 @@ __global__ __launch_bounds__(256) void k_chol_step(float* __restrict__ L, float*
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int64_t i = i0 + quad_row(wave, a, r, lane), j = j0 + quad_col(wave, c, lane);
-          if (i < dim && j < dim && (bi != bj || j <= i)) L[i * dim + j] -= u4[a][c][r];
+          if (i < dim && j < dim && (bi != bj || j <= i)) L[i * dim + j] = cv[a][c][r] - u4[a][c][r];
         }
     __syncthreads();  // before the next tile's rows overwrite LDS
   }
