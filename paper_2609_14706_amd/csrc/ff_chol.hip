@@ -240,24 +240,36 @@ __device__ __forceinline__ int cholinv_lds(LeafLDS& sm, int o, int wave, int lan
 
 // 128 x 128 x 128 product of two LDS operands held as rows (pitch SP):
 // acc[a][b] = P[rows of tile a] Q[rows of tile b]^T over all 128 k, for the
-// 64 x 64 quadrant (wm, wn) of this wave (2 x 2 tiles of 32 x 32).
+// 64 x 64 quadrant (wm, wn) of this wave (2 x 2 tiles of 32 x 32).  The
+// operands of eight k steps are read before their products are issued.
 __device__ __forceinline__ void quad_product(const float (*P)[SP], const float (*Q)[SP], int wave,
                                              int lane, f32x16 (&acc)[2][2]) {
   const int wm = wave >> 1, wn = wave & 1, li = lane & 31, lk = lane >> 5;
+  const float* pp[2] = {&P[wm * 64 + li][lk], &P[wm * 64 + 32 + li][lk]};
+  const float* qq[2] = {&Q[wn * 64 + li][lk], &Q[wn * 64 + 32 + li][lk]};
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
     for (int c = 0; c < 2; ++c)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][c][r] = 0.0f;
-#pragma unroll 4
-  for (int k = 0; k < NB; k += 2) {
-    const float p0 = P[wm * 64 + li][k + lk], p1 = P[wm * 64 + 32 + li][k + lk];
-    const float q0 = Q[wn * 64 + li][k + lk], q1 = Q[wn * 64 + 32 + li][k + lk];
-    acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(p0, q0, acc[0][0], 0, 0, 0);
-    acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(p0, q1, acc[0][1], 0, 0, 0);
-    acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(p1, q0, acc[1][0], 0, 0, 0);
-    acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(p1, q1, acc[1][1], 0, 0, 0);
+#pragma unroll
+  for (int k = 0; k < NB; k += 16) {
+    float pv[2][8], qv[2][8];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        pv[t][e] = pp[t][k + 2 * e];
+        qv[t][e] = qq[t][k + 2 * e];
+      }
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+          acc[a][c] = __builtin_amdgcn_mfma_f32_32x32x2f32(pv[a][e], qv[c][e], acc[a][c], 0, 0, 0);
   }
 }
 // Quadrant-relative row / column of element r of this lane in tile (a, c).
@@ -583,6 +595,34 @@ struct PanelLDS {
   float x[NB][SP];
 };
 
+// Column blocks CA and CB (CB < CA) of row half h of the panel product:
+// acc0 over k < 32 (CA + 1), acc1 over k < 32 (CB + 1), with the operands of
+// eight k steps read before their products are issued.
+template <int CA, int CB>
+__device__ __forceinline__ void panel_tiles(const PanelLDS& sm, int h, int li, int lk, f32x16& acc0,
+                                            f32x16& acc1) {
+  const float* pa = &sm.a[h * 32 + li][lk];
+  const float* px = &sm.x[CA * 32 + li][lk];
+  const float* py = &sm.x[CB * 32 + li][lk];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc0[r] = acc1[r] = 0.0f;
+#pragma unroll
+  for (int k = 0; k < 32 * (CA + 1); k += 16) {
+    float av[8], xv[8], yv[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      av[e] = pa[k + 2 * e];
+      xv[e] = px[k + 2 * e];
+      if (k < 32 * (CB + 1)) yv[e] = py[k + 2 * e];
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(av[e], xv[e], acc0, 0, 0, 0);
+      if (k < 32 * (CB + 1)) acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(av[e], yv[e], acc1, 0, 0, 0);
+    }
+  }
+}
+
 __global__ __launch_bounds__(256) void k_panel_solve(float* __restrict__ P, const float* __restrict__ Xkk,
                                                      int64_t ld, int64_t rows, const int* st) {
   if (ff_halted(st)) return;
@@ -623,18 +663,8 @@ __global__ __launch_bounds__(256) void k_panel_solve(float* __restrict__ P, cons
   const int li = lane & 31, lk = lane >> 5;
   const int h = wave & 1, cA = wave < 2 ? 3 : 2, cB = 3 - cA;
   f32x16 acc0, acc1;
-#pragma unroll
-  for (int r = 0; r < 16; ++r) acc0[r] = acc1[r] = 0.0f;
-#pragma unroll 4
-  for (int k = 0; k < 32 * (cB + 1); k += 2) {
-    const float av = sm.a[h * 32 + li][k + lk];
-    acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(av, sm.x[cA * 32 + li][k + lk], acc0, 0, 0, 0);
-    acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(av, sm.x[cB * 32 + li][k + lk], acc1, 0, 0, 0);
-  }
-#pragma unroll 4
-  for (int k = 32 * (cB + 1); k < 32 * (cA + 1); k += 2)
-    acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.a[h * 32 + li][k + lk], sm.x[cA * 32 + li][k + lk], acc0,
-                                                0, 0, 0);
+  if (wave < 2) panel_tiles<3, 0>(sm, h, li, lk, acc0, acc1);
+  else panel_tiles<2, 1>(sm, h, li, lk, acc0, acc1);
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const int64_t g = r0 + h * 32 + 8 * (r >> 2) + 4 * lk + (r & 3);

@@ -392,7 +392,9 @@ ff_status inverse_p1_split(ff_handle_s* h, Side& s, int64_t o, int64_t sz, int64
 // leaves, each node's first product as soon as its left half and its panels
 // are done, its second when its last leaf is; the work is handed over every
 // kInvEvery panels (an event on the main stream costs a few microseconds
-// there).  The upper triangle of s.L is scratch.
+// there), and every second panel near the end, where what is still undone
+// after the last leaf is the factorisation's tail.  The upper triangle of
+// s.L is scratch.
 constexpr int64_t kInvEvery = 8;
 constexpr int64_t kTwoLevel = 6144;
 constexpr int64_t kOuter = 1024;
@@ -432,7 +434,10 @@ ff_status chol_blocked(ff_handle_s* h, Side& s, int iteration) {
       const int64_t k = o / kLeaf, rest = d - o - kLeaf;
       // the panel L_ik = A_ik Li_kk^T, in place
       FF_HIP(launch_panel_solve(s.L + (o + kLeaf) * d + o, s.Li + o * d + o, d, rest, h->st, ms));
-      if ((k + 1) % kInvEvery == 0 && (rc = hand_over(k, true)) != FF_OK) return rc;
+      // every kInvEvery panels, and every second one among the last
+      // kInvEvery (the last steps leave most CUs idle for the tree's products)
+      const bool tail = k + 1 + kInvEvery >= nb && (k + 1) % 2 == 0;
+      if (((k + 1) % kInvEvery == 0 || tail) && (rc = hand_over(k, true)) != FF_OK) return rc;
       if (o + kLeaf == pe) break;  // the last panel of the outer panel
       // diagonal block k + 1 and the panel's update of the outer panel's columns
       FF_HIP(launch_chol_step(s.L, s.Li, d, o + kLeaf, o, pe, s.slots, iteration, s.code, h->st, ms));
