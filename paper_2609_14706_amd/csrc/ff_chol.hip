@@ -39,7 +39,7 @@ struct LeafLDS {
   float S[NB][SP];  // A, overwritten by L (lower triangle)
   float X[NB][SP];  // L^-1
   float T[64][65];  // product scratch
-  double ldp[NB / BS];
+  float dg[NB];  // diagonal of L (log-determinant)
   int bad;
 };
 
@@ -61,7 +61,7 @@ __device__ __forceinline__ float bcast(float v, int lane) {
 // diagonal are never read for the lower triangle and are cleared at the end.
 // base_factor leaves the lane's row of L or column of X in v (and L[r][r]
 // in diag) and returns the block-relative failing column or -1;
-// base_store writes them to S and X and the log-determinant share.
+// base_store writes them to S and X and L[r][r] to dg.
 __device__ __forceinline__ int base_factor(LeafLDS& sm, int o, int lane, float (&v)[BS], float& diag) {
   float col[BS], nxt[BS];
   const int r = lane & 31;
@@ -117,11 +117,7 @@ __device__ __forceinline__ void base_store(LeafLDS& sm, int o, int lane, const f
     if (rowlane) sm.S[o + r][o + c] = c <= r ? v[c] : 0.0f;
     else sm.X[o + c][o + r] = v[c];
   }
-  // log-determinant share: sum of log L_jj over the block
-  double ls = rowlane ? log((double)diag) : 0.0;
-#pragma unroll
-  for (int w = 16; w >= 1; w >>= 1) ls += __shfl_xor(ls, w, 32);
-  if (lane == 0) sm.ldp[o / BS] = ls;
+  if (rowlane) sm.dg[o + r] = diag;
 }
 
 // The products of a recursion level are h x h (h = 64 or 32) with k running
@@ -472,11 +468,6 @@ __device__ __forceinline__ void leaf_body(LeafLDS& sm, const float* Lblk, float*
     }
     return;
   }
-  if (tid == 0) {
-    double s = 0.0;
-    for (int p = 0; p < NB / BS; ++p) s += sm.ldp[p];
-    logdet[slot] = s;
-  }
   const bool vec_out = b == NB && (ld & 3) == 0 && (reinterpret_cast<uintptr_t>(Liblk) & 15) == 0 &&
                        (reinterpret_cast<uintptr_t>(Lout) & 15) == 0;
   if (vec_out) {
@@ -509,6 +500,14 @@ __device__ __forceinline__ void leaf_body(LeafLDS& sm, const float* Lblk, float*
 #pragma unroll 8
       for (int i = i0; i < b; i += 2) Lout[(int64_t)i * ld + j] = j <= i ? sm.S[i][j] : 0.0f;
     }
+  }
+  // log-determinant share, sum of log L_jj over the block (kept off the
+  // pivots' path; ragged blocks are padded with unit pivots)
+  if (wave == 0) {
+    double ls = log((double)sm.dg[lane]) + log((double)sm.dg[lane + 64]);
+#pragma unroll
+    for (int w = 32; w >= 1; w >>= 1) ls += __shfl_xor(ls, w, 64);
+    if (lane == 0) logdet[slot] = ls;
   }
 }
 
