@@ -112,11 +112,12 @@ __device__ __forceinline__ int base_factor(LeafLDS& sm, int o, int lane, float (
 __device__ __forceinline__ void base_store(LeafLDS& sm, int o, int lane, const float (&v)[BS], float diag) {
   const int r = lane & 31;
   const bool rowlane = lane < BS;
+  // one store per entry for all lanes: row r of S (row lanes) or column r
+  // of X (column lanes)
+  float* dst = rowlane ? &sm.S[o + r][o] : &sm.X[o][o + r];
+  const int step = rowlane ? 1 : SP;
 #pragma unroll
-  for (int c = 0; c < BS; ++c) {
-    if (rowlane) sm.S[o + r][o + c] = c <= r ? v[c] : 0.0f;
-    else sm.X[o + c][o + r] = v[c];
-  }
+  for (int c = 0; c < BS; ++c) dst[c * step] = (rowlane && c > r) ? 0.0f : v[c];
   if (rowlane) sm.dg[o + r] = diag;
 }
 
