@@ -138,18 +138,30 @@ struct LevelTile {
     Acc acc;
 #pragma unroll
     for (int r = 0; r < NACC; ++r) acc[r] = 0.0f;
+    // the operands of eight k steps are read before their products are issued
     if constexpr (H == 64) {
       const int li = lane & 31, lk = lane >> 5;
-#pragma unroll 8
-      for (int k = 0; k < H; k += 2)
-        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(geta(ti * T + li, k + lk), getb(k + lk, tj * T + li),
-                                                   acc, 0, 0, 0);
+#pragma unroll
+      for (int k = 0; k < H; k += 16) {
+        float a[8], b[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          a[e] = geta(ti * T + li, k + 2 * e + lk);
+          b[e] = getb(k + 2 * e + lk, tj * T + li);
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], b[e], acc, 0, 0, 0);
+      }
     } else {
       const int li = lane & 15, lk = lane >> 4;
+      float a[H / 4], b[H / 4];
 #pragma unroll
-      for (int k = 0; k < H; k += 4)
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(geta(ti * T + li, k + lk), getb(k + lk, tj * T + li),
-                                                   acc, 0, 0, 0);
+      for (int e = 0; e < H / 4; ++e) {
+        a[e] = geta(ti * T + li, 4 * e + lk);
+        b[e] = getb(4 * e + lk, tj * T + li);
+      }
+#pragma unroll
+      for (int e = 0; e < H / 4; ++e) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[e], b[e], acc, 0, 0, 0);
     }
     return acc;
   }
