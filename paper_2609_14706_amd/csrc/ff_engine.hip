@@ -397,7 +397,7 @@ ff_status inverse_p1_split(ff_handle_s* h, Side& s, int64_t o, int64_t sz, int64
 // s.L is scratch.
 constexpr int64_t kInvEvery = 8;
 constexpr int64_t kTwoLevel = 6144;
-constexpr int64_t kOuter = 1024;
+constexpr int64_t kOuter = 2048;
 
 ff_status chol_blocked(ff_handle_s* h, Side& s, int iteration) {
   ff_status rc = side_streams(s);
