@@ -182,12 +182,19 @@ __device__ __forceinline__ void zero_upper(LeafLDS& sm, int tid);
 // pre: the first base block of a leaf whose update A -= P P^T (P staged in
 // X) has been applied to the tile (0, 0) only: waves 1..3 apply it to the
 // other nine lower tiles meanwhile, and the base block's own writes to X wait
-// until they have read P.
-__device__ __forceinline__ void base_step(LeafLDS& sm, int o, int wave, int lane, bool pre) {
+// until they have read P.  Otherwise waves 1..3 run side (thread index
+// 0..191 among them) meanwhile.
+struct NoSide {
+  __device__ void operator()(int) const {}
+};
+template <class Side = NoSide>
+__device__ __forceinline__ void base_step(LeafLDS& sm, int o, int wave, int lane, bool pre,
+                                          const Side& side = Side()) {
   float v[BS], diag = 1.0f;
   int b = -1;
   if (wave == 0) b = base_factor(sm, o, lane, v, diag);
   else if (pre) pre_update<3>(sm, lane, wave, 3);
+  else side((int)threadIdx.x - 64);
   if (pre) {
     __syncthreads();
     zero_upper(sm, threadIdx.x);
@@ -201,13 +208,15 @@ __device__ __forceinline__ void base_step(LeafLDS& sm, int o, int wave, int lane
 
 // Recursive cholinv of the block at (o, o) of size S (64 or 128, unrolled at
 // compile time); every wave takes every barrier.  Returns the failing column
-// or -1.  pre: see base_step (passed on to the first base block).
-template <int S>
-__device__ __forceinline__ int cholinv_lds(LeafLDS& sm, int o, int wave, int lane, bool pre = false) {
+// or -1.  pre, side: see base_step (passed on to the first base block);
+// side2: side work for the first base block of the second half.
+template <int S, class Side = NoSide, class Side2 = NoSide>
+__device__ __forceinline__ int cholinv_lds(LeafLDS& sm, int o, int wave, int lane, bool pre = false,
+                                           const Side& side = Side(), const Side2& side2 = Side2()) {
   constexpr int h = S / 2;
   typedef LevelTile<h> LT;
-  if constexpr (h == BS) base_step(sm, o, wave, lane, pre);
-  else cholinv_lds<h>(sm, o, wave, lane, pre);
+  if constexpr (h == BS) base_step(sm, o, wave, lane, pre, side);
+  else cholinv_lds<h>(sm, o, wave, lane, pre, side);
   if (sm.bad >= 0) return sm.bad;
   const int o2 = o + h;
   const int oc = LT::col(wave, lane);
@@ -226,8 +235,8 @@ __device__ __forceinline__ int cholinv_lds(LeafLDS& sm, int o, int wave, int lan
     for (int r = 0; r < LT::NACC; ++r) sm.S[o2 + LT::row(wave, r, lane)][o2 + oc] -= u[r];
   }
   __syncthreads();
-  if constexpr (h == BS) base_step(sm, o2, wave, lane, false);
-  else cholinv_lds<h>(sm, o2, wave, lane);
+  if constexpr (h == BS) base_step(sm, o2, wave, lane, false, side2);
+  else cholinv_lds<h>(sm, o2, wave, lane, false, side2);
   if (sm.bad >= 0) return sm.bad;
   // Y = L21 X11 -> T;  X21 = -X22 Y
   {
@@ -392,6 +401,27 @@ __device__ __forceinline__ void quad4_map(int tid, int& row0, int& col) {
   col = 32 * ((tid >> 5) & 3) + 4 * (tid & 7);
 }
 
+// 64 x 64 block of an LDS operand (from row r0, column c0) to dst (leading
+// dimension ld) as float4 moves; mode 0: as is, 1: lower triangle (zeros
+// above the block's diagonal), 2: zeros.  Thread t of STRIDE; the 32 lanes of
+// a half wave cover 4 rows x 32 columns (distinct banks, 128-byte segments).
+template <int STRIDE>
+__device__ __forceinline__ void store64(const float (*src)[SP], int r0, int c0, float* dst, int64_t ld,
+                                        int mode, int t) {
+#pragma unroll
+  for (int k = 0; k < (1024 + STRIDE - 1) / STRIDE; ++k) {
+    const int f = t + k * STRIDE;
+    if (f < 1024) {
+      const int r = 4 * (f >> 6) + ((f >> 3) & 3), c = 32 * ((f >> 5) & 1) + 4 * (f & 7);
+      float e[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        e[q] = (mode == 2 || (mode == 1 && c + q > r)) ? 0.0f : src[r0 + r][c0 + c + q];
+      *reinterpret_cast<float4*>(dst + (int64_t)r * ld + c) = make_float4(e[0], e[1], e[2], e[3]);
+    }
+  }
+}
+
 // Cholesky + inverse of one diagonal block of size b <= 128 by one
 // workgroup: reads the lower triangle of Lblk (ld), writes the block of L^-1
 // (lower, zeros above) to Liblk and, when Lout is not null, L itself over the
@@ -471,7 +501,22 @@ __device__ __forceinline__ void leaf_body(LeafLDS& sm, const float* Lblk, float*
     if (wave == 0) pre_update<1>(sm, lane, 0, 1);
     __syncthreads();
   }
-  const int bad = cholinv_lds<NB>(sm, 0, wave, lane, Lpre != nullptr);
+  const bool vec_out = b == NB && (ld & 3) == 0 && (reinterpret_cast<uintptr_t>(Liblk) & 15) == 0 &&
+                       (reinterpret_cast<uintptr_t>(Lout) & 15) == 0;
+  // While wave 0 factors the first base block of the second half, waves
+  // 1..3 store what is final by then: L11, L^-1 11, the zeros above them and
+  // L21.
+  auto early = [&](int t) {
+    if (!vec_out) return;
+    store64<192>(sm.X, 0, 0, Liblk, ld, 1, t);
+    store64<192>(sm.X, 0, 0, Liblk + 64, ld, 2, t);
+    if (Lout != nullptr) {
+      store64<192>(sm.S, 0, 0, Lout, ld, 1, t);
+      store64<192>(sm.S, 0, 0, Lout + 64, ld, 2, t);
+      store64<192>(sm.S, 64, 0, Lout + 64 * ld, ld, 0, t);
+    }
+  };
+  const int bad = cholinv_lds<NB>(sm, 0, wave, lane, Lpre != nullptr, NoSide(), early);
   if (bad >= 0) {
     if (tid == 0) {
       st[1] = side;
@@ -481,31 +526,11 @@ __device__ __forceinline__ void leaf_body(LeafLDS& sm, const float* Lblk, float*
     }
     return;
   }
-  const bool vec_out = b == NB && (ld & 3) == 0 && (reinterpret_cast<uintptr_t>(Liblk) & 15) == 0 &&
-                       (reinterpret_cast<uintptr_t>(Lout) & 15) == 0;
   if (vec_out) {
-    // float4 stores (quad4_map), lower triangle, zeros above
-    int r, c;
-    quad4_map(tid, r, c);
-    float4 w[NB / 8];
-#pragma unroll
-    for (int t = 0; t < NB / 8; ++t) {
-      const int i = r + 8 * t;
-      w[t] = make_float4(c + 0 <= i ? sm.X[i][c + 0] : 0.0f, c + 1 <= i ? sm.X[i][c + 1] : 0.0f,
-                         c + 2 <= i ? sm.X[i][c + 2] : 0.0f, c + 3 <= i ? sm.X[i][c + 3] : 0.0f);
-    }
-#pragma unroll
-    for (int t = 0; t < NB / 8; ++t) *reinterpret_cast<float4*>(Liblk + (int64_t)(r + 8 * t) * ld + c) = w[t];
-    if (Lout != nullptr) {  // the factor itself, over the block it was read from
-#pragma unroll
-      for (int t = 0; t < NB / 8; ++t) {
-        const int i = r + 8 * t;
-        w[t] = make_float4(c + 0 <= i ? sm.S[i][c + 0] : 0.0f, c + 1 <= i ? sm.S[i][c + 1] : 0.0f,
-                           c + 2 <= i ? sm.S[i][c + 2] : 0.0f, c + 3 <= i ? sm.S[i][c + 3] : 0.0f);
-      }
-#pragma unroll
-      for (int t = 0; t < NB / 8; ++t) *reinterpret_cast<float4*>(Lout + (int64_t)(r + 8 * t) * ld + c) = w[t];
-    }
+    // the rest: L22, L^-1 22 and L^-1 21
+    store64<256>(sm.X, 64, 64, Liblk + 64 * ld + 64, ld, 1, tid);
+    store64<256>(sm.X, 64, 0, Liblk + 64 * ld, ld, 0, tid);
+    if (Lout != nullptr) store64<256>(sm.S, 64, 64, Lout + 64 * ld + 64, ld, 1, tid);
   } else if (j < b) {
 #pragma unroll 8
     for (int i = i0; i < b; i += 2) Liblk[(int64_t)i * ld + j] = j <= i ? sm.X[i][j] : 0.0f;
