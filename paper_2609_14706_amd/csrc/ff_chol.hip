@@ -175,29 +175,44 @@ struct LevelTile {
 };
 
 template <int NT>
-__device__ __forceinline__ void pre_update(LeafLDS& sm, int lane, int first, int stride);
-__device__ __forceinline__ void zero_upper(LeafLDS& sm, int tid);
+__device__ __forceinline__ void pre_update(LeafLDS& sm, int lane, const int (&ts)[NT]);
 
 // Base block at (o, o) by wave 0; everyone waits.  Records the first failure.
-// pre: the first base block of a leaf whose update A -= P P^T (P staged in
-// X) has been applied to the tile (0, 0) only: waves 1..3 apply it to the
-// other nine lower tiles meanwhile, and the base block's own writes to X wait
-// until they have read P.  Otherwise waves 1..3 run side (thread index
+// A leaf whose update A -= P P^T (P staged in X) has been applied to the
+// lower 32 x 32 tile (0, 0) only gives the rest to waves 1..3 during its
+// first two base blocks: pre = 1 (the block at 0) the six tiles of block
+// rows 1..3 that read rows 0..63 of P, after which the block's own writes to
+// X (over P's first rows) may go ahead; pre = 2 (the block at 32) the three
+// tiles (2,2) (3,2) (3,3), which read only rows 64.. of P and are needed
+// from the second half on.  Otherwise waves 1..3 run side (thread index
 // 0..191 among them) meanwhile.
 struct NoSide {
   __device__ void operator()(int) const {}
 };
 template <class Side = NoSide>
-__device__ __forceinline__ void base_step(LeafLDS& sm, int o, int wave, int lane, bool pre,
+__device__ __forceinline__ void base_step(LeafLDS& sm, int o, int wave, int lane, int pre,
                                           const Side& side = Side()) {
   float v[BS], diag = 1.0f;
   int b = -1;
-  if (wave == 0) b = base_factor(sm, o, lane, v, diag);
-  else if (pre) pre_update<3>(sm, lane, wave, 3);
-  else side((int)threadIdx.x - 64);
-  if (pre) {
+  if (wave == 0) {
+    b = base_factor(sm, o, lane, v, diag);
+  } else if (pre == 1) {
+    const int ts[2] = {wave, wave == 1 ? 4 : wave + 4};  // (1,0) (2,1) | (1,1) (3,0) | (2,0) (3,1)
+    pre_update<2>(sm, lane, ts);
+  } else if (pre == 2) {
+    const int ts[1] = {wave == 1 ? 5 : wave + 6};  // (2,2) | (3,2) | (3,3)
+    pre_update<1>(sm, lane, ts);
+  } else {
+    side((int)threadIdx.x - 64);
+  }
+  if (pre == 1) {
     __syncthreads();
-    zero_upper(sm, threadIdx.x);
+    // the recursion reads X only where it has written it, except the block
+    // above the diagonal inside X11 (and X22, see leaf_body) of the top
+    // level: zero X[0:32][32:64]
+    const int r = threadIdx.x >> 3, c = 4 * (threadIdx.x & 7);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sm.X[r][32 + c + e] = 0.0f;
   }
   if (wave == 0) {
     base_store(sm, o, lane, v, diag);
@@ -208,10 +223,11 @@ __device__ __forceinline__ void base_step(LeafLDS& sm, int o, int wave, int lane
 
 // Recursive cholinv of the block at (o, o) of size S (64 or 128, unrolled at
 // compile time); every wave takes every barrier.  Returns the failing column
-// or -1.  pre, side: see base_step (passed on to the first base block);
-// side2: side work for the first base block of the second half.
+// or -1.  pre, side: see base_step (pre = 1 goes to the first base block,
+// pre = 2 to the second); side2: side work for the first base block of the
+// second half.
 template <int S, class Side = NoSide, class Side2 = NoSide>
-__device__ __forceinline__ int cholinv_lds(LeafLDS& sm, int o, int wave, int lane, bool pre = false,
+__device__ __forceinline__ int cholinv_lds(LeafLDS& sm, int o, int wave, int lane, int pre = 0,
                                            const Side& side = Side(), const Side2& side2 = Side2()) {
   constexpr int h = S / 2;
   typedef LevelTile<h> LT;
@@ -235,8 +251,8 @@ __device__ __forceinline__ int cholinv_lds(LeafLDS& sm, int o, int wave, int lan
     for (int r = 0; r < LT::NACC; ++r) sm.S[o2 + LT::row(wave, r, lane)][o2 + oc] -= u[r];
   }
   __syncthreads();
-  if constexpr (h == BS) base_step(sm, o2, wave, lane, false, side2);
-  else cholinv_lds<h>(sm, o2, wave, lane, false, side2);
+  if constexpr (h == BS) base_step(sm, o2, wave, lane, pre == 1 ? 2 : 0, side2);
+  else cholinv_lds<h>(sm, o2, wave, lane, 0, side2);
   if (sm.bad >= 0) return sm.bad;
   // Y = L21 X11 -> T;  X21 = -X22 Y
   {
@@ -326,19 +342,19 @@ __device__ __forceinline__ void load_rows(float (*T)[SP], const float* M, int64_
 }
 
 // A -= P P^T on the lower triangle of the block in S, with P (128 x 128)
-// staged in X, for NT of the ten lower 32 x 32 tiles (ti >= tj) in the
-// order (0,0) (1,0) (1,1) (2,0) (2,1) (2,2) (3,0) (3,1) (3,2) (3,3): tiles
-// first, first + stride, ...  The operands of eight k steps are read before
-// their products are issued.
+// staged in X, for NT of the ten lower 32 x 32 tiles (ti >= tj), numbered in
+// the order (0,0) (1,0) (1,1) (2,0) (2,1) (2,2) (3,0) (3,1) (3,2) (3,3): the
+// tiles ts.  The operands of eight k steps are read before their products
+// are issued.
 template <int NT>
-__device__ __forceinline__ void pre_update(LeafLDS& sm, int lane, int first, int stride) {
+__device__ __forceinline__ void pre_update(LeafLDS& sm, int lane, const int (&ts)[NT]) {
   const int li = lane & 31, lk = lane >> 5;
   const float* pa[NT];
   const float* pb[NT];
   int ti[NT], tj[NT];
 #pragma unroll
   for (int q = 0; q < NT; ++q) {
-    const int t = first + stride * q;
+    const int t = ts[q];
     ti[q] = t < 1 ? 0 : t < 3 ? 1 : t < 6 ? 2 : 3;
     tj[q] = t - ti[q] * (ti[q] + 1) / 2;
     pa[q] = &sm.X[ti[q] * 32 + li][lk];
@@ -378,18 +394,6 @@ __device__ __forceinline__ void pre_update(LeafLDS& sm, int lane, int first, int
       const int i = ti[q] * 32 + 8 * (r >> 2) + 4 * lk + (r & 3), j = tj[q] * 32 + li;
       sm.S[i][j] = j <= i ? sv[q][r] - u[q][r] : sv[q][r];
     }
-}
-
-// The recursion reads X only where it has written it, except the blocks
-// above the diagonal inside X11 and X22 of the top level (the base blocks
-// write theirs in full): zero those two 32 x 32 blocks.
-__device__ __forceinline__ void zero_upper(LeafLDS& sm, int tid) {
-  const int r = tid >> 3, c = 4 * (tid & 7);
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    sm.X[r][32 + c + e] = 0.0f;
-    sm.X[64 + r][96 + c + e] = 0.0f;
-  }
 }
 
 // Thread tid's share of a 128 x 128 block moved as float4: rows
@@ -497,16 +501,23 @@ __device__ __forceinline__ void leaf_body(LeafLDS& sm, const float* Lblk, float*
       load_rows(sm.X, Lpre, ld, 0, 0, b, tid);
       __syncthreads();
     }
-    // tile (0, 0) now, the other nine during the first base block
-    if (wave == 0) pre_update<1>(sm, lane, 0, 1);
+    // tile (0, 0) now, the other nine during the first two base blocks
+    if (wave == 0) {
+      const int ts[1] = {0};
+      pre_update<1>(sm, lane, ts);
+    }
     __syncthreads();
   }
   const bool vec_out = b == NB && (ld & 3) == 0 && (reinterpret_cast<uintptr_t>(Liblk) & 15) == 0 &&
                        (reinterpret_cast<uintptr_t>(Lout) & 15) == 0;
   // While wave 0 factors the first base block of the second half, waves
   // 1..3 store what is final by then: L11, L^-1 11, the zeros above them and
-  // L21.
+  // L21.  (Without P, X was zeroed when the block was read.)
   auto early = [&](int t) {
+    // the block above the diagonal inside X22 is read before it is written:
+    // zero X[64:96][96:128] (P no longer needed)
+#pragma unroll
+    for (int f = t; f < 1024; f += 192) sm.X[64 + (f >> 5)][96 + (f & 31)] = 0.0f;
     if (!vec_out) return;
     store64<192>(sm.X, 0, 0, Liblk, ld, 1, t);
     store64<192>(sm.X, 0, 0, Liblk + 64, ld, 2, t);
@@ -516,7 +527,7 @@ __device__ __forceinline__ void leaf_body(LeafLDS& sm, const float* Lblk, float*
       store64<192>(sm.S, 64, 0, Lout + 64 * ld, ld, 0, t);
     }
   };
-  const int bad = cholinv_lds<NB>(sm, 0, wave, lane, Lpre != nullptr, NoSide(), early);
+  const int bad = cholinv_lds<NB>(sm, 0, wave, lane, Lpre != nullptr ? 1 : 0, NoSide(), early);
   if (bad >= 0) {
     if (tid == 0) {
       st[1] = side;
