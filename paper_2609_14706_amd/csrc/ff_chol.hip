@@ -16,7 +16,10 @@
 // with X = L^-1.  32 x 32 base blocks are factored and inverted by one wave
 // in registers (half the lanes hold rows of L, half columns of L^-1; each new
 // column of L is broadcast through LDS); the products run on the fp32 matrix
-// cores, one output tile per wave.  A ragged block (b < 128) is padded with
+// cores, one output tile per wave.  While wave 0 factors a base block, the
+// other three waves do work off the pivot chain: the rest of the panel's
+// update of the block (first two base blocks) and the stores of the parts of
+// L and L^-1 already final (third).  A ragged block (b < 128) is padded with
 // the identity.
 #include <math.h>
 
@@ -430,9 +433,10 @@ __device__ __forceinline__ void store64(const float (*src)[SP], int r0, int c0, 
 // workgroup: reads the lower triangle of Lblk (ld), writes the block of L^-1
 // (lower, zeros above) to Liblk and, when Lout is not null, L itself over the
 // block; sum(log diag L) into logdet[slot]; on a non-positive or NaN pivot
-// sets st = {iteration, side, pivot_base + j} and returns.  Lpre (optional): the block row of the last panel to
-// the left (b rows x 128, leading dimension ld), whose update
-// A -= Lpre Lpre^T is applied to the block first.
+// sets st = {iteration, side, pivot_base + j} and returns (the outputs then
+// hold partial results, at most the first half's).  Lpre (optional): the
+// block row of the last panel to the left (b rows x 128, leading dimension
+// ld), whose update A -= Lpre Lpre^T is applied to the block first.
 __device__ __forceinline__ void leaf_body(LeafLDS& sm, const float* Lblk, float* __restrict__ Liblk,
                                           int64_t ld, int b, int64_t pivot_base, double* logdet,
                                           int slot, int iteration, int side, int* st, float* Lout,
