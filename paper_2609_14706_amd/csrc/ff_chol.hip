@@ -227,11 +227,13 @@ __device__ __forceinline__ void base_step(LeafLDS& sm, int o, int wave, int lane
 // Recursive cholinv of the block at (o, o) of size S (64 or 128, unrolled at
 // compile time); every wave takes every barrier.  Returns the failing column
 // or -1.  pre, side: see base_step (pre = 1 goes to the first base block,
-// pre = 2 to the second); side2: side work for the first base block of the
-// second half.
-template <int S, class Side = NoSide, class Side2 = NoSide>
+// pre = 2 to the second); side2, side3: side work for the first and second
+// base blocks of the second half.  A side3 other than NoSide computes this
+// level's Y = L21 X11 into T (the level then skips that product).
+template <int S, class Side = NoSide, class Side2 = NoSide, class Side3 = NoSide>
 __device__ __forceinline__ int cholinv_lds(LeafLDS& sm, int o, int wave, int lane, int pre = 0,
-                                           const Side& side = Side(), const Side2& side2 = Side2()) {
+                                           const Side& side = Side(), const Side2& side2 = Side2(),
+                                           const Side3& side3 = Side3()) {
   constexpr int h = S / 2;
   typedef LevelTile<h> LT;
   if constexpr (h == BS) base_step(sm, o, wave, lane, pre, side);
@@ -255,19 +257,24 @@ __device__ __forceinline__ int cholinv_lds(LeafLDS& sm, int o, int wave, int lan
   }
   __syncthreads();
   if constexpr (h == BS) base_step(sm, o2, wave, lane, pre == 1 ? 2 : 0, side2);
-  else cholinv_lds<h>(sm, o2, wave, lane, 0, side2);
+  else cholinv_lds<h>(sm, o2, wave, lane, 0, side2, side3);
   if (sm.bad >= 0) return sm.bad;
-  // Y = L21 X11 -> T;  X21 = -X22 Y
-  {
+  // Y = L21 X11 (into C at h = 32, T at h = 64: the second half's Y may be
+  // in T already, made by side3);  X21 = -X22 Y
+  auto ybuf = [&](int k, int j) -> float& {
+    if constexpr (h == BS) return sm.C[k][j];
+    else return sm.T[k][j];
+  };
+  if constexpr (std::is_same<Side3, NoSide>::value) {
     const typename LT::Acc y = LT::product(wave, lane, [&](int i, int k) { return sm.S[o2 + i][o + k]; },
                                            [&](int k, int j) { return sm.X[o + k][o + j]; });
 #pragma unroll
-    for (int r = 0; r < LT::NACC; ++r) sm.T[LT::row(wave, r, lane)][oc] = y[r];
+    for (int r = 0; r < LT::NACC; ++r) ybuf(LT::row(wave, r, lane), oc) = y[r];
+    __syncthreads();
   }
-  __syncthreads();
   {
     const typename LT::Acc x21 = LT::product(wave, lane, [&](int i, int k) { return sm.X[o2 + i][o2 + k]; },
-                                             [&](int k, int j) { return sm.T[k][j]; });
+                                             [&](int k, int j) { return ybuf(k, j); });
 #pragma unroll
     for (int r = 0; r < LT::NACC; ++r) sm.X[o2 + LT::row(wave, r, lane)][o + oc] = -x21[r];
   }
@@ -531,7 +538,22 @@ __device__ __forceinline__ void leaf_body(LeafLDS& sm, const float* Lblk, float*
       store64<192>(sm.S, 64, 0, Lout + 64 * ld, ld, 0, t);
     }
   };
-  const int bad = cholinv_lds<NB>(sm, 0, wave, lane, Lpre != nullptr ? 1 : 0, NoSide(), early);
+  // While it factors the second: the top level's Y = L21 X11 (64 x 64 x 64)
+  // into T, the four 32 x 32 tiles on waves 1..3 (1: tiles 0 and 3).
+  auto top_y = [&](int) {
+    typedef LevelTile<64> LT;
+    const int w = (int)threadIdx.x >> 6;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int tw = q == 0 ? w - 1 : 3;
+      if (q == 1 && w != 1) break;
+      const LT::Acc y = LT::product(tw, lane, [&](int i, int k) { return sm.S[64 + i][k]; },
+                                    [&](int k, int j) { return sm.X[k][j]; });
+#pragma unroll
+      for (int r = 0; r < LT::NACC; ++r) sm.T[LT::row(tw, r, lane)][LT::col(tw, lane)] = y[r];
+    }
+  };
+  const int bad = cholinv_lds<NB>(sm, 0, wave, lane, Lpre != nullptr ? 1 : 0, NoSide(), early, top_y);
   if (bad >= 0) {
     if (tid == 0) {
       st[1] = side;
