@@ -435,8 +435,9 @@ ff_status chol_blocked(ff_handle_s* h, Side& s, int iteration) {
       // the panel L_ik = A_ik Li_kk^T, in place
       FF_HIP(launch_panel_solve(s.L + (o + kLeaf) * d + o, s.Li + o * d + o, d, rest, h->st, ms));
       // every kInvEvery panels, and every second one among the last
-      // kInvEvery (the last steps leave most CUs idle for the tree's products)
-      const bool tail = k + 1 + kInvEvery >= nb && (k + 1) % 2 == 0;
+      // kInvEvery and the one before the last leaf (the last steps leave most
+      // CUs idle for the tree's products)
+      const bool tail = k + 1 + kInvEvery >= nb && ((k + 1) % 2 == 0 || k + 2 == nb);
       if (((k + 1) % kInvEvery == 0 || tail) && (rc = hand_over(k, true)) != FF_OK) return rc;
       if (o + kLeaf == pe) break;  // the last panel of the outer panel
       // diagonal block k + 1 and the panel's update of the outer panel's columns
