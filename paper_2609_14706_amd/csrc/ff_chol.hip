@@ -512,10 +512,30 @@ __device__ __forceinline__ void leaf_body(LeafLDS& sm, const float* Lblk, float*
       load_rows(sm.X, Lpre, ld, 0, 0, b, tid);
       __syncthreads();
     }
-    // tile (0, 0) now, the other nine during the first two base blocks
-    if (wave == 0) {
-      const int ts[1] = {0};
-      pre_update<1>(sm, lane, ts);
+    // tile (0, 0) now, the other nine during the first two base blocks.
+    // Tile (0, 0) splits k over the four waves (k in [32 w, 32 w + 32) on
+    // wave w), whose partial products meet in T and are summed in a fixed
+    // order.
+    {
+      const int li = lane & 31, lk = lane >> 5;
+      const float* pa = &sm.X[li][32 * wave + lk];
+      float a[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) a[e] = pa[2 * e];
+      f32x16 u;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) u[r] = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) u = __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], a[e], u, 0, 0, 0);
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        sm.T[32 * (wave >> 1) + 8 * (r >> 2) + 4 * lk + (r & 3)][32 * (wave & 1) + li] = u[r];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int f = tid + 256 * e, i = f >> 5, jj = f & 31;
+      if (jj <= i) sm.S[i][jj] -= (sm.T[i][jj] + sm.T[i][32 + jj]) + (sm.T[32 + i][jj] + sm.T[32 + i][32 + jj]);
     }
     __syncthreads();
   }
