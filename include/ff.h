@@ -155,9 +155,14 @@ ff_status ff_init(const ff_config* cfg, ff_handle* out);
  * *iters_done receives the number of iterations completed by this call.
  * loglik (host array of `iters` doubles, may be NULL) receives, per completed
  * iteration, the matrix-normal log-likelihood of the samples under the new
- * A (x) B, evaluated as -(N/2)(m log|A| + n log|B|) - (N m n/2)(1 + log 2 pi),
- * which is exact when damping == 0 (the trace term equals N m n after a
- * maximum-likelihood half step, Section 5 trace identity).
+ * A (x) B, -(N/2)(m log|A| + n log|B|) - T/2 - (N m n/2) log 2 pi, with the
+ * log-determinants from the Cholesky pivots and the trace term
+ * T = sum_i tr(B^-1 G_i A^-1 G_i^T) in closed form: N m n after a
+ * maximum-likelihood half step (Section 5 trace identity); with damping
+ * kappa > 0 (Appendix B), N d' (d - kappa/(1 + kappa) (tr(F)/d) ||L_F^-1||_F^2)
+ * for the second-updated factor F (dimension d, the other one d') and its
+ * Cholesky factor L_F, which the next iteration needs anyway.  The other
+ * estimators report NaN.
  * FF_ERR_NOT_SPD: a factor to be inverted was not positive definite (the
  * paper assumes invertibility, Section 2; use damping > 0).  The handle then
  * keeps the factors of the last completed iteration and stays usable.  An
@@ -165,6 +170,37 @@ ff_status ff_init(const ff_config* cfg, ff_handle* out);
  * entry is NaN); the next iteration, which must invert it, fails.
  * Errors: FF_ERR_INVALID_ARG, FF_ERR_NOT_SPD, FF_ERR_HIP. */
 ff_status ff_iterate(ff_handle h, int iters, int* iters_done, double* loglik);
+
+/* ff_iterate with the convergence diagnostic of the iteration.  After each
+ * iteration g the device evaluates, in fp64, the relative change of the
+ * normalised Kronecker product
+ *   delta_g = ||A_g (x) B_g - A_{g-1} (x) B_{g-1}||_F / (||A_{g-1}||_F ||B_{g-1}||_F)
+ * from ||X (x) Y - X' (x) Y'||^2 = ||dX||^2 ||Y||^2 + ||X'||^2 ||dY||^2
+ * + 2 <dX, X'> <Y, dY> (dX = X - X', dY = Y - Y'; the mn x mn product is
+ * never formed; for the first iteration of a handle the previous iterate is
+ * the start A0 / B0 or identity).  delta (host array of max_iters doubles,
+ * may be NULL) receives delta_g per completed iteration.  tol > 0 stops after
+ * the first iteration with delta_g <= tol; that iteration is complete (its
+ * factors, log-likelihood and the factorisation the next one needs) and
+ * *iters_done counts it.  tol == 0 runs all max_iters.  No host round trip
+ * per iteration: later iterations already enqueued return at once on the
+ * device.  Errors: as ff_iterate, and FF_ERR_INVALID_ARG for a negative or
+ * non-finite tol. */
+ff_status ff_iterate_tol(ff_handle h, int max_iters, double tol, int* iters_done, double* loglik,
+                         double* delta);
+
+/* One half step of Section 5 with the other factor held fixed, unscaled and
+ * undamped: FF_HALF_B: out (m x m) = (1/(N n)) sum_i G_i F^-1 G_i^T with
+ * F (n x n); FF_HALF_A: out (n x n) = (1/(N m)) sum_i G_i^T F^-1 G_i with
+ * F (m x m).  (The Frobenius estimator uses F in place of F^-1.)  F: DEVICE
+ * fp32 row-major SPD (lower triangle read), or NULL for the handle's current
+ * factor; out: DEVICE fp32, 16-byte aligned.  Same path as an iteration's
+ * update (factorisation, whitening, symmetric product).  The handle's factors
+ * are untouched; the next ff_iterate refactorises them.  Synchronises the
+ * stream.  Errors: FF_ERR_INVALID_ARG (also for the Marginal and Input
+ * estimators), FF_ERR_NOT_SPD (F not positive definite), FF_ERR_HIP. */
+typedef enum { FF_HALF_B = 0, FF_HALF_A = 1 } ff_half;
+ff_status ff_half_step(ff_handle h, ff_half which, const float* F, float* out);
 
 /* Copy the current factors: A (n x n) and B (m x m), fp32 row-major,
  * normalised to tr(A) = n.  on_host = 0: A and B are device pointers and the

@@ -113,11 +113,14 @@ def half_step_A(G, B, *, iteration=0):
     return 0.5 * (A + A.T)
 
 
-def half_step_B_rows(G, A, rows):
-    """Rows ``rows`` of the B update (1/(N n)) sum_i G_i A^-1 G_i^T.
+def half_step_B_rows(G, A, rows, progress=None):
+    """Rows ``rows`` of the B update (1/(N n)) sum_i G_i A^-1 G_i^T
+    (Section 5, update of B); A = None means the identity.
 
-    For large layers: the samples are converted to fp64 one at a time
-    (uint16 = bf16 bit patterns), so only one sample is held in fp64.
+    Row r of sample i's term is (A^-1 G_i[r]^T)^T G_i^T, one Cholesky solve
+    per selected row.  For large layers: the samples are converted to fp64
+    one at a time (uint16 = bf16 bit patterns), so only one sample is held
+    in fp64.  ``progress(i)``, if given, is called after sample i.
     """
     G = np.asarray(G)
     N, m, n = G.shape
@@ -131,7 +134,34 @@ def half_step_B_rows(G, A, rows):
         if not identity:
             R = sla.cho_solve(cA, R.T, check_finite=False).T
         out += R @ Gi.T
+        if progress is not None:
+            progress(i)
     return out / (N * n)
+
+
+def half_step_A_rows(G, B, rows, progress=None):
+    """Rows ``rows`` of the A update (1/(N m)) sum_i G_i^T B^-1 G_i
+    (Section 5, update of A); B = None means the identity.
+
+    Row c of sample i's term is (B^-1 G_i[:, c])^T G_i, one Cholesky solve
+    per selected column of G_i; samples are converted one at a time.
+    ``progress(i)``, if given, is called after sample i.
+    """
+    G = np.asarray(G)
+    N, m, n = G.shape
+    rows = np.asarray(rows)
+    identity = B is None
+    cB = None if identity else _chol(np.asarray(B, np.float64), "B", 0)
+    out = np.zeros((len(rows), n))
+    for i in range(N):
+        Gi = as_f64_samples(G[i:i + 1])[0]
+        C = Gi[:, rows]                                 # (m, r)
+        if not identity:
+            C = sla.cho_solve(cB, C, check_finite=False)
+        out += C.T @ Gi
+        if progress is not None:
+            progress(i)
+    return out / (N * m)
 
 
 def damp(X, kappa):

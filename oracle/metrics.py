@@ -35,13 +35,6 @@ def kron_rel_error(A, B, A_ref, B_ref) -> float:
     return float(np.sqrt(max(sq, 0.0)) / den)
 
 
-def kron_rel_error_scale_free(A, B, A_ref, B_ref) -> float:
-    """Same, after scaling each product to unit Frobenius norm."""
-    A, B, A_ref, B_ref = map(_f64, (A, B, A_ref, B_ref))
-    return kron_rel_error(A / np.linalg.norm(A), B / np.linalg.norm(B),
-                          A_ref / np.linalg.norm(A_ref), B_ref / np.linalg.norm(B_ref))
-
-
 def trace_identity(G, A, B) -> float:
     """(1/(N m n)) sum_i tr(B^-1 G_i A^-1 G_i^T)  (Section 5 trace identity).
 

@@ -21,6 +21,7 @@ FF_APPLY, FF_APPLY_INV = 0, 1
 FF_SAMPLES_DENSE, FF_SAMPLES_RANK1 = 0, 1
 FF_SCALES_WATERFILL, FF_SCALES_GIVEN = 0, 1
 FF_EST_FLIPFLOP, FF_EST_FROBENIUS, FF_EST_MARGINAL, FF_EST_INPUT = 0, 1, 2, 3
+FF_HALF_B, FF_HALF_A = 0, 1
 ESTIMATORS = {"flipflop": FF_EST_FLIPFLOP, "frobenius": FF_EST_FROBENIUS,
               "marginal": FF_EST_MARGINAL, "input": FF_EST_INPUT}
 KERNEL_IDS = {"whiten": 0, "syrk": 1, "reduce": 2, "cholinv": 3, "quant_diag": 4}
@@ -66,6 +67,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "ff_workspace_size": (st, [ctypes.POINTER(ff_config), ctypes.POINTER(ctypes.c_size_t)]),
         "ff_init": (st, [ctypes.POINTER(ff_config), ctypes.POINTER(H)]),
         "ff_iterate": (st, [H, ctypes.c_int, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_double)]),
+        "ff_iterate_tol": (st, [H, ctypes.c_int, ctypes.c_double, ctypes.POINTER(ctypes.c_int),
+                                ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
+        "ff_half_step": (st, [H, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]),
         "ff_factors": (st, [H, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int]),
         "ff_kron_apply": (st, [H, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int]),
         "ff_objective": (st, [H, ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(ctypes.c_double)]),
@@ -140,6 +144,24 @@ def ff_iterate(h, iters: int, want_loglik: bool = True):
         err.loglik = lls
         raise err
     return done.value, lls
+
+
+def ff_iterate_tol(h, max_iters: int, tol: float):
+    """(iterations done, log-likelihoods, relative changes of A (x) B)."""
+    done = ctypes.c_int(0)
+    ll = (ctypes.c_double * max(max_iters, 1))()
+    dl = (ctypes.c_double * max(max_iters, 1))()
+    code = load_library().ff_iterate_tol(h, max_iters, float(tol), ctypes.byref(done), ll, dl)
+    lls, dls = list(ll[:done.value]), list(dl[:done.value])
+    if code != FF_OK:
+        err = FlipFlopError(code, ff_last_error(), done.value)
+        err.loglik, err.delta = lls, dls
+        raise err
+    return done.value, lls, dls
+
+
+def ff_half_step(h, which: int, F_ptr, out_ptr):
+    _check(load_library().ff_half_step(h, which, F_ptr, out_ptr))
 
 
 def ff_factors(h, A_ptr: int, B_ptr: int, on_host: int):
@@ -292,6 +314,39 @@ class FlipFlop:
             raise
         self.iters_done += done
         return ll
+
+    def iterate_tol(self, max_iters: int, tol: float = 0.0):
+        """Up to `max_iters` iterations, stopping after the first whose relative
+        change of A (x) B is <= tol (tol = 0: never); returns
+        (iterations done, log-likelihoods, relative changes); see ff_iterate_tol."""
+        try:
+            done, ll, dl = ff_iterate_tol(self.h, int(max_iters), tol)
+        except FlipFlopError as e:
+            self.iters_done += e.iters_done
+            raise
+        self.iters_done += done
+        return done, ll, dl
+
+    def half_step(self, which: str, F=None):
+        """One unscaled, undamped half step with the other factor fixed:
+        which = "B": (1/(N n)) sum_i G_i F^-1 G_i^T (F n x n, default the
+        current A); which = "A": (1/(N m)) sum_i G_i^T F^-1 G_i (F m x m,
+        default the current B).  Returns a new fp32 CUDA tensor."""
+        import torch
+        code, dim_out, dim_in = {"B": (FF_HALF_B, self.m, self.n),
+                                 "A": (FF_HALF_A, self.n, self.m)}[which]
+        keep = None
+        pf = None
+        if F is not None:
+            keep = F.to(device=self.device, dtype=torch.float32).contiguous()
+            if tuple(keep.shape) != (dim_in, dim_in):
+                raise ValueError(f"F must be {dim_in} x {dim_in}")
+            pf = keep.data_ptr()
+        out = torch.empty((dim_out, dim_out), dtype=torch.float32, device=self.device)
+        torch.cuda.current_stream(self.device).synchronize()
+        ff_half_step(self.h, code, pf, out.data_ptr())
+        del keep
+        return out
 
     def factors(self):
         """(A, B) as new fp32 CUDA tensors, tr(A) = n."""

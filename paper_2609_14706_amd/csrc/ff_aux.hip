@@ -233,9 +233,18 @@ __global__ __launch_bounds__(256) void k_normalise(float* __restrict__ FA, int64
   if (blockIdx.x == 0 && threadIdx.x == 0) *c_out = c;
 }
 
+// Trace term of the log-likelihood, sum_i tr(B^-1 G_i A^-1 G_i^T).  After
+// the second update of an iteration, F_d = F_h + kappa t I with F_h the
+// maximum-likelihood half step (dimension d, scaled by 1 / (N d_o)) and
+// t = tr(F_h) / d; the term is N d_o tr(F_d^-1 F_h) = N d_o (d - kappa t tr(F_d^-1)),
+// which the normalisation (F_n = F_d / c or c F_d, the other factor scaled
+// the other way) leaves unchanged.  In terms of the normalised factor and
+// its Cholesky factor L_n: N d_o (d - kappa / (1 + kappa) (tr(F_n) / d) ||L_n^-1||_F^2).
+// part holds per-workgroup (sum of squares of L_n^-1, diagonal sum of F_n).
 __global__ __launch_bounds__(256) void k_loglik(const double* slotsA, int nA, const double* slotsB,
                                                 int nB, const double* cptr, int first_is_B,
-                                                double m, double n, double N, double* ll_out,
+                                                double m, double n, double N, double kappa,
+                                                const double* part, int nparts, double* ll_out,
                                                 const int* st) {
   if (ff_halted(st)) return;
   if (threadIdx.x != 0) return;
@@ -249,8 +258,92 @@ __global__ __launch_bounds__(256) void k_loglik(const double* slotsA, int nA, co
   // (B <- c B, or A <- A / c in the A-first order).
   if (first_is_B) lb += m * logc;
   else la -= n * logc;
+  double trace_term = N * m * n;
+  if (kappa > 0.0 && part != nullptr) {
+    double ss = 0.0, tf = 0.0;
+    for (int b = 0; b < nparts; ++b) {
+      ss += part[2 * b];
+      tf += part[2 * b + 1];
+    }
+    const double d = first_is_B ? n : m, d_o = first_is_B ? m : n;
+    trace_term = N * d_o * (d - kappa / (1.0 + kappa) * (tf / d) * ss);
+  }
   const double log2pi = 1.8378770664093454835606594728112;
-  *ll_out = -0.5 * N * (m * la + n * lb) - 0.5 * N * m * n * (1.0 + log2pi);
+  *ll_out = -0.5 * N * (m * la + n * lb) - 0.5 * trace_term - 0.5 * N * m * n * log2pi;
+}
+
+// Per-workgroup partial sums (fixed strided subsets, fixed-order reduction)
+// of sum Li^2 over dim x dim and of the diagonal of F.
+__global__ __launch_bounds__(256) void k_sumsq_trace(const float* __restrict__ Li,
+                                                     const float* __restrict__ F, int64_t dim,
+                                                     double* __restrict__ part, const int* st) {
+  if (ff_halted(st)) return;
+  __shared__ double red[256];
+  const int64_t stride = (int64_t)kDiagBlocks * 256;
+  const int64_t first = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  double ss = 0.0, tf = 0.0;
+  for (int64_t i = first; i < dim * dim; i += stride) {
+    const double v = (double)Li[i];
+    ss += v * v;
+  }
+  for (int64_t i = first; i < dim; i += stride) tf += (double)F[i * dim + i];
+  ss = block_sum_256(ss, red);
+  tf = block_sum_256(tf, red);
+  if (threadIdx.x == 0) {
+    part[2 * blockIdx.x] = ss;
+    part[2 * blockIdx.x + 1] = tf;
+  }
+}
+
+// Relative change of the Kronecker product between two iterates, in fp64,
+// from the differences themselves (no cancellation floor):
+//   ||A (x) B - Ap (x) Bp||_F^2 = ||dA||^2 ||B||^2 + ||Ap||^2 ||dB||^2 + 2 <dA, Ap> <B, dB>,
+// dA = A - Ap, dB = B - Bp, divided by ||Ap||_F ||Bp||_F.  Partials per
+// workgroup: [||dA||^2, <dA,Ap>, ||Ap||^2, ||B||^2, ||dB||^2, <B,dB>, ||Bp||^2, 0].
+__global__ __launch_bounds__(256) void k_delta_partial(const float* __restrict__ A,
+                                                       const float* __restrict__ Ap, int64_t nA,
+                                                       const float* __restrict__ B,
+                                                       const float* __restrict__ Bp, int64_t nB,
+                                                       double* __restrict__ part, const int* st) {
+  if (ff_halted(st)) return;
+  __shared__ double red[256];
+  const int64_t stride = (int64_t)kDiagBlocks * 256;
+  const int64_t first = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  double v[7] = {0, 0, 0, 0, 0, 0, 0};
+  for (int64_t i = first; i < nA; i += stride) {
+    const double a = A[i], ap = Ap[i], d = a - ap;
+    v[0] += d * d;
+    v[1] += d * ap;
+    v[2] += ap * ap;
+  }
+  for (int64_t i = first; i < nB; i += stride) {
+    const double b = B[i], bp = Bp[i], d = b - bp;
+    v[3] += b * b;
+    v[4] += d * d;
+    v[5] += b * d;
+    v[6] += bp * bp;
+  }
+  for (int k = 0; k < 7; ++k) {
+    const double r = block_sum_256(v[k], red);
+    if (threadIdx.x == 0) part[8 * blockIdx.x + k] = r;
+  }
+}
+
+// delta_out = the relative change; with tol > 0 and delta <= tol, st[3] =
+// iteration, which halts the rest of the pipeline (the iterate is complete).
+__global__ __launch_bounds__(64) void k_delta_final(const double* __restrict__ part,
+                                                    double* delta_out, double tol, int iteration,
+                                                    int* st) {
+  if (ff_halted(st)) return;
+  if (threadIdx.x != 0) return;
+  double v[7] = {0, 0, 0, 0, 0, 0, 0};
+  for (int b = 0; b < kDiagBlocks; ++b)
+    for (int k = 0; k < 7; ++k) v[k] += part[8 * b + k];
+  const double sq = v[0] * v[3] + v[2] * v[4] + 2.0 * v[1] * v[5];
+  const double den = sqrt(v[2] * v[6]);
+  const double delta = sqrt(sq > 0.0 ? sq : 0.0) / den;
+  *delta_out = delta;
+  if (tol > 0.0 && delta <= tol) st[3] = iteration;
 }
 
 // Partial sums of a[i] * b[i] in fp64: block z sums a fixed strided subset
@@ -428,9 +521,27 @@ hipError_t launch_normalise(float* FA, int64_t n, float* FB, int64_t m, const do
 
 hipError_t launch_loglik(const double* slotsA, int nA, const double* slotsB, int nB,
                          const double* c, int first_is_B, double m, double n, double N,
-                         double* ll_out, const int* st, hipStream_t s) {
+                         double kappa, const double* part, double* ll_out, const int* st,
+                         hipStream_t s) {
   hipLaunchKernelGGL(k_loglik, dim3(1), dim3(64), 0, s, slotsA, nA, slotsB, nB, c, first_is_B, m,
-                     n, N, ll_out, st);
+                     n, N, kappa, part, kDiagBlocks, ll_out, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_sumsq_trace(const float* Li, const float* F, int64_t dim, double* part,
+                              const int* st, hipStream_t s) {
+  if (dim < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_sumsq_trace, dim3(kDiagBlocks), dim3(256), 0, s, Li, F, dim, part, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_delta(const float* A, const float* Ap, int64_t nA, const float* B,
+                        const float* Bp, int64_t nB, double* part, double* delta_out, double tol,
+                        int iteration, int* st, hipStream_t s) {
+  if (nA < 1 || nB < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_delta_partial, dim3(kDiagBlocks), dim3(256), 0, s, A, Ap, nA, B, Bp, nB,
+                     part, st);
+  hipLaunchKernelGGL(k_delta_final, dim3(1), dim3(64), 0, s, part, delta_out, tol, iteration, st);
   return hipGetLastError();
 }
 

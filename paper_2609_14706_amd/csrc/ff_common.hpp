@@ -17,10 +17,13 @@ typedef uint16_t bf16_t;  // bf16 bit pattern in memory
 //          factor to be inverted was not positive definite.
 //   st[1]: side that failed (1 = A, 2 = B).
 //   st[2]: 0-based pivot index of the first failing pivot.
-// Every kernel that belongs to the iteration returns at once when st[0] is
-// set, so that the factors of the last completed iteration stay intact.
+//   st[3]: 0, or the 1-based global iteration after which the relative
+//          change of A (x) B fell to the caller's tolerance.
+// Every kernel that belongs to the iteration returns at once when st[0] or
+// st[3] is set, so that the factors of the last completed iteration stay
+// intact.
 __device__ __forceinline__ bool ff_halted(const int* st) {
-  return st != nullptr && __builtin_nontemporal_load(st) != 0;
+  return st != nullptr && (__builtin_nontemporal_load(st) | __builtin_nontemporal_load(st + 3)) != 0;
 }
 
 __device__ __forceinline__ bf16_t f32_to_bf16(float x) {

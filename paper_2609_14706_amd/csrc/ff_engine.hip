@@ -17,6 +17,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -81,7 +82,8 @@ struct Layout {
   // rank-one: gx = padded x (T_p x n_p), gt = padded g (T_p x m_p),
   // w = row-norm partials (bf16) or whitened tokens (fp32), s = weighted
   // transposed tokens, wv = token weights (2 T_p floats)
-  size_t off_small, off_ll, off_slotsA, off_slotsB, off_gx, off_gt, off_w, off_p, off_s, off_wv;
+  size_t off_small, off_ll, off_diag, off_slotsA, off_slotsB, off_gx, off_gt, off_w, off_p, off_s,
+      off_wv;
   size_t w_bytes;  // capacity of the w region
   size_t off_A[6], off_B[6];  // F0, F1, L, Li, Lw, Lw2
   size_t total;
@@ -162,6 +164,9 @@ Layout make_layout(const ff_config* c) {
   };
   L.off_small = take(kAlign);  // status[4] @0, c @64, trA @128, trB @192
   L.off_ll = take(sizeof(double) * kLLCap);
+  // relative changes (kLLCap), their partial sums (8 per workgroup) and the
+  // damped trace term's partial sums (2 per workgroup)
+  L.off_diag = take(sizeof(double) * (kLLCap + 10 * kDiagBlocks));
   L.off_slotsA = take(sizeof(double) * ((n + kLeaf - 1) / kLeaf));
   L.off_slotsB = take(sizeof(double) * ((m + kLeaf - 1) / kLeaf));
   const int64_t dmax = std::max(L.m_p, L.n_p);
@@ -234,6 +239,10 @@ struct ff_handle_s {
   int* st = nullptr;
   double* c = nullptr;
   double* ll = nullptr;
+  double* delta = nullptr;   // relative change of A (x) B per iteration (ring of kLLCap)
+  double* dpart = nullptr;   // its partial sums
+  double* spart = nullptr;   // partial sums of the damped log-likelihood's trace term
+  bool single_stream = false;  // no second stream: the inverse tree runs on the main stream
   int64_t iters_total = 0;
   int cur = 0;
   // measurement hook
@@ -400,26 +409,34 @@ constexpr int64_t kTwoLevel = 6144;
 constexpr int64_t kOuter = 2048;
 
 ff_status chol_blocked(ff_handle_s* h, Side& s, int iteration) {
-  ff_status rc = side_streams(s);
+  // One stream (h->single_stream): the inverse products go on the main
+  // stream in the same order, after the panels they need.
+  const bool two = !h->single_stream;
+  ff_status rc = two ? side_streams(s) : FF_OK;
   if (rc != FF_OK) return rc;
   const int64_t d = s.dim;
   const int64_t nb = (d + kLeaf - 1) / kLeaf;
   const int64_t outer = d > kTwoLevel ? kOuter : nb * kLeaf;
   hipStream_t ms = h->stream;
+  hipStream_t is = two ? s.istream : ms;
   // the inverse stream starts after the work already on the main stream
-  FF_HIP(hipEventRecord(s.ev_leaf, ms));
-  FF_HIP(hipStreamWaitEvent(s.istream, s.ev_leaf, 0));
+  if (two) {
+    FF_HIP(hipEventRecord(s.ev_leaf, ms));
+    FF_HIP(hipStreamWaitEvent(is, s.ev_leaf, 0));
+  }
   int64_t handed = 0;  // leaves whose inverse products are enqueued
   // Leaves [handed, upto] are done, and the panel below leaf upto too when
   // panel_done (all earlier panels are).
   auto hand_over = [&](int64_t upto, bool panel_done) -> ff_status {
-    FF_HIP(hipEventRecord(s.ev_leaf, ms));
-    FF_HIP(hipStreamWaitEvent(s.istream, s.ev_leaf, 0));
+    if (two) {
+      FF_HIP(hipEventRecord(s.ev_leaf, ms));
+      FF_HIP(hipStreamWaitEvent(is, s.ev_leaf, 0));
+    }
     for (int64_t j = handed; j <= upto; ++j) {
-      ff_status r2 = inverse_p2_ending(h, s, 0, d, j, s.istream);
+      ff_status r2 = inverse_p2_ending(h, s, 0, d, j, is);
       if (r2 != FF_OK) return r2;
       if (j + 1 < nb && (panel_done || j < upto)) {
-        r2 = inverse_p1_split(h, s, 0, d, j, s.istream);
+        r2 = inverse_p1_split(h, s, 0, d, j, is);
         if (r2 != FF_OK) return r2;
       }
     }
@@ -457,8 +474,10 @@ ff_status chol_blocked(ff_handle_s* h, Side& s, int iteration) {
     }
   }
   if ((rc = hand_over(nb - 1, false)) != FF_OK) return rc;
-  FF_HIP(hipEventRecord(s.ev_inv, s.istream));
-  FF_HIP(hipStreamWaitEvent(ms, s.ev_inv, 0));
+  if (two) {
+    FF_HIP(hipEventRecord(s.ev_inv, is));
+    FF_HIP(hipStreamWaitEvent(ms, s.ev_inv, 0));
+  }
   return FF_OK;
 }
 
@@ -531,7 +550,8 @@ ff_status token_weights(ff_handle_s* h, Side& p, float* wbuf) {
 // unit: all weights 1 and scale 1/N (the token mean E[u u^T] of the Marginal
 // and Input estimators, Table 1).
 ff_status update_rank1(ff_handle_s* h, Side& s, Side& p, int slot, bool finish,
-                       bool unit = false) {
+                       bool unit = false, float* dst = nullptr) {
+  float* F = dst != nullptr ? dst : s.F[slot];
   float* wbuf = h->wv;
   const int64_t T_p = h->lay.T_p;
   if (unit) {
@@ -556,7 +576,7 @@ ff_status update_rank1(ff_handle_s* h, Side& s, Side& p, int slot, bool finish,
                               h->P, h->st, h->stream));
     }
     Timed t(h, 2, 0.0);
-    FF_HIP(launch_reduce_frag(h->P, s.splits, s.dim_p, s.F[slot], s.dim, scale, h->st, h->stream));
+    FF_HIP(launch_reduce_frag(h->P, s.splits, s.dim_p, F, s.dim, scale, h->st, h->stream));
   } else {
     {
       Timed t(h, 1, sflop);
@@ -571,21 +591,21 @@ ff_status update_rank1(ff_handle_s* h, Side& s, Side& p, int slot, bool finish,
       FF_HIP(launch_gemm_f32(q, 1, h->stream));
     }
     Timed t(h, 2, 0.0);
-    FF_HIP(launch_reduce_rowmajor(h->P, s.splits, s.dim_p, s.F[slot], s.dim, scale, h->st,
-                                  h->stream));
+    FF_HIP(launch_reduce_rowmajor(h->P, s.splits, s.dim_p, F, s.dim, scale, h->st, h->stream));
   }
-  if (finish) FF_HIP(launch_trace_damp(s.F[slot], s.dim, h->cfg.damping, s.tr, h->st, h->stream));
+  if (finish) FF_HIP(launch_trace_damp(F, s.dim, h->cfg.damping, s.tr, h->st, h->stream));
   return FF_OK;
 }
 
-// s.F[slot] = (1/(N p.dim)) sum_i X_i Li_p^T Li_p X_i^T  (+ damping), trace into
+// s.F[slot] (or dst) = (1/(N p.dim)) sum_i X_i Li_p^T Li_p X_i^T  (+ damping), trace into
 // s.tr; with finish = false, without damping and trace.  p_identity: p's
 // factor is exactly I (the default start), so Li_p = I and the whitened
 // samples are the samples themselves (bitwise: a product with I is exact);
 // the symmetric product then reads X directly.
 ff_status update(ff_handle_s* h, Side& s, Side& p, int slot, bool finish = true,
-                 bool p_identity = false) {
-  if (h->lay.rank1) return update_rank1(h, s, p, slot, finish);
+                 bool p_identity = false, float* dst = nullptr) {
+  if (h->lay.rank1) return update_rank1(h, s, p, slot, finish, false, dst);
+  float* F = dst != nullptr ? dst : s.F[slot];
   const void* X = (&s == &h->B) ? h->Gx : h->Gt;
   const int64_t N = h->N, rows = N * s.dim_p, Kp = p.dim_p;
   const double scale = 1.0 / ((double)N * (double)p.dim);
@@ -605,8 +625,7 @@ ff_status update(ff_handle_s* h, Side& s, Side& p, int slot, bool finish = true,
     }
     {
       Timed t(h, 2, 0.0);
-      FF_HIP(launch_reduce_frag(h->P, s.splits, s.dim_p, s.F[slot], s.dim, scale, h->st,
-                                h->stream));
+      FF_HIP(launch_reduce_frag(h->P, s.splits, s.dim_p, F, s.dim, scale, h->st, h->stream));
     }
   } else {
     GemmF32 g{};
@@ -635,11 +654,10 @@ ff_status update(ff_handle_s* h, Side& s, Side& p, int slot, bool finish = true,
     }
     {
       Timed t(h, 2, 0.0);
-      FF_HIP(launch_reduce_rowmajor(h->P, s.splits, s.dim_p, s.F[slot], s.dim, scale, h->st,
-                                    h->stream));
+      FF_HIP(launch_reduce_rowmajor(h->P, s.splits, s.dim_p, F, s.dim, scale, h->st, h->stream));
     }
   }
-  if (finish) FF_HIP(launch_trace_damp(s.F[slot], s.dim, h->cfg.damping, s.tr, h->st, h->stream));
+  if (finish) FF_HIP(launch_trace_damp(F, s.dim, h->cfg.damping, s.tr, h->st, h->stream));
   return FF_OK;
 }
 
@@ -654,6 +672,68 @@ ff_status clear_status(ff_handle_s* h) {
   return FF_OK;
 }
 
+// Relative change of A (x) B between the iterate in `slot` and the one
+// before it (fp64 on the device, into h->delta[k]); with tol > 0 a change
+// <= tol sets st[3] = g and the rest of the enqueued pipeline halts.
+ff_status enqueue_delta(ff_handle_s* h, int slot, int k, int64_t g, double tol) {
+  FF_HIP(launch_delta(h->A.F[slot], h->A.F[slot ^ 1], h->n * h->n, h->B.F[slot], h->B.F[slot ^ 1],
+                      h->m * h->m, h->dpart, h->delta + k, tol, (int)g, h->st, h->stream));
+  return FF_OK;
+}
+
+// After the chunk's single synchronisation: the number of iterations that
+// completed (a failing factorisation, st[0], or the tolerance, st[3]), the
+// host copies of the per-iteration outputs, and the handle's counters.
+// Returns the status to report; *converged is set when the tolerance stopped
+// the chunk, *failed when a factorisation failed (both cached whitening
+// operands are then stale).
+ff_status finish_chunk(ff_handle_s* h, int64_t base, int iters, int* done, double* loglik,
+                       double* delta, bool has_loglik, bool* converged, bool* failed) {
+  int st[4];
+  ff_status rc = read_status(h, st);
+  if (rc != FF_OK) return rc;
+  if (h->timing) collect_timing(h);
+  int completed = iters;
+  *converged = false;
+  *failed = st[0] != 0;
+  if (st[0] != 0) {
+    completed = (int)std::max<int64_t>(0, std::min<int64_t>(iters, st[0] - 1 - base));
+  } else if (st[3] != 0) {
+    completed = (int)std::max<int64_t>(0, std::min<int64_t>(iters, st[3] - base));
+    *converged = true;
+  }
+  if (completed > 0) {
+    if (loglik != nullptr) {
+      if (has_loglik)
+        FF_HIP(hipMemcpy(loglik, h->ll, sizeof(double) * completed, hipMemcpyDeviceToHost));
+      else
+        for (int k = 0; k < completed; ++k) loglik[k] = NAN;
+    }
+    if (delta != nullptr)
+      FF_HIP(hipMemcpy(delta, h->delta, sizeof(double) * completed, hipMemcpyDeviceToHost));
+    if (st[0] != 0) {  // the closing factorisation of the last one failed
+      if (loglik != nullptr) loglik[completed - 1] = NAN;
+      if (delta != nullptr) delta[completed - 1] = NAN;
+    }
+  }
+  h->iters_total = base + completed;
+  h->cur = (int)(h->iters_total & 1);
+  *done = completed;
+  if (st[0] != 0 || st[3] != 0) {
+    if ((rc = clear_status(h)) != FF_OK) return rc;
+    FF_HIP(hipStreamSynchronize(h->stream));
+  }
+  if (st[0] != 0) {
+    h->A.lw_valid = h->B.lw_valid = false;
+    if (st[0] == base + iters + 1) return FF_OK;  // only the look-ahead failed
+    char msg[160];
+    snprintf(msg, sizeof msg, "factor %s not positive definite at iteration %d (pivot %d)",
+             st[1] == 1 ? "A" : "B", st[0], st[2]);
+    return fail(FF_ERR_NOT_SPD, msg);
+  }
+  return FF_OK;
+}
+
 // Up to kLLCap iterations; synchronises once.
 //
 // The factorisation of the second-updated factor that closes iteration g is
@@ -661,9 +741,11 @@ ff_status clear_status(ff_handle_s* h) {
 // iteration g is complete (the oracle also returns such a singular factor),
 // and only a later iteration that would invert it fails.
 // Marginal / Input estimators (Table 1): token means, no factorisation.
-ff_status iterate_means(ff_handle_s* h, int iters, int* done, double* loglik) {
+ff_status iterate_means(ff_handle_s* h, int iters, int* done, double* loglik, double tol,
+                        double* delta, bool* converged) {
   *done = 0;
   const int64_t base = h->iters_total;
+  const bool want_delta = delta != nullptr || tol > 0.0;
   ff_status rc;
   for (int k = 1; k <= iters; ++k) {
     const int slot = (int)((base + k) & 1);
@@ -676,26 +758,24 @@ ff_status iterate_means(ff_handle_s* h, int iters, int* done, double* loglik) {
     }
     FF_HIP(launch_normalise(h->A.F[slot], h->n, h->B.F[slot], h->m, h->A.tr, h->c, h->st,
                             h->stream));
+    if (want_delta && (rc = enqueue_delta(h, slot, k - 1, base + k, tol)) != FF_OK) return rc;
   }
-  int st[4];
-  if ((rc = read_status(h, st)) != FF_OK) return rc;
-  if (h->timing) collect_timing(h);
-  if (st[0] != 0) return fail(FF_ERR_STATE, "device status set during the token means");
-  if (loglik != nullptr)
-    for (int k = 0; k < iters; ++k) loglik[k] = NAN;
-  h->iters_total = base + iters;
-  h->cur = (int)(h->iters_total & 1);
+  bool failed = false;
+  rc = finish_chunk(h, base, iters, done, loglik, delta, false, converged, &failed);
   h->A.lw_valid = h->B.lw_valid = false;
-  *done = iters;
-  return FF_OK;
+  return rc;
 }
 
-ff_status iterate_chunk(ff_handle_s* h, int iters, int* done, double* loglik) {
+ff_status iterate_chunk(ff_handle_s* h, int iters, int* done, double* loglik, double tol,
+                        double* delta, bool* converged) {
   if (h->cfg.estimator == FF_EST_MARGINAL || h->cfg.estimator == FF_EST_INPUT)
-    return iterate_means(h, iters, done, loglik);
+    return iterate_means(h, iters, done, loglik, tol, delta, converged);
   *done = 0;
+  *converged = false;
   const bool bfirst = h->cfg.order == FF_ORDER_B_FIRST;
   const bool flipflop = h->cfg.estimator == FF_EST_FLIPFLOP;
+  const bool want_delta = delta != nullptr || tol > 0.0;
+  const double kappa = h->cfg.damping;
   Side& first = bfirst ? h->B : h->A;
   Side& second = bfirst ? h->A : h->B;
   const int64_t base = h->iters_total;
@@ -716,40 +796,150 @@ ff_status iterate_chunk(ff_handle_s* h, int iters, int* done, double* loglik) {
     FF_HIP(launch_normalise(h->A.F[slot], h->n, h->B.F[slot], h->m, h->A.tr, h->c, h->st,
                             h->stream));
     if ((rc = operand(h, second, slot, (int)(g + 1))) != FF_OK) return rc;
-    if (flipflop)
+    if (flipflop) {
+      // with damping the trace term needs ||L^-1||_F^2 of the factor just factorised
+      if (kappa > 0.0)
+        FF_HIP(launch_sumsq_trace(second.Li, second.F[slot], second.dim, h->spart, h->st,
+                                  h->stream));
       FF_HIP(launch_loglik(h->A.slots, h->A.nslots, h->B.slots, h->B.nslots, h->c, bfirst ? 1 : 0,
-                           (double)h->m, (double)h->n, (double)h->N, h->ll + (k - 1), h->st,
-                           h->stream));
+                           (double)h->m, (double)h->n, (double)h->N, kappa,
+                           kappa > 0.0 ? h->spart : nullptr, h->ll + (k - 1), h->st, h->stream));
+    }
+    if (want_delta && (rc = enqueue_delta(h, slot, k - 1, g, tol)) != FF_OK) return rc;
   }
-  int st[4];
-  if ((rc = read_status(h, st)) != FF_OK) return rc;
-  if (h->timing) collect_timing(h);
-  int completed = iters;
-  if (st[0] != 0) completed = (int)std::max<int64_t>(0, std::min<int64_t>(iters, st[0] - 1 - base));
-  if (loglik != nullptr && completed > 0) {
-    if (flipflop)
-      FF_HIP(hipMemcpy(loglik, h->ll, sizeof(double) * completed, hipMemcpyDeviceToHost));
-    else
-      for (int k = 0; k < completed; ++k) loglik[k] = NAN;
-    if (st[0] != 0) loglik[completed - 1] = NAN;  // its closing factorisation failed
-  }
-  h->iters_total = base + completed;
-  h->cur = (int)(h->iters_total & 1);
-  *done = completed;
-  if (st[0] != 0) {
-    second.lw_valid = false;
-    first.lw_valid = false;
-    if ((rc = clear_status(h)) != FF_OK) return rc;
-    FF_HIP(hipStreamSynchronize(h->stream));
-    if (st[0] == base + iters + 1) return FF_OK;  // only the look-ahead failed
-    char msg[160];
-    snprintf(msg, sizeof msg, "factor %s not positive definite at iteration %d (pivot %d)",
-             st[1] == 1 ? "A" : "B", st[0], st[2]);
-    return fail(FF_ERR_NOT_SPD, msg);
-  }
-  second.lw_valid = true;
+  bool failed = false;
+  rc = finish_chunk(h, base, iters, done, loglik, delta, flipflop, converged, &failed);
+  if (rc != FF_OK) return rc;
+  // the look-ahead factorisation of the last completed iteration ran unless
+  // a factorisation failed (then both cached operands are stale)
+  if (!failed) second.lw_valid = true;
   return FF_OK;
 }
+
+// Chunks of at most kLLCap iterations (32 when timing, to bound the events
+// in flight), each synchronised once; stops early when a chunk converged.
+ff_status run_iterations(ff_handle_s* h, int iters, double tol, int* iters_done, double* loglik,
+                         double* delta) {
+  if (iters_done != nullptr) *iters_done = 0;
+  if (h == nullptr) return fail(FF_ERR_INVALID_ARG, "handle is NULL");
+  if (iters < 0) return fail(FF_ERR_INVALID_ARG, "iters must be >= 0");
+  if (h->iters_total + (int64_t)iters > 0x7fffffffLL)
+    return fail(FF_ERR_STATE, "iteration counter overflow");
+  int total = 0;
+  const int cap = h->timing ? 32 : kLLCap;
+  while (total < iters) {
+    const int chunk = std::min(cap, iters - total);
+    int done = 0;
+    bool converged = false;
+    ff_status rc = iterate_chunk(h, chunk, &done, loglik ? loglik + total : nullptr, tol,
+                                 delta ? delta + total : nullptr, &converged);
+    total += done;
+    if (iters_done != nullptr) *iters_done = total;
+    if (rc != FF_OK || converged) return rc;
+  }
+  return FF_OK;
+}
+
+// Everything ff_init checks besides the workspace.
+ff_status validate_config(const ff_config* cfg) {
+  ff_status rc = validate_shape(cfg);
+  if (rc != FF_OK) return rc;
+  if (cfg->form == FF_SAMPLES_RANK1) {
+    if (cfg->x == nullptr || cfg->g == nullptr || ((uintptr_t)cfg->x % 16) != 0 ||
+        ((uintptr_t)cfg->g % 16) != 0)
+      return fail(FF_ERR_INVALID_ARG, "x and g must be non-NULL 16-byte aligned device pointers");
+  } else if (cfg->G == nullptr || ((uintptr_t)cfg->G % 16) != 0) {
+    return fail(FF_ERR_INVALID_ARG, "G must be a non-NULL 16-byte aligned device pointer");
+  }
+  if (cfg->order != FF_ORDER_B_FIRST && cfg->order != FF_ORDER_A_FIRST)
+    return fail(FF_ERR_INVALID_ARG, "unknown order");
+  if (!(cfg->damping >= 0.0) || !isfinite(cfg->damping))
+    return fail(FF_ERR_INVALID_ARG, "damping must be finite and >= 0");
+  if (((uintptr_t)cfg->A0 % 16) != 0 || ((uintptr_t)cfg->B0 % 16) != 0)
+    return fail(FF_ERR_INVALID_ARG, "A0/B0 must be 16-byte aligned");
+  return FF_OK;
+}
+
+// Fill the handle for cfg over the workspace and enqueue the set-up.
+ff_status init_handle(const ff_config* cfg, const Layout& lay, ff_handle_s* h) {
+  h->cfg = *cfg;
+  if (!is_bf16(cfg)) h->cfg.whiten_split = 1;
+  h->stream = (hipStream_t)cfg->stream;
+  h->m = cfg->m;
+  h->n = cfg->n;
+  h->N = cfg->N;
+  h->bf16 = is_bf16(cfg);
+  h->elem = elem_bytes(cfg);
+  h->lay = lay;
+  if (hipGetDevice(&h->device) != hipSuccess) return fail(FF_ERR_HIP, "hipGetDevice failed");
+  char* ws = (char*)cfg->workspace;
+  h->st = (int*)(ws + lay.off_small);
+  h->c = (double*)(ws + lay.off_small + 64);
+  h->A.tr = (double*)(ws + lay.off_small + 128);
+  h->B.tr = (double*)(ws + lay.off_small + 192);
+  h->ll = (double*)(ws + lay.off_ll);
+  h->delta = (double*)(ws + lay.off_diag);
+  h->dpart = h->delta + kLLCap;
+  h->spart = h->dpart + 8 * kDiagBlocks;
+  h->A.slots = (double*)(ws + lay.off_slotsA);
+  h->B.slots = (double*)(ws + lay.off_slotsB);
+  h->A.nslots = (int)((h->n + kLeaf - 1) / kLeaf);
+  h->B.nslots = (int)((h->m + kLeaf - 1) / kLeaf);
+  h->Gx = lay.own_gx ? (const void*)(ws + lay.off_gx) : cfg->G;
+  h->Gt = ws + lay.off_gt;
+  h->W = ws + lay.off_w;
+  h->P = (float*)(ws + lay.off_p);
+  if (lay.rank1) {
+    h->S = ws + lay.off_s;
+    h->wv = (float*)(ws + lay.off_wv);
+  }
+  auto side = [&](Side& s, const size_t* o, int64_t dim, int64_t dim_p, int splits, int code) {
+    s.dim = dim;
+    s.dim_p = dim_p;
+    s.F[0] = (float*)(ws + o[0]);
+    s.F[1] = (float*)(ws + o[1]);
+    s.L = (float*)(ws + o[2]);
+    s.Li = (float*)(ws + o[3]);
+    s.Lw = ws + o[4];
+    s.Lw2 = h->cfg.whiten_split == 2 ? (void*)(ws + o[5]) : nullptr;
+    s.splits = splits;
+    s.code = code;
+  };
+  side(h->A, lay.off_A, h->n, lay.n_p, lay.splitsA, 1);
+  side(h->B, lay.off_B, h->m, lay.m_p, lay.splitsB, 2);
+  h->A.start_identity = cfg->A0 == nullptr;
+  h->B.start_identity = cfg->B0 == nullptr;
+
+  auto setup = [&]() -> ff_status {
+    FF_HIP(launch_set_int(h->st, 4, 0, h->stream));
+    const int64_t N = h->N, m = h->m, n = h->n;
+    if (lay.rank1) {
+      // tokens as one padded matrix each: x -> T_p x n_p, g -> T_p x m_p
+      FF_HIP(launch_pack(cfg->x, (void*)h->Gx, 1, N, n, lay.T_p, lay.n_p, 0, h->elem, h->stream));
+      FF_HIP(launch_pack(cfg->g, h->Gt, 1, N, m, lay.T_p, lay.m_p, 0, h->elem, h->stream));
+    } else {
+      if (lay.own_gx)
+        FF_HIP(launch_pack(cfg->G, (void*)h->Gx, N, m, n, lay.m_p, lay.n_p, 0, h->elem, h->stream));
+      FF_HIP(launch_pack(cfg->G, h->Gt, N, m, n, lay.n_p, lay.m_p, 1, h->elem, h->stream));
+    }
+    // Upper blocks of L^-1 are never written by the factorisation: zero once.
+    FF_HIP(launch_fill_f32(h->A.Li, n * n, 0.0f, h->stream));
+    FF_HIP(launch_fill_f32(h->B.Li, m * m, 0.0f, h->stream));
+    if (cfg->A0 != nullptr)
+      FF_HIP(hipMemcpyAsync(h->A.F[0], cfg->A0, n * n * sizeof(float), hipMemcpyDeviceToDevice,
+                            h->stream));
+    else
+      FF_HIP(launch_identity_f32(h->A.F[0], n, h->stream));
+    if (cfg->B0 != nullptr)
+      FF_HIP(hipMemcpyAsync(h->B.F[0], cfg->B0, m * m * sizeof(float), hipMemcpyDeviceToDevice,
+                            h->stream));
+    else
+      FF_HIP(launch_identity_f32(h->B.F[0], m, h->stream));
+    return FF_OK;
+  };
+  return setup();
+}
+
 
 // ------------------------------------------------------------ quantiser
 struct QuantLayout {
@@ -849,22 +1039,9 @@ ff_status ff_workspace_size(const ff_config* cfg, size_t* bytes) {
 }
 
 ff_status ff_init(const ff_config* cfg, ff_handle* out) {
-  ff_status rc = validate_shape(cfg);
+  ff_status rc = validate_config(cfg);
   if (rc != FF_OK) return rc;
   if (out == nullptr) return fail(FF_ERR_INVALID_ARG, "out is NULL");
-  if (cfg->form == FF_SAMPLES_RANK1) {
-    if (cfg->x == nullptr || cfg->g == nullptr || ((uintptr_t)cfg->x % 16) != 0 ||
-        ((uintptr_t)cfg->g % 16) != 0)
-      return fail(FF_ERR_INVALID_ARG, "x and g must be non-NULL 16-byte aligned device pointers");
-  } else if (cfg->G == nullptr || ((uintptr_t)cfg->G % 16) != 0) {
-    return fail(FF_ERR_INVALID_ARG, "G must be a non-NULL 16-byte aligned device pointer");
-  }
-  if (cfg->order != FF_ORDER_B_FIRST && cfg->order != FF_ORDER_A_FIRST)
-    return fail(FF_ERR_INVALID_ARG, "unknown order");
-  if (!(cfg->damping >= 0.0) || !isfinite(cfg->damping))
-    return fail(FF_ERR_INVALID_ARG, "damping must be finite and >= 0");
-  if (((uintptr_t)cfg->A0 % 16) != 0 || ((uintptr_t)cfg->B0 % 16) != 0)
-    return fail(FF_ERR_INVALID_ARG, "A0/B0 must be 16-byte aligned");
   const Layout lay = make_layout(cfg);
   if (cfg->workspace == nullptr || ((uintptr_t)cfg->workspace % kAlign) != 0)
     return fail(FF_ERR_WORKSPACE, "workspace must be a non-NULL 256-byte aligned device pointer");
@@ -876,82 +1053,7 @@ ff_status ff_init(const ff_config* cfg, ff_handle* out) {
   }
   ff_handle_s* h = new (std::nothrow) ff_handle_s();
   if (h == nullptr) return fail(FF_ERR_INVALID_ARG, "host allocation of the handle failed");
-  h->cfg = *cfg;
-  if (!is_bf16(cfg)) h->cfg.whiten_split = 1;
-  h->stream = (hipStream_t)cfg->stream;
-  h->m = cfg->m;
-  h->n = cfg->n;
-  h->N = cfg->N;
-  h->bf16 = is_bf16(cfg);
-  h->elem = elem_bytes(cfg);
-  h->lay = lay;
-  if (hipGetDevice(&h->device) != hipSuccess) {
-    delete h;
-    return fail(FF_ERR_HIP, "hipGetDevice failed");
-  }
-  char* ws = (char*)cfg->workspace;
-  h->st = (int*)(ws + lay.off_small);
-  h->c = (double*)(ws + lay.off_small + 64);
-  h->A.tr = (double*)(ws + lay.off_small + 128);
-  h->B.tr = (double*)(ws + lay.off_small + 192);
-  h->ll = (double*)(ws + lay.off_ll);
-  h->A.slots = (double*)(ws + lay.off_slotsA);
-  h->B.slots = (double*)(ws + lay.off_slotsB);
-  h->A.nslots = (int)((h->n + kLeaf - 1) / kLeaf);
-  h->B.nslots = (int)((h->m + kLeaf - 1) / kLeaf);
-  h->Gx = lay.own_gx ? (const void*)(ws + lay.off_gx) : cfg->G;
-  h->Gt = ws + lay.off_gt;
-  h->W = ws + lay.off_w;
-  h->P = (float*)(ws + lay.off_p);
-  if (lay.rank1) {
-    h->S = ws + lay.off_s;
-    h->wv = (float*)(ws + lay.off_wv);
-  }
-  auto side = [&](Side& s, const size_t* o, int64_t dim, int64_t dim_p, int splits, int code) {
-    s.dim = dim;
-    s.dim_p = dim_p;
-    s.F[0] = (float*)(ws + o[0]);
-    s.F[1] = (float*)(ws + o[1]);
-    s.L = (float*)(ws + o[2]);
-    s.Li = (float*)(ws + o[3]);
-    s.Lw = ws + o[4];
-    s.Lw2 = h->cfg.whiten_split == 2 ? (void*)(ws + o[5]) : nullptr;
-    s.splits = splits;
-    s.code = code;
-  };
-  side(h->A, lay.off_A, h->n, lay.n_p, lay.splitsA, 1);
-  side(h->B, lay.off_B, h->m, lay.m_p, lay.splitsB, 2);
-  h->A.start_identity = cfg->A0 == nullptr;
-  h->B.start_identity = cfg->B0 == nullptr;
-
-  auto setup = [&]() -> ff_status {
-    FF_HIP(launch_set_int(h->st, 4, 0, h->stream));
-    const int64_t N = h->N, m = h->m, n = h->n;
-    if (lay.rank1) {
-      // tokens as one padded matrix each: x -> T_p x n_p, g -> T_p x m_p
-      FF_HIP(launch_pack(cfg->x, (void*)h->Gx, 1, N, n, lay.T_p, lay.n_p, 0, h->elem, h->stream));
-      FF_HIP(launch_pack(cfg->g, h->Gt, 1, N, m, lay.T_p, lay.m_p, 0, h->elem, h->stream));
-    } else {
-      if (lay.own_gx)
-        FF_HIP(launch_pack(cfg->G, (void*)h->Gx, N, m, n, lay.m_p, lay.n_p, 0, h->elem, h->stream));
-      FF_HIP(launch_pack(cfg->G, h->Gt, N, m, n, lay.n_p, lay.m_p, 1, h->elem, h->stream));
-    }
-    // Upper blocks of L^-1 are never written by the factorisation: zero once.
-    FF_HIP(launch_fill_f32(h->A.Li, n * n, 0.0f, h->stream));
-    FF_HIP(launch_fill_f32(h->B.Li, m * m, 0.0f, h->stream));
-    if (cfg->A0 != nullptr)
-      FF_HIP(hipMemcpyAsync(h->A.F[0], cfg->A0, n * n * sizeof(float), hipMemcpyDeviceToDevice,
-                            h->stream));
-    else
-      FF_HIP(launch_identity_f32(h->A.F[0], n, h->stream));
-    if (cfg->B0 != nullptr)
-      FF_HIP(hipMemcpyAsync(h->B.F[0], cfg->B0, m * m * sizeof(float), hipMemcpyDeviceToDevice,
-                            h->stream));
-    else
-      FF_HIP(launch_identity_f32(h->B.F[0], m, h->stream));
-    return FF_OK;
-  };
-  rc = setup();
+  rc = init_handle(cfg, lay, h);
   if (rc != FF_OK) {
     delete h;
     return rc;
@@ -961,20 +1063,41 @@ ff_status ff_init(const ff_config* cfg, ff_handle* out) {
 }
 
 ff_status ff_iterate(ff_handle h, int iters, int* iters_done, double* loglik) {
-  if (iters_done != nullptr) *iters_done = 0;
+  return run_iterations(h, iters, 0.0, iters_done, loglik, nullptr);
+}
+
+ff_status ff_iterate_tol(ff_handle h, int max_iters, double tol, int* iters_done, double* loglik,
+                         double* delta) {
+  if (!(tol >= 0.0) || !isfinite(tol)) {
+    if (iters_done != nullptr) *iters_done = 0;
+    return fail(FF_ERR_INVALID_ARG, "tol must be finite and >= 0");
+  }
+  return run_iterations(h, max_iters, tol, iters_done, loglik, delta);
+}
+
+ff_status ff_half_step(ff_handle h, ff_half which, const float* F, float* out) {
   if (h == nullptr) return fail(FF_ERR_INVALID_ARG, "handle is NULL");
-  if (iters < 0) return fail(FF_ERR_INVALID_ARG, "iters must be >= 0");
-  if (h->iters_total + (int64_t)iters > 0x7fffffffLL)
-    return fail(FF_ERR_STATE, "iteration counter overflow");
-  int total = 0;
-  const int cap = h->timing ? 32 : kLLCap;
-  while (total < iters) {
-    const int chunk = std::min(cap, iters - total);
-    int done = 0;
-    ff_status rc = iterate_chunk(h, chunk, &done, loglik ? loglik + total : nullptr);
-    total += done;
-    if (iters_done != nullptr) *iters_done = total;
-    if (rc != FF_OK) return rc;
+  if (which != FF_HALF_B && which != FF_HALF_A) return fail(FF_ERR_INVALID_ARG, "unknown half step");
+  if (h->cfg.estimator != FF_EST_FLIPFLOP && h->cfg.estimator != FF_EST_FROBENIUS)
+    return fail(FF_ERR_INVALID_ARG, "half steps exist for the FlipFlop and Frobenius estimators");
+  if (out == nullptr || ((uintptr_t)out % 16) != 0 || ((uintptr_t)F % 16) != 0)
+    return fail(FF_ERR_INVALID_ARG, "out (and F if given) must be 16-byte aligned device pointers");
+  Side& s = which == FF_HALF_B ? h->B : h->A;  // the factor computed
+  Side& p = which == FF_HALF_B ? h->A : h->B;  // the factor held fixed
+  const float* src = F != nullptr ? F : p.F[h->cur];
+  // the whitening operands no longer belong to the current factors
+  h->A.lw_valid = h->B.lw_valid = false;
+  ff_status rc = h->cfg.estimator == FF_EST_FROBENIUS ? revchol_operand(h, p, src, -1)
+                                                      : cholinv_from(h, p, src, -1);
+  if (rc != FF_OK) return rc;
+  if ((rc = update(h, s, p, 0, false, false, out)) != FF_OK) return rc;
+  int st[4];
+  if ((rc = read_status(h, st)) != FF_OK) return rc;
+  if (st[0] != 0) {
+    if ((rc = clear_status(h)) != FF_OK) return rc;
+    FF_HIP(hipStreamSynchronize(h->stream));
+    return fail(FF_ERR_NOT_SPD, std::string("the fixed factor (") + (st[1] == 1 ? "A" : "B") +
+                                    ") is not positive definite in ff_half_step");
   }
   return FF_OK;
 }

@@ -119,12 +119,28 @@ hipError_t launch_trace_damp(float* F, int64_t dim, double kappa, double* tr, co
 hipError_t launch_normalise(float* FA, int64_t n, float* FB, int64_t m, const double* trA,
                             double* c_out, const int* st, hipStream_t s);
 
-// ll = -(N/2)(m logdetA + n logdetB) - (N m n / 2)(1 + log 2 pi), with
-// logdet = 2 * sum of slots; the side factorised before the normalisation
-// gets its log-determinant corrected by -+ dim * log c.
+// ll = -(N/2)(m logdetA + n logdetB) - T/2 - (N m n / 2) log 2 pi, with
+// logdet = 2 * sum of slots (the side factorised before the normalisation
+// gets its log-determinant corrected by -+ dim * log c) and T the trace
+// term: N m n when kappa = 0, otherwise from the kDiagBlocks partials of
+// launch_sumsq_trace on the second-updated factor (exact under damping).
+constexpr int kDiagBlocks = 256;
 hipError_t launch_loglik(const double* slotsA, int nA, const double* slotsB, int nB,
                          const double* c, int first_is_B, double m, double n, double N,
-                         double* ll_out, const int* st, hipStream_t s);
+                         double kappa, const double* part, double* ll_out, const int* st,
+                         hipStream_t s);
+
+// part[2 b] / part[2 b + 1]: fixed-order partial sums of Li^2 (dim x dim)
+// and of diag(F), b < kDiagBlocks.
+hipError_t launch_sumsq_trace(const float* Li, const float* F, int64_t dim, double* part,
+                              const int* st, hipStream_t s);
+
+// *delta_out = ||A (x) B - Ap (x) Bp||_F / (||Ap||_F ||Bp||_F) in fp64 (part:
+// 8 kDiagBlocks doubles of scratch); with tol > 0 and delta <= tol, st[3] =
+// iteration (the rest of the enqueued pipeline halts).
+hipError_t launch_delta(const float* A, const float* Ap, int64_t nA, const float* B,
+                        const float* Bp, int64_t nB, double* part, double* delta_out, double tol,
+                        int iteration, int* st, hipStream_t s);
 
 // w[r] = sum_j P[r][j] (square = 0) or sum_j P[r][j]^2 (square = 1), rows x cols.
 hipError_t launch_row_sums(const float* P, int64_t rows, int64_t cols, int square, float* w,

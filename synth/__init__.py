@@ -17,13 +17,13 @@ draws the weights and factors the WaterKron quantiser consumes.
 """
 from .generator import (WORKLOADS, Workload, workload, generate, generate_device,
                         power_law_spectrum, haar_orthogonal, f32_to_bf16_bits,
-                        bf16_bits_to_f32)
+                        bf16_bits_to_f32, sample_digests, basis_digest, spd_start)
 from .tokens import (TOKEN_WORKLOADS, TokenWorkload, token_workload, generate_tokens,
                      generate_tokens_device)
 from .quant import QUANT_WORKLOADS, QuantWorkload, quant_workload, generate_quant
 
 __all__ = ["WORKLOADS", "Workload", "workload", "generate", "generate_device",
            "power_law_spectrum", "haar_orthogonal", "f32_to_bf16_bits",
-           "bf16_bits_to_f32", "TOKEN_WORKLOADS", "TokenWorkload", "token_workload",
+           "bf16_bits_to_f32", "sample_digests", "basis_digest", "spd_start", "TOKEN_WORKLOADS", "TokenWorkload", "token_workload",
            "generate_tokens", "generate_tokens_device", "QUANT_WORKLOADS", "QuantWorkload",
            "quant_workload", "generate_quant"]

@@ -153,3 +153,12 @@ def test_estimator_validation(lib):
         c.form = ff.FF_SAMPLES_DENSE
     c.estimator = ff.FF_EST_FROBENIUS
     assert ff.ff_workspace_size(c) == ff.ff_workspace_size(cfg())
+
+
+def test_new_entry_points_validate_handles(lib):
+    with pytest.raises(ff.FlipFlopError) as ei:
+        ff.ff_iterate_tol(None, 3, 1e-3)
+    assert ei.value.code == ff.FF_ERR_INVALID_ARG
+    with pytest.raises(ff.FlipFlopError) as ei:
+        ff.ff_half_step(None, ff.FF_HALF_B, None, 0x1000)
+    assert ei.value.code == ff.FF_ERR_INVALID_ARG

@@ -1,0 +1,154 @@
+"""GPU diagnostics of the iteration against the fp64 oracle: the relative
+change of A (x) B per iteration and the tolerance stop (ff_iterate_tol), the
+log-likelihood under damping (ff_iterate), and single half steps with a
+given fixed factor (ff_half_step), unscaled."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+
+def to_device(G_np, device):
+    import torch
+    if G_np.dtype == np.uint16:
+        return torch.from_numpy(G_np.view(np.int16)).to(device).view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(G_np, dtype=np.float32)).to(device)
+
+
+def oracle_deltas(G, iters, **kw):
+    """kron_rel_error(A_g, B_g, A_{g-1}, B_{g-1}) along the oracle's iterates,
+    the start factors (identity or A0 / B0) before the first."""
+    r = oracle.flipflop(G, iters, keep_history=True, **kw)
+    N, m, n = G.shape
+    prev = (np.eye(n) if kw.get("A0") is None else np.asarray(kw["A0"], np.float64),
+            np.eye(m) if kw.get("B0") is None else np.asarray(kw["B0"], np.float64))
+    out = []
+    for A, B in r.history:
+        out.append(oracle.kron_rel_error(A, B, *prev))
+        prev = (A, B)
+    return np.array(out), r
+
+
+@pytest.mark.parametrize("order", ["B_FIRST", "A_FIRST"])
+def test_relative_change_per_iteration_matches_oracle(gpu, order):
+    import paper_2609_14706_amd as ffe
+    w = synth.workload("tiny")
+    d = synth.generate(w)
+    ref, _ = oracle_deltas(d.G, 12, order=order)
+    f = ffe.FlipFlop(to_device(d.G, gpu), order=order)
+    done, ll, dl = f.iterate_tol(12)
+    f.close()
+    assert done == 12 and len(dl) == 12 and len(ll) == 12
+    dl = np.array(dl)
+    print("device:", dl)
+    print("oracle:", ref)
+    np.testing.assert_allclose(dl, ref, rtol=1e-3, atol=2e-6)
+    assert np.all(np.diff(ref[3:]) < 0)               # the iteration contracts
+
+
+def test_tolerance_stop_at_the_oracles_iteration(gpu):
+    """tol between the oracle's changes at iterations k - 1 and k stops the
+    device after iteration k with the oracle's iterate k; later calls go on
+    from there exactly like an uninterrupted run."""
+    import paper_2609_14706_amd as ffe
+    w = synth.workload("tiny")
+    d = synth.generate(w)
+    ref, r = oracle_deltas(d.G, 20)
+    k = 7
+    tol = float(np.sqrt(ref[k - 2] * ref[k - 1]))     # strictly between changes k - 1 and k
+    assert ref[k - 1] < tol < ref[k - 2]
+    G = to_device(d.G, gpu)
+    f = ffe.FlipFlop(G)
+    done, ll, dl = f.iterate_tol(20, tol)
+    assert done == k and f.iters_done == k and len(dl) == k and len(ll) == k
+    A, B = f.factors()
+    A_k, B_k = r.history[k - 1]
+    assert oracle.kron_rel_error(A.double().cpu().numpy(), B.double().cpu().numpy(), A_k, B_k) < 1e-5
+    ll_more = f.iterate(3)
+    A2, B2 = f.factors()
+    f.close()
+    g = ffe.FlipFlop(G)
+    ll_all = g.iterate(k + 3)
+    A3, B3 = g.factors()
+    g.close()
+    import torch
+    assert torch.equal(A2, A3) and torch.equal(B2, B3)
+    np.testing.assert_array_equal(np.array(ll + ll_more), np.array(ll_all))
+
+
+def test_tolerance_zero_and_invalid(gpu):
+    import paper_2609_14706_amd as ffe
+    d = synth.generate(synth.workload("tiny").scaled(m=20, n=30, N=40))
+    f = ffe.FlipFlop(to_device(d.G, gpu))
+    done, _, dl = f.iterate_tol(4, 0.0)
+    assert done == 4 and all(np.isfinite(dl))
+    for bad in (-1.0, float("nan"), float("inf")):
+        with pytest.raises(ffe.FlipFlopError) as ei:
+            f.iterate_tol(2, bad)
+        assert ei.value.code == ffe.FF_ERR_INVALID_ARG
+    f.close()
+
+
+@pytest.mark.parametrize("order", ["B_FIRST", "A_FIRST"])
+@pytest.mark.parametrize("kappa", [0.0, 0.1, 1.0])
+def test_loglik_exact_with_and_without_damping(gpu, order, kappa):
+    """The device log-likelihood of every iteration equals the oracle's
+    direct evaluation (per-sample Cholesky solves of the full trace term) on
+    the oracle's iterates, damped or not."""
+    import paper_2609_14706_amd as ffe
+    w = synth.workload("tiny").scaled(m=48, n=80, N=40)
+    d = synth.generate(w)
+    iters = 4
+    r = oracle.flipflop(d.G, iters, order=order, damping=kappa, keep_history=True)
+    f = ffe.FlipFlop(to_device(d.G, gpu), order=order, damping=kappa)
+    ll = f.iterate(iters)
+    f.close()
+    ref = np.array([oracle.loglik(d.G, A, B) for A, B in r.history])
+    print(f"kappa {kappa} {order}: device {np.array(ll)} oracle {ref}")
+    np.testing.assert_allclose(np.array(ll), ref, rtol=2e-6)
+
+
+@pytest.mark.parametrize("dtype,tol", [("f32", 1e-5), ("bf16", 5e-3)])
+@pytest.mark.parametrize("shape", [(130, 70, 9), (600, 520, 6)])
+def test_half_step_unscaled_against_oracle(gpu, dtype, tol, shape):
+    """ff_half_step with seeded SPD fixed factors, both sides, every row,
+    unscaled: against the oracle's half steps."""
+    import torch
+    import paper_2609_14706_amd as ffe
+    m, n, N = shape
+    w = synth.workload("attn").scaled(m=m, n=n, N=N, dtype=dtype)
+    d = synth.generate(w)
+    A0, B0 = synth.spd_start(n, 11, rank=16), synth.spd_start(m, 12, rank=16)
+    f = ffe.FlipFlop(to_device(d.G, gpu))
+    Bh = f.half_step("B", torch.from_numpy(A0)).double().cpu().numpy()
+    Ah = f.half_step("A", torch.from_numpy(B0)).double().cpu().numpy()
+    # the handle's factors are untouched and the iteration unaffected
+    ll = f.iterate(2)
+    A, B = f.factors()
+    f.close()
+    G64 = oracle.as_f64_samples(d.G)
+    Bref = oracle.half_step_B(G64, A0.astype(np.float64))
+    Aref = oracle.half_step_A(G64, B0.astype(np.float64))
+    eb = np.linalg.norm(Bh - Bref) / np.linalg.norm(Bref)
+    ea = np.linalg.norm(Ah - Aref) / np.linalg.norm(Aref)
+    print(f"half steps {m}x{n} N={N} {dtype}: B {eb:.2e}, A {ea:.2e}")
+    assert eb < tol and ea < tol
+    ref = oracle.flipflop(d.G, 2)
+    assert oracle.kron_rel_error(A.double().cpu().numpy(), B.double().cpu().numpy(),
+                                 ref.A, ref.B) < tol
+
+
+def test_half_step_rejects_a_singular_fixed_factor(gpu):
+    import torch
+    import paper_2609_14706_amd as ffe
+    d = synth.generate(synth.workload("tiny").scaled(m=20, n=30, N=40))
+    f = ffe.FlipFlop(to_device(d.G, gpu))
+    F = torch.zeros((30, 30), dtype=torch.float32)
+    with pytest.raises(ffe.FlipFlopError) as ei:
+        f.half_step("B", F)
+    assert ei.value.code == ffe.FF_ERR_NOT_SPD
+    f.iterate(2)                                          # the handle stays usable
+    f.close()

@@ -577,3 +577,67 @@ def test_frobenius_tokens_equal_dense_frobenius_on_materialised_samples():
     c = oracle.frobenius_tokens(x, g, 3, order="A_FIRST")
     d = oracle.frobenius(oracle.materialise(x, g), 3, order="A_FIRST")
     np.testing.assert_allclose(c.A, d.A, rtol=1e-11)
+
+
+# ------------------------------------------- row oracles of the half steps
+
+def _block_half_steps(G, A, B):
+    """Both half steps from the explicit second moment H (column-major vec):
+    with H4[j, a, k, b] = E[G_aj G_bk], E[G A^-1 G^T]_ab = sum_jk (A^-1)_jk H4[j,a,k,b]
+    and E[G^T B^-1 G]_jk = sum_ab (B^-1)_ab H4[j,a,k,b]."""
+    N, m, n = G.shape
+    H4 = explicit_H(G).reshape(n, m, n, m)
+    Bh = np.einsum("jk,jakb->ab", np.linalg.inv(A), H4) / n
+    Ah = np.einsum("ab,jakb->jk", np.linalg.inv(B), H4) / m
+    return Ah, Bh
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_half_step_row_oracles_every_row_unscaled(bf16):
+    """The row oracles used at full size give every row of the half steps,
+    unscaled, with a non-identity factor: against the dense half steps and
+    against the explicit Kronecker form; the identity branch against the
+    sample second moment."""
+    rng = np.random.default_rng(31)
+    m, n, N = 7, 5, 9
+    A, B = rand_spd(n, rng, 30.0), rand_spd(m, rng, 20.0)
+    G = matrix_normal(N, A, B, rng)
+    if bf16:
+        G = synth.f32_to_bf16_bits(G.astype(np.float32))
+    G64 = oracle.as_f64_samples(G)
+    A0, B0 = rand_spd(n, rng, 50.0), rand_spd(m, rng, 50.0)
+    rb = oracle.half_step_B_rows(G, A0, np.arange(m))
+    ra = oracle.half_step_A_rows(G, B0, np.arange(n))
+    np.testing.assert_allclose(rb, oracle.half_step_B(G64, A0), rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(ra, oracle.half_step_A(G64, B0), rtol=1e-12, atol=1e-13)
+    Ah, _ = _block_half_steps(G64, np.eye(n), B0)
+    _, Bh = _block_half_steps(G64, A0, np.eye(m))
+    np.testing.assert_allclose(rb, Bh, rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(ra, Ah, rtol=1e-10, atol=1e-12)
+    # a subset of rows in any order, and the identity branch
+    sel = np.array([4, 0, 2])
+    np.testing.assert_allclose(oracle.half_step_B_rows(G, A0, sel), rb[sel], rtol=1e-13)
+    np.testing.assert_allclose(oracle.half_step_A_rows(G, B0, sel), ra[sel], rtol=1e-13)
+    X = G64.transpose(0, 2, 1).reshape(N * n, m)              # stacked G_i^T
+    np.testing.assert_allclose(oracle.half_step_B_rows(G, None, np.arange(m)), X.T @ X / (N * n),
+                               rtol=1e-12)
+    Y = G64.reshape(N * m, n)
+    np.testing.assert_allclose(oracle.half_step_A_rows(G, None, np.arange(n)), Y.T @ Y / (N * m),
+                               rtol=1e-12)
+
+
+def test_token_row_oracle_every_row_unscaled():
+    """Rows of the per-token B half step, unscaled, with a non-identity A and
+    a chunk size that splits the tokens: against the token half step and
+    against the dense row oracle on the materialised samples g_t x_t^T."""
+    rng = np.random.default_rng(32)
+    T, m, n = 57, 6, 4
+    x, g = rng.standard_normal((T, n)), rng.standard_normal((T, m))
+    A0 = rand_spd(n, rng, 40.0)
+    rows = np.arange(m)
+    r = oracle.half_step_B_tokens_rows(x, g, A0, rows, chunk=10)
+    np.testing.assert_allclose(r, oracle.half_step_B_tokens(x, g, A0), rtol=1e-12)
+    Gt = g[:, :, None] * x[:, None, :]
+    np.testing.assert_allclose(r, oracle.half_step_B_rows(Gt, A0, rows), rtol=1e-12)
+    np.testing.assert_allclose(oracle.half_step_B_tokens_rows(x, g, None, rows, chunk=7),
+                               oracle.half_step_B_rows(Gt, None, rows), rtol=1e-12)
