@@ -57,7 +57,10 @@ def test_tolerance_stop_at_the_oracles_iteration(gpu):
     w = synth.workload("tiny")
     d = synth.generate(w)
     ref, r = oracle_deltas(d.G, 20)
-    k = 7
+    # the fp32 iterates fluctuate at ~1e-7 (relative), so the device's changes
+    # bottom out there: stop at the first iteration whose change is below 1e-4
+    k = int(np.argmax(ref < 1e-4)) + 1
+    assert k >= 3 and ref[k - 1] > 1e-6
     tol = float(np.sqrt(ref[k - 2] * ref[k - 1]))     # strictly between changes k - 1 and k
     assert ref[k - 1] < tol < ref[k - 2]
     G = to_device(d.G, gpu)
