@@ -280,6 +280,27 @@ ff_status ff_quantize(ff_handle h, const float* W, const float* A, const float* 
                       double gamma, ff_scale_mode mode, float* alpha, float* beta, int32_t* Z,
                       float* V, double* distortion, void* workspace, size_t workspace_bytes);
 
+/* For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  One call
+ * does what ff_init + ff_iterate + ff_factors(on_host = 0) do, with the same
+ * kernels and results, but takes its scratch from a static device array of
+ * FF_NOALLOC_SCRATCH_BYTES that the library holds on each device it runs on
+ * (until the process ends) instead of a caller workspace, and creates no
+ * streams or events (the factorisation's inverse products run on cfg->stream).
+ * It calls no allocating routine.  cfg: as for ff_init; cfg->workspace and
+ * cfg->workspace_bytes are ignored.  A (n x n) and B (m x m): DEVICE fp32
+ * outputs, tr(A) = n.  iters_done / loglik: as ff_iterate.  The call
+ * synchronises cfg->stream.  Every call on one device shares that device's
+ * array and the set-up rewrites everything it reads, so a call depends on no
+ * earlier one; calls that overlap in time on one device (several host
+ * threads or streams) race and give undefined results.
+ * Errors: FF_ERR_WORKSPACE when ff_workspace_size(cfg) exceeds
+ * FF_NOALLOC_SCRATCH_BYTES (the message gives both sizes), and the errors of
+ * ff_init and ff_iterate. */
+#define FF_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+ff_status ff_fit_noalloc(const ff_config* cfg, int iters, int* iters_done, double* loglik,
+                         float* A, float* B);
+
 /* Release the handle (host memory only; waits for the handle's stream).
  * NULL is accepted. */
 ff_status ff_destroy(ff_handle h);

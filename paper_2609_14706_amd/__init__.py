@@ -12,8 +12,8 @@ from .binding import (FF_APPLY, FF_APPLY_INV, FF_BF16, FF_ERR_HIP, FF_ERR_INVALI
                       FF_ORDER_A_FIRST, FF_ORDER_B_FIRST, FF_SAMPLES_DENSE, FF_SAMPLES_RANK1,
                       FF_SCALES_GIVEN, FF_SCALES_WATERFILL, FF_EST_FLIPFLOP, FF_EST_FROBENIUS,
                       FF_EST_MARGINAL, FF_EST_INPUT, ESTIMATORS, FlipFlop, FlipFlopError, ff_config,
-                      ff_destroy, ff_factors, ff_half_step, ff_init, ff_iterate,
-                      ff_iterate_tol, ff_kernel_timing, FF_HALF_A, FF_HALF_B,
+                      ff_destroy, ff_factors, ff_fit_noalloc, ff_half_step, ff_init, ff_iterate,
+                      ff_iterate_tol, ff_kernel_timing, FF_HALF_A, FF_HALF_B, FF_NOALLOC_SCRATCH_BYTES,
                       ff_kron_apply, ff_last_error, ff_objective, ff_quantize,
                       ff_quantize_workspace_size, ff_set_timing, ff_status_string,
                       ff_workspace_size, header_functions, load_library, LIB_PATH)

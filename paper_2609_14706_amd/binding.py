@@ -22,6 +22,7 @@ FF_SAMPLES_DENSE, FF_SAMPLES_RANK1 = 0, 1
 FF_SCALES_WATERFILL, FF_SCALES_GIVEN = 0, 1
 FF_EST_FLIPFLOP, FF_EST_FROBENIUS, FF_EST_MARGINAL, FF_EST_INPUT = 0, 1, 2, 3
 FF_HALF_B, FF_HALF_A = 0, 1
+FF_NOALLOC_SCRATCH_BYTES = 64 << 20   # include/ff.h
 ESTIMATORS = {"flipflop": FF_EST_FLIPFLOP, "frobenius": FF_EST_FROBENIUS,
               "marginal": FF_EST_MARGINAL, "input": FF_EST_INPUT}
 KERNEL_IDS = {"whiten": 0, "syrk": 1, "reduce": 2, "cholinv": 3, "quant_diag": 4}
@@ -70,6 +71,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "ff_iterate_tol": (st, [H, ctypes.c_int, ctypes.c_double, ctypes.POINTER(ctypes.c_int),
                                 ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
         "ff_half_step": (st, [H, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]),
+        "ff_fit_noalloc": (st, [ctypes.POINTER(ff_config), ctypes.c_int, ctypes.POINTER(ctypes.c_int),
+                                ctypes.POINTER(ctypes.c_double), ctypes.c_void_p, ctypes.c_void_p]),
         "ff_factors": (st, [H, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int]),
         "ff_kron_apply": (st, [H, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int]),
         "ff_objective": (st, [H, ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(ctypes.c_double)]),
@@ -162,6 +165,20 @@ def ff_iterate_tol(h, max_iters: int, tol: float):
 
 def ff_half_step(h, which: int, F_ptr, out_ptr):
     _check(load_library().ff_half_step(h, which, F_ptr, out_ptr))
+
+
+def ff_fit_noalloc(cfg: ff_config, iters: int, A_ptr, B_ptr):
+    """(iterations done, log-likelihoods); cfg.workspace is ignored."""
+    done = ctypes.c_int(0)
+    ll = (ctypes.c_double * max(iters, 1))()
+    code = load_library().ff_fit_noalloc(ctypes.byref(cfg), iters, ctypes.byref(done), ll, A_ptr,
+                                         B_ptr)
+    lls = list(ll[:done.value])
+    if code != FF_OK:
+        err = FlipFlopError(code, ff_last_error(), done.value)
+        err.loglik = lls
+        raise err
+    return done.value, lls
 
 
 def ff_factors(h, A_ptr: int, B_ptr: int, on_host: int):

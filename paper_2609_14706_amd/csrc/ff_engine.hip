@@ -1013,6 +1013,36 @@ bool finite_positive(const float* dev, int64_t count, hipStream_t stream, std::s
 
 }  // namespace
 
+// ================================================= allocation-free scratch
+// Device scratch of ff_fit_noalloc, for callers that cannot allocate device
+// memory.  Each device the library runs on holds its own copy until the
+// process ends.  In host code `scratch` is only a stand-in for the symbol:
+// its device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[FF_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Address of the current device's copy of `scratch`.
+ff_status scratch_on_current_device(void** out) {
+  int dev = 0;
+  FF_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(FF_ERR_INVALID_ARG, "device index out of range");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    FF_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (p == nullptr || ((uintptr_t)p % kAlign) != 0)
+      return fail(FF_ERR_HIP, "device scratch has no usable address");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return FF_OK;
+}
+}  // namespace
+
 // ====================================================================== ABI
 extern "C" {
 
@@ -1064,6 +1094,43 @@ ff_status ff_init(const ff_config* cfg, ff_handle* out) {
 
 ff_status ff_iterate(ff_handle h, int iters, int* iters_done, double* loglik) {
   return run_iterations(h, iters, 0.0, iters_done, loglik, nullptr);
+}
+
+ff_status ff_fit_noalloc(const ff_config* cfg, int iters, int* iters_done, double* loglik,
+                         float* A, float* B) {
+  if (iters_done != nullptr) *iters_done = 0;
+  ff_status rc = validate_config(cfg);
+  if (rc != FF_OK) return rc;
+  if (iters < 0) return fail(FF_ERR_INVALID_ARG, "iters must be >= 0");
+  if (A == nullptr || B == nullptr || ((uintptr_t)A % 16) != 0 || ((uintptr_t)B % 16) != 0)
+    return fail(FF_ERR_INVALID_ARG, "A and B must be non-NULL 16-byte aligned device pointers");
+  const Layout lay = make_layout(cfg);
+  if (lay.total > (size_t)FF_NOALLOC_SCRATCH_BYTES) {
+    char msg[192];
+    snprintf(msg, sizeof msg,
+             "problem needs %zu bytes of scratch; the allocation-free entry point holds %zu "
+             "(use ff_init with a workspace)", lay.total, (size_t)FF_NOALLOC_SCRATCH_BYTES);
+    return fail(FF_ERR_WORKSPACE, msg);
+  }
+  void* ws = nullptr;
+  if ((rc = scratch_on_current_device(&ws)) != FF_OK) return rc;
+  ff_config c = *cfg;
+  c.workspace = ws;
+  c.workspace_bytes = FF_NOALLOC_SCRATCH_BYTES;
+  // The handle lives on this stack frame; with one stream and no timing it
+  // creates no streams or events, so there is nothing to release.
+  ff_handle_s h;
+  h.single_stream = true;
+  if ((rc = init_handle(&c, lay, &h)) != FF_OK) return rc;
+  rc = run_iterations(&h, iters, 0.0, iters_done, loglik, nullptr);
+  if (rc == FF_OK) {
+    FF_HIP(hipMemcpyAsync(A, h.A.F[h.cur], h.n * h.n * sizeof(float), hipMemcpyDeviceToDevice,
+                          h.stream));
+    FF_HIP(hipMemcpyAsync(B, h.B.F[h.cur], h.m * h.m * sizeof(float), hipMemcpyDeviceToDevice,
+                          h.stream));
+  }
+  FF_HIP(hipStreamSynchronize(h.stream));
+  return rc;
 }
 
 ff_status ff_iterate_tol(ff_handle h, int max_iters, double tol, int* iters_done, double* loglik,

@@ -155,6 +155,31 @@ def test_estimator_validation(lib):
     assert ff.ff_workspace_size(c) == ff.ff_workspace_size(cfg())
 
 
+def test_noalloc_entry_rejects_oversized_problems_before_any_device_call(lib):
+    import paper_2609_14706_amd as ffe
+    c = cfg(4096, 4096, 128, ff.FF_BF16)
+    c.G = 0x100000                                        # never dereferenced
+    assert ff.ff_workspace_size(c) > ffe.FF_NOALLOC_SCRATCH_BYTES
+    with pytest.raises(ff.FlipFlopError) as ei:
+        ff.ff_fit_noalloc(c, 1, 0x200000, 0x300000)
+    assert ei.value.code == ff.FF_ERR_WORKSPACE
+    assert "bytes of scratch" in str(ei.value)
+    with pytest.raises(ff.FlipFlopError) as ei:          # outputs are checked first
+        ff.ff_fit_noalloc(c, 1, 0, 0)
+    assert ei.value.code == ff.FF_ERR_INVALID_ARG
+
+
+def test_noalloc_scratch_size_matches_the_header(lib):
+    import re
+    import paper_2609_14706_amd as ffe
+    from paper_2609_14706_amd.binding import HEADER
+    text = open(HEADER).read()
+    mo = re.search(r"#define FF_NOALLOC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", text)
+    assert mo and int(mo.group(1)) << int(mo.group(2)) == ffe.FF_NOALLOC_SCRATCH_BYTES
+    # the tiny workload fits, the headline one does not
+    assert ff.ff_workspace_size(cfg(64, 128, 256)) < ffe.FF_NOALLOC_SCRATCH_BYTES
+
+
 def test_new_entry_points_validate_handles(lib):
     with pytest.raises(ff.FlipFlopError) as ei:
         ff.ff_iterate_tol(None, 3, 1e-3)
