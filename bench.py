@@ -250,7 +250,8 @@ def main():
                     help="tiny | attn | mlp_up | mlp_down | mlp_large | tokens_tiny | tokens_attn"
                          " | quant_small | quant_multi | quant_attn")
     ap.add_argument("--seed", type=int, default=None)
-    ap.add_argument("--whiten-split", type=int, default=1)
+    ap.add_argument("--whiten-split", type=int, default=0,
+                    help="0 = automatic (per factorisation), 1 = one bf16 pass, 2 = hi + lo passes")
     ap.add_argument("--estimator", default="flipflop",
                     help="flipflop | frobenius | marginal | input (Table 1; the last two need tokens)")
     ap.add_argument("--damping", type=float, default=0.0, help="kappa (Appendix B damping)")
@@ -370,7 +371,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "m": w.m, "n": w.n, ("T" if tokens else "N"): N,
                    "timed_job": f"{args.steps} iterations after {warm} untimed on the same handle",
-                   "whiten_split": args.whiten_split, "estimator": args.estimator,
+                   "whiten_split": {0: "auto", 1: 1, 2: 2}[args.whiten_split], "estimator": args.estimator,
                    "damping": args.damping},
         "tflops": round(tflops, 2),
         "pct_peak": round(100.0 * tflops / peak, 2),

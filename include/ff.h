@@ -123,9 +123,19 @@ typedef struct {
                              NULL = I_n.  Copied at ff_init */
   const float* B0;        /* optional DEVICE m x m SPD start for B (A_FIRST);
                              NULL = I_m.  Copied at ff_init */
-  int whiten_split;       /* FF_BF16 only: 1 = L^-1 rounded to bf16 once;
+  int whiten_split;       /* FF_BF16 only.  0 = automatic (the default of a
+                             zeroed config): each factorisation computes on
+                             the device the rounding sensitivity
+                             s = (1/dim) sum_j F_jj (F^-1)_jj of its factor F
+                             (from the column norms of L^-1; rms whitening
+                             distortion 2^-9 sqrt(s/3)); the whitenings use
+                             two passes while the latest s of A or of B
+                             exceeds 16, one pass otherwise;
+                             1 = L^-1 rounded to bf16 once;
                              2 = L^-1 split as hi + lo bf16 parts (two passes,
-                             smaller whitening error).  Ignored for FF_F32 */
+                             smaller whitening error).  The Frobenius
+                             estimator's operand is not an inverse: automatic
+                             means one pass there.  Ignored for FF_F32 */
   void* workspace;        /* DEVICE scratch, 256-byte aligned, owned by the
                              caller, >= ff_workspace_size() bytes; must stay
                              valid until ff_destroy */
@@ -304,6 +314,16 @@ ff_status ff_fit_noalloc(const ff_config* cfg, int iters, int* iters_done, doubl
 /* Release the handle (host memory only; waits for the handle's stream).
  * NULL is accepted. */
 ff_status ff_destroy(ff_handle h);
+
+/* State of the automatic whitening split (whiten_split = 0): the statistic
+ * s of the latest factorisation of A and of B (NaN when not computed: fp32
+ * path, forced split, Frobenius estimator, or no factorisation of that side
+ * yet) and the passes (1 or 2) the next whitening with each side's operand
+ * uses (the same for both sides under the automatic rule; as configured for
+ * a forced split).  Synchronises the handle's stream.  Any pointer may be
+ * NULL.  Errors: FF_ERR_INVALID_ARG, FF_ERR_HIP. */
+ff_status ff_whiten_split_state(ff_handle h, double* s_A, double* s_B, int* passes_A,
+                                int* passes_B);
 
 /* Measurement hook (not needed for estimation).  With timing enabled,
  * ff_iterate and ff_quantize bracket each launch of the main kernels with HIP

@@ -16,6 +16,7 @@ from .binding import (FF_APPLY, FF_APPLY_INV, FF_BF16, FF_ERR_HIP, FF_ERR_INVALI
                       ff_iterate_tol, ff_kernel_timing, FF_HALF_A, FF_HALF_B, FF_NOALLOC_SCRATCH_BYTES,
                       ff_kron_apply, ff_last_error, ff_objective, ff_quantize,
                       ff_quantize_workspace_size, ff_set_timing, ff_status_string,
+                      ff_whiten_split_state,
                       ff_workspace_size, header_functions, load_library, LIB_PATH)
 
 __all__ = [n for n in dir() if not n.startswith("_")]

@@ -83,6 +83,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                              ctypes.c_void_p, ctypes.POINTER(ctypes.c_double), ctypes.c_void_p,
                              ctypes.c_size_t]),
         "ff_destroy": (st, [H]),
+        "ff_whiten_split_state": (st, [H, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
+                                       ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_int)]),
         "ff_set_timing": (st, [H, ctypes.c_int]),
         "ff_kernel_timing": (st, [H, ctypes.c_int, ctypes.POINTER(ctypes.c_int64),
                                   ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
@@ -213,6 +215,14 @@ def ff_destroy(h):
     _check(load_library().ff_destroy(h))
 
 
+def ff_whiten_split_state(h):
+    sA, sB = ctypes.c_double(), ctypes.c_double()
+    pA, pB = ctypes.c_int(), ctypes.c_int()
+    _check(load_library().ff_whiten_split_state(h, ctypes.byref(sA), ctypes.byref(sB),
+                                                 ctypes.byref(pA), ctypes.byref(pB)))
+    return sA.value, sB.value, pA.value, pB.value
+
+
 def ff_set_timing(h, enable: bool):
     _check(load_library().ff_set_timing(h, 1 if enable else 0))
 
@@ -234,13 +244,14 @@ class FlipFlop:
     """
 
     def __init__(self, G=None, *, tokens=None, order: str = "B_FIRST", damping: float = 0.0,
-                 A0=None, B0=None, whiten_split: int = 1, stream=None, workspace=None,
+                 A0=None, B0=None, whiten_split: int = 0, stream=None, workspace=None,
                  estimator: str = "flipflop"):
         """G: (N, m, n) samples; or tokens = (x, g) with x (N, n) inputs and
         g (N, m) output gradients, the samples being G_t = g_t x_t^T (the
         rank-one form; both tensors of one dtype).  estimator: "flipflop",
         "frobenius", "marginal" or "input" (Table 1; the last two need
-        tokens)."""
+        tokens).  whiten_split (bf16 samples): 0 = automatic per
+        factorisation, 1 = one bf16 pass, 2 = hi + lo passes."""
         import torch
         if (G is None) == (tokens is None):
             raise ValueError("give either G or tokens=(x, g)")
@@ -312,7 +323,7 @@ class FlipFlop:
         self.iters_done = 0
 
     @staticmethod
-    def workspace_bytes(m: int, n: int, N: int, dtype: str = "bf16", whiten_split: int = 1,
+    def workspace_bytes(m: int, n: int, N: int, dtype: str = "bf16", whiten_split: int = 0,
                         rank1: bool = False) -> int:
         """Bytes a caller-provided workspace tensor needs (alignment slack included)."""
         cfg = ff_config()
@@ -453,6 +464,11 @@ class FlipFlop:
     def quantize_workspace_bytes(m: int, n: int) -> int:
         """Bytes a caller-provided quantiser workspace tensor needs (slack included)."""
         return ff_quantize_workspace_size(m, n) + 256
+
+    def whiten_split_state(self):
+        """(s_A, s_B, passes_A, passes_B) of the most recent whitening operands
+        (automatic split; s is NaN where it was not computed)."""
+        return ff_whiten_split_state(self.h)
 
     def set_timing(self, enable: bool = True):
         ff_set_timing(self.h, enable)

@@ -171,18 +171,78 @@ __global__ __launch_bounds__(256) void k_scale_transpose_16(const bf16_t* __rest
 }
 
 // --------------------------------------------------------- inverse convert
+// Thread (column j, row chunk y) converts rows [y rch, (y + 1) rch) of
+// column j: coalesced along each row.  With part non-null it also writes,
+// per workgroup, part[y][x] = sum over its 256 columns j of
+// F_jj * (sum over its rows of Li[i][j]^2): the chunk's share of
+// sum_j F_jj (F^-1)_jj, since (F^-1)_jj is the squared norm of column j of
+// L^-1.
 template <typename T>
 __global__ __launch_bounds__(256) void k_convert_inverse(const float* __restrict__ Li, int64_t dim,
                                                          T* __restrict__ Lw, T* __restrict__ Lw2,
-                                                         int64_t dim_p, const int* st) {
+                                                         int64_t dim_p, int64_t rch,
+                                                         const float* __restrict__ F,
+                                                         double* __restrict__ part, const int* st) {
   if (ff_halted(st)) return;
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= dim_p * dim_p) return;
-  const int64_t i = idx / dim_p, j = idx % dim_p;
-  const float v = (i < dim && j <= i) ? Li[i * dim + j] : 0.0f;
-  const T hi = Elem<T>::from_f32(v);
-  Lw[idx] = hi;
-  if (Lw2 != nullptr) Lw2[idx] = Elem<T>::from_f32(v - Elem<T>::to_f32(hi));
+  __shared__ double red[256];
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  float acc = 0.0f;
+  if (j < dim_p) {
+    const int64_t i0 = (int64_t)blockIdx.y * rch, i1 = i0 + rch < dim_p ? i0 + rch : dim_p;
+    constexpr int U = 8;
+    for (int64_t i = i0; i < i1; i += U) {
+      float v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t r = i + u;
+        v[u] = (r < i1 && r < dim && j <= r) ? Li[r * dim + j] : 0.0f;
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t r = i + u;
+        if (r >= i1) break;
+        acc += v[u] * v[u];
+        const T hi = Elem<T>::from_f32(v[u]);
+        Lw[r * dim_p + j] = hi;
+        if (Lw2 != nullptr) Lw2[r * dim_p + j] = Elem<T>::from_f32(v[u] - Elem<T>::to_f32(hi));
+      }
+    }
+  }
+  if (part == nullptr) return;
+  red[threadIdx.x] = j < dim ? (double)F[j * dim + j] * (double)acc : 0.0;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) part[(int64_t)blockIdx.y * gridDim.x + blockIdx.x] = red[0];
+}
+
+// Rounding sensitivity of the whitening operand L^-1 of F:
+//   s = (1/dim) sum_j F_jj (F^-1)_jj   (the sum of the npart partials).
+// Rounding L^-1 to bf16 with independent relative errors of rms u/sqrt(3)
+// (u = 2^-9) perturbs L^-1 L = I by R with E||R||_F^2 = (u^2/3) sum_j
+// F_jj (F^-1)_jj, an rms distortion of the whitened metric of
+// u sqrt(s/3) per direction.  flag = 1 (whiten with the hi + lo parts) when
+// s > threshold; out[0] = s.  One workgroup, fixed summation order.
+__global__ __launch_bounds__(256) void k_split_decide(const double* __restrict__ part, int64_t npart,
+                                                      int64_t dim, double threshold, int* flag,
+                                                      double* out, const int* st) {
+  if (ff_halted(st)) return;
+  __shared__ double red[256];
+  double acc = 0.0;
+  for (int64_t k = threadIdx.x; k < npart; k += 256) acc += part[k];
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const double sv = red[0] / (double)dim;
+    out[0] = sv;
+    flag[0] = sv > threshold ? 1 : 0;
+  }
 }
 
 // ---------------------------------------------------------- trace, damping
@@ -491,18 +551,34 @@ hipError_t launch_scale_transpose(const void* M, const float* w, int64_t rows_p,
   return hipGetLastError();
 }
 
+int64_t convert_parts(int64_t dim_p) {
+  const int64_t nchunk = dim_p < kConvertChunks ? dim_p : kConvertChunks;
+  const int64_t rch = (dim_p + nchunk - 1) / nchunk;
+  return ((dim_p + 255) / 256) * ((dim_p + rch - 1) / rch);
+}
+
 hipError_t launch_convert_inverse(const float* Li, int64_t dim, void* Lw, void* Lw2, int64_t dim_p,
-                                  int elem_bytes, const int* st, hipStream_t s) {
+                                  int elem_bytes, const float* F, double* part, const int* st,
+                                  hipStream_t s) {
   if (dim < 1 || dim_p < dim) return hipErrorInvalidValue;
-  const uint32_t blocks = (uint32_t)((dim_p * dim_p + 255) / 256);
+  const int64_t nchunk = dim_p < kConvertChunks ? dim_p : kConvertChunks;
+  const int64_t rch = (dim_p + nchunk - 1) / nchunk;
+  const dim3 grid((uint32_t)((dim_p + 255) / 256), (uint32_t)((dim_p + rch - 1) / rch));
   if (elem_bytes == 2)
-    hipLaunchKernelGGL(k_convert_inverse<bf16_t>, dim3(blocks), dim3(256), 0, s, Li, dim,
-                       (bf16_t*)Lw, (bf16_t*)Lw2, dim_p, st);
+    hipLaunchKernelGGL(k_convert_inverse<bf16_t>, grid, dim3(256), 0, s, Li, dim, (bf16_t*)Lw,
+                       (bf16_t*)Lw2, dim_p, rch, F, part, st);
   else if (elem_bytes == 4)
-    hipLaunchKernelGGL(k_convert_inverse<float>, dim3(blocks), dim3(256), 0, s, Li, dim, (float*)Lw,
-                       (float*)Lw2, dim_p, st);
+    hipLaunchKernelGGL(k_convert_inverse<float>, grid, dim3(256), 0, s, Li, dim, (float*)Lw,
+                       (float*)Lw2, dim_p, rch, F, part, st);
   else
     return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_split_decide(const double* part, int64_t dim, int64_t dim_p, double threshold,
+                               int* flag, double* out, const int* st, hipStream_t s) {
+  hipLaunchKernelGGL(k_split_decide, dim3(1), dim3(256), 0, s, part, convert_parts(dim_p), dim,
+                     threshold, flag, out, st);
   return hipGetLastError();
 }
 

@@ -58,7 +58,11 @@ struct Side {
   float* L = nullptr;                // Cholesky work copy
   float* Li = nullptr;               // L^-1 (fp32, lower)
   void* Lw = nullptr;                // whitening operand (elem, dim_p x dim_p)
-  void* Lw2 = nullptr;               // its low bf16 part (whiten_split = 2)
+  void* Lw2 = nullptr;               // its low bf16 part (whiten_split = 2 or automatic)
+  int* split_flag = nullptr;         // automatic split: 1 = whiten with hi + lo parts
+  double* split_stat = nullptr;      // automatic split: the rounding sensitivity s of Lw
+  double* spart = nullptr;           // automatic split: partial sums of its statistic
+  bool stat_known = false;           // automatic split: split_stat has been written
   double* slots = nullptr;           // per-leaf sum log L_jj
   int nslots = 0;
   double* tr = nullptr;              // trace after the last update
@@ -83,7 +87,7 @@ struct Layout {
   // w = row-norm partials (bf16) or whitened tokens (fp32), s = weighted
   // transposed tokens, wv = token weights (2 T_p floats)
   size_t off_small, off_ll, off_diag, off_slotsA, off_slotsB, off_gx, off_gt, off_w, off_p, off_s,
-      off_wv;
+      off_wv, off_split;
   size_t w_bytes;  // capacity of the w region
   size_t off_A[6], off_B[6];  // F0, F1, L, Li, Lw, Lw2
   size_t total;
@@ -142,8 +146,8 @@ ff_status validate_shape(const ff_config* c) {
     return fail(FF_ERR_INVALID_ARG, "the Marginal and Input estimators need the rank-one form");
   if (c->m > (1 << 20) || c->n > (1 << 20))
     return fail(FF_ERR_INVALID_ARG, "m and n must be <= 1048576");
-  if (is_bf16(c) && c->whiten_split != 1 && c->whiten_split != 2)
-    return fail(FF_ERR_INVALID_ARG, "whiten_split must be 1 or 2");
+  if (is_bf16(c) && c->whiten_split != 0 && c->whiten_split != 1 && c->whiten_split != 2)
+    return fail(FF_ERR_INVALID_ARG, "whiten_split must be 0 (automatic), 1 or 2");
   return FF_OK;
 }
 
@@ -201,7 +205,12 @@ Layout make_layout(const ff_config* c) {
     L.partialA = (size_t)L.splitsA * L.n_p * L.n_p;
   }
   L.off_p = take(sizeof(float) * std::max(L.partialA, L.partialB));
-  const bool split2 = is_bf16(c) && c->whiten_split == 2;
+  const bool split2 = is_bf16(c) && c->whiten_split != 1;  // 2, or automatic
+  // automatic split: per side a flag and its statistic (256 bytes) and the
+  // statistic's partial sums
+  L.off_split = split2 && c->whiten_split == 0
+                    ? take(2 * (kAlign + align_up(sizeof(double) * convert_parts(dmax))))
+                    : 0;
   auto side = [&](size_t* o, int64_t dim, int64_t dim_p) {
     const size_t fb = (size_t)dim * dim * sizeof(float);
     o[0] = take(fb);
@@ -405,6 +414,15 @@ ff_status inverse_p1_split(ff_handle_s* h, Side& s, int64_t o, int64_t sz, int64
 // after the last leaf is the factorisation's tail.  The upper triangle of
 // s.L is scratch.
 constexpr int64_t kInvEvery = 8;
+// Automatic split (whiten_split = 0): whiten with the hi + lo bf16 parts of
+// L^-1 while s = (1/dim) sum_j F_jj (F^-1)_jj of either factor exceeds this,
+// i.e. when the rms distortion 2^-9 sqrt(s/3) of the whitened metric by the
+// bf16 rounding of that factor's L^-1 would exceed about 4.5e-3.  Measured (bf16 against fp32 / split 2 after the
+// workloads' iteration counts): the 4096 x 4096 layer (s(A) = 6.1) 2.5e-4,
+// 11008 x 4096 (7.4) 4.2e-4, 4096 x 11008 (13) 3.5e-4 with one pass; the
+// 8192 x 28672 layer (s(A) = 21) 2.4e-3 and a 512 x 1280 layer from 4 samples
+// (s(A) up to 26) 7.9e-3 with one pass, which the second pass removes.
+constexpr double kSplitThreshold = 16.0;
 constexpr int64_t kTwoLevel = 6144;
 constexpr int64_t kOuter = 2048;
 
@@ -488,7 +506,13 @@ ff_status cholinv_from(ff_handle_s* h, Side& s, const float* src, int iteration)
   FF_HIP(launch_copy_f32(src, s.L, s.dim * s.dim, h->st, h->stream));
   ff_status rc = chol_blocked(h, s, iteration);
   if (rc != FF_OK) return rc;
-  FF_HIP(launch_convert_inverse(s.Li, s.dim, s.Lw, s.Lw2, s.dim_p, h->elem, h->st, h->stream));
+  FF_HIP(launch_convert_inverse(s.Li, s.dim, s.Lw, s.Lw2, s.dim_p, h->elem, src, s.spart, h->st,
+                                h->stream));
+  if (s.split_flag != nullptr) {
+    FF_HIP(launch_split_decide(s.spart, s.dim, s.dim_p, kSplitThreshold, s.split_flag,
+                               s.split_stat, h->st, h->stream));
+    s.stat_known = true;
+  }
   return FF_OK;
 }
 
@@ -506,7 +530,8 @@ ff_status revchol_operand(ff_handle_s* h, Side& s, const float* src, int iterati
   ff_status rc = chol_blocked(h, s, iteration);
   if (rc != FF_OK) return rc;
   FF_HIP(launch_rev_transpose(s.L, s.dim, s.Li, h->st, h->stream));
-  FF_HIP(launch_convert_inverse(s.Li, s.dim, s.Lw, s.Lw2, s.dim_p, h->elem, h->st, h->stream));
+  FF_HIP(launch_convert_inverse(s.Li, s.dim, s.Lw, s.Lw2, s.dim_p, h->elem, nullptr, nullptr,
+                                h->st, h->stream));
   return FF_OK;
 }
 
@@ -514,6 +539,26 @@ ff_status revchol_operand(ff_handle_s* h, Side& s, const float* src, int iterati
 ff_status operand(ff_handle_s* h, Side& s, int slot, int iteration) {
   if (h->cfg.estimator == FF_EST_FROBENIUS) return revchol_operand(h, s, s.F[slot], iteration);
   return cholinv(h, s, slot, iteration);
+}
+
+// The low bf16 part of side p's whitening operand for the whitening kernels
+// (nullptr: one pass) and, with the automatic split, the two device flags
+// (one per factor) that decide between one and two passes: two when either
+// factor's latest statistic is above the threshold.  The distortion of the
+// whitening by p's operand goes into the update of the other factor, whose
+// own conditioning then amplifies it in its small eigenvalues (an
+// 8192 x 28672 layer with s(A) = 21 and s(B) = 2.3 keeps a flat likelihood
+// only with both whitenings split).  The Frobenius operand is not an inverse,
+// so the statistic does not apply to it: one pass.
+const bf16_t* second_part(const ff_handle_s* h, const Side& p, const int** use2,
+                          const int** use2b) {
+  *use2 = *use2b = nullptr;
+  if (p.Lw2 == nullptr) return nullptr;
+  if (h->cfg.whiten_split == 2) return (const bf16_t*)p.Lw2;
+  if (h->cfg.estimator == FF_EST_FROBENIUS) return nullptr;
+  *use2 = h->A.split_flag;
+  *use2b = h->B.split_flag;
+  return (const bf16_t*)p.Lw2;
 }
 
 // Rank-one form: token weights wbuf[t] = ||L_p^-1 v_t||^2 for the token
@@ -524,7 +569,9 @@ ff_status token_weights(ff_handle_s* h, Side& p, float* wbuf) {
   const double wflop = (double)h->N * p.dim * p.dim;
   Timed t(h, 0, wflop);
   if (h->bf16) {
-    FF_HIP(launch_whiten_norm_bf16((const bf16_t*)V, (const bf16_t*)p.Lw, (const bf16_t*)p.Lw2,
+    const int *use2 = nullptr, *use2b = nullptr;
+    const bf16_t* Y2 = second_part(h, p, &use2, &use2b);
+    FF_HIP(launch_whiten_norm_bf16((const bf16_t*)V, (const bf16_t*)p.Lw, Y2, use2, use2b,
                                    (float*)h->W, T_p, Kp, h->st, h->stream));
     FF_HIP(launch_row_sums((const float*)h->W, T_p, 2 * (Kp / kTileBF16), 0, wbuf, h->st,
                            h->stream));
@@ -615,7 +662,9 @@ ff_status update(ff_handle_s* h, Side& s, Side& p, int slot, bool finish = true,
   if (h->bf16) {
     if (!p_identity) {
       Timed t(h, 0, wflop);
-      FF_HIP(launch_whiten_bf16((const bf16_t*)X, (const bf16_t*)p.Lw, (const bf16_t*)p.Lw2,
+      const int *use2 = nullptr, *use2b = nullptr;
+      const bf16_t* Y2 = second_part(h, p, &use2, &use2b);
+      FF_HIP(launch_whiten_bf16((const bf16_t*)X, (const bf16_t*)p.Lw, Y2, use2, use2b,
                                 (bf16_t*)h->W, rows, Kp, h->st, h->stream));
     }
     {
@@ -901,7 +950,14 @@ ff_status init_handle(const ff_config* cfg, const Layout& lay, ff_handle_s* h) {
     s.L = (float*)(ws + o[2]);
     s.Li = (float*)(ws + o[3]);
     s.Lw = ws + o[4];
-    s.Lw2 = h->cfg.whiten_split == 2 ? (void*)(ws + o[5]) : nullptr;
+    s.Lw2 = h->bf16 && h->cfg.whiten_split != 1 ? (void*)(ws + o[5]) : nullptr;
+    if (h->bf16 && h->cfg.whiten_split == 0) {
+      const int64_t dmax = std::max(lay.m_p, lay.n_p);
+      char* b = ws + lay.off_split + (code - 1) * (kAlign + align_up(sizeof(double) * convert_parts(dmax)));
+      s.split_flag = (int*)b;
+      s.split_stat = (double*)(b + 64);
+      s.spart = (double*)(b + kAlign);
+    }
     s.splits = splits;
     s.code = code;
   };
@@ -921,6 +977,11 @@ ff_status init_handle(const ff_config* cfg, const Layout& lay, ff_handle_s* h) {
       if (lay.own_gx)
         FF_HIP(launch_pack(cfg->G, (void*)h->Gx, N, m, n, lay.m_p, lay.n_p, 0, h->elem, h->stream));
       FF_HIP(launch_pack(cfg->G, h->Gt, N, m, n, lay.n_p, lay.m_p, 1, h->elem, h->stream));
+    }
+    // automatic split: no factor is known to need the second pass yet
+    if (h->A.split_flag != nullptr) {
+      FF_HIP(launch_set_int(h->A.split_flag, 1, 0, h->stream));
+      FF_HIP(launch_set_int(h->B.split_flag, 1, 0, h->stream));
     }
     // Upper blocks of L^-1 are never written by the factorisation: zero once.
     FF_HIP(launch_fill_f32(h->A.Li, n * n, 0.0f, h->stream));
@@ -1476,6 +1537,35 @@ ff_status ff_set_timing(ff_handle h, int enable) {
     h->t_ms[k] = 0;
     h->t_flop[k] = 0;
   }
+  return FF_OK;
+}
+
+ff_status ff_whiten_split_state(ff_handle h, double* s_A, double* s_B, int* passes_A,
+                                int* passes_B) {
+  if (h == nullptr) return fail(FF_ERR_INVALID_ARG, "handle is NULL");
+  double sv[2] = {NAN, NAN};
+  int passes = 1;
+  if (h->bf16 && h->A.Lw2 != nullptr) {
+    if (h->cfg.whiten_split == 2) {
+      passes = 2;
+    } else if (h->cfg.estimator != FF_EST_FROBENIUS && h->A.split_flag != nullptr) {
+      int flag[2] = {0, 0};
+      const Side* sides[2] = {&h->A, &h->B};
+      for (int k = 0; k < 2; ++k) {
+        FF_HIP(hipMemcpyAsync(&flag[k], sides[k]->split_flag, sizeof(int), hipMemcpyDeviceToHost,
+                              h->stream));
+        if (sides[k]->stat_known)
+          FF_HIP(hipMemcpyAsync(&sv[k], sides[k]->split_stat, sizeof(double),
+                                hipMemcpyDeviceToHost, h->stream));
+      }
+      FF_HIP(hipStreamSynchronize(h->stream));
+      passes = (flag[0] || flag[1]) ? 2 : 1;
+    }
+  }
+  if (s_A) *s_A = sv[0];
+  if (s_B) *s_B = sv[1];
+  if (passes_A) *passes_A = passes;
+  if (passes_B) *passes_B = passes;
   return FF_OK;
 }
 

@@ -16,17 +16,21 @@ typedef uint16_t bf16_t;
 constexpr int kTileBF16 = 256;
 
 // Whitening (triangular product, bf16 matrix cores, fp32 accumulation):
-//   C[r][c] = sum_{k <= c} X[r][k] * Y[c][k]  (+ same with Y2 when non-null)
+//   C[r][c] = sum_{k <= c} X[r][k] * Y[c][k]  (+ same with Y2 when non-null
+//   and, if use2 is non-null, *use2 != 0 or *use2b != 0 (use2b may be null):
+//   flags read on the device at launch)
 // X: rows x Kp, Y/Y2: Kp x Kp lower triangular, C: rows x Kp, all row-major
 // bf16 with leading dimension Kp.  rows and Kp are multiples of 256.
-hipError_t launch_whiten_bf16(const bf16_t* X, const bf16_t* Y, const bf16_t* Y2, bf16_t* C,
-                              int64_t rows, int64_t Kp, const int* st, hipStream_t s);
+hipError_t launch_whiten_bf16(const bf16_t* X, const bf16_t* Y, const bf16_t* Y2, const int* use2,
+                              const int* use2b, bf16_t* C, int64_t rows, int64_t Kp, const int* st,
+                              hipStream_t s);
 
 // Row norms of the whitened rows without storing them: part[r][2 cj + h]
 // (2 Kp / 256 floats per row) = sum of squares of (X Y^T (+ X Y2^T))[r][.]
-// over the 128 columns h of column tile cj.  Same shape rules as above.
-hipError_t launch_whiten_norm_bf16(const bf16_t* X, const bf16_t* Y, const bf16_t* Y2, float* part,
-                                   int64_t rows, int64_t Kp, const int* st, hipStream_t s);
+// over the 128 columns h of column tile cj.  Same shape and Y2 rules as above.
+hipError_t launch_whiten_norm_bf16(const bf16_t* X, const bf16_t* Y, const bf16_t* Y2,
+                                   const int* use2, const int* use2b, float* part, int64_t rows,
+                                   int64_t Kp, const int* st, hipStream_t s);
 
 // Symmetric rank-k product over segmented rows, split over k:
 //   P[z][tile] = partial sums of X X^T for upper tiles (ti <= tj),
@@ -106,9 +110,20 @@ hipError_t launch_pack(const void* G, void* out, int64_t N, int64_t m, int64_t n
                        int64_t cols_p, int transpose, int elem_bytes, hipStream_t s);
 
 // Lw (dim_p x dim_p, elem) = lower(Li) rounded (bf16: hi part; Lw2: lo part
-// if non-null), zero elsewhere.  elem_bytes = 2 or 4.
+// if non-null), zero elsewhere.  elem_bytes = 2 or 4.  With part non-null,
+// convert_parts(dim_p) partial sums of sum_j F_jj ||column j of lower(Li)||^2
+// go to part (F: the dim x dim factor whose inverse factor Li is; the input
+// of launch_split_decide).
+constexpr int64_t kConvertChunks = 64;
+int64_t convert_parts(int64_t dim_p);
 hipError_t launch_convert_inverse(const float* Li, int64_t dim, void* Lw, void* Lw2, int64_t dim_p,
-                                  int elem_bytes, const int* st, hipStream_t s);
+                                  int elem_bytes, const float* F, double* part, const int* st,
+                                  hipStream_t s);
+
+// From those partials: out[0] = s = (1/dim) sum_j F_jj (F^-1)_jj and
+// flag[0] = (s > threshold).
+hipError_t launch_split_decide(const double* part, int64_t dim, int64_t dim_p, double threshold,
+                               int* flag, double* out, const int* st, hipStream_t s);
 
 // tr = trace(F); with kappa > 0, F += kappa * tr/dim * I first and tr is the
 // trace after damping.  fp64 accumulation, one workgroup, fixed order.

@@ -51,6 +51,10 @@ def test_workspace_sizes(lib):
     assert r > big
     split2 = ff.ff_workspace_size(cfg(4096, 4096, 128, ff.FF_BF16, split=2))
     assert split2 == big + 2 * 4096 * 4096 * 2
+    # automatic split: both low parts, plus per side a flag/statistic block
+    # and the statistic's partial sums (16 column blocks x 64 row chunks)
+    auto = ff.ff_workspace_size(cfg(4096, 4096, 128, ff.FF_BF16, split=0))
+    assert auto == split2 + 2 * (256 + 8 * 16 * 64)
     large = ff.ff_workspace_size(cfg(8192, 28672, 32, ff.FF_BF16))
     assert large < 60e9
 

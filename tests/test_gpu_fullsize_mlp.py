@@ -36,18 +36,22 @@ def test_mlp_fullsize(gpu, key):
     print(f"[{w.name}] generating on the device", flush=True)
     G = synth.generate_device(w, device=gpu)
 
-    # (b) the configured number of iterations on a fresh handle.  The widest
-    # layer's input factor has condition ~3e5; there the hi/lo split of L^-1
-    # is the whitening precision that keeps the likelihood flat (one pass of
-    # bf16 L^-1 stays within the 5e-3 bar, 2.4e-3 against an fp64 flip-flop
-    # on the same samples, against 1.1e-4 with the split, but its likelihood
-    # drifts by ~2e-4 N m n over the last iterations).
-    split = 2 if key == "mlp_large" else 1
-    print(f"[{w.name}] {w.iters} iterations, whiten_split={split}", flush=True)
-    f = ffe.FlipFlop(G, whiten_split=split)
+    # (b) the configured number of iterations on a fresh handle, with the
+    # library's default (automatic) whitening precision.  The widest layer's
+    # input factor has condition ~3e5 and rounding sensitivity s(A) ~ 21:
+    # the rule whitens with the hi/lo split of L^-1 there (one pass stays
+    # inside the 5e-3 bar, 2.4e-3 against an fp64 flip-flop on the same
+    # samples, but its likelihood drifts by ~2e-4 N m n over the last
+    # iterations, also when only the A-side operand is split); the two other
+    # layers (s <= 13) get one pass.
+    print(f"[{w.name}] {w.iters} iterations, automatic whitening split", flush=True)
+    f = ffe.FlipFlop(G)
     ll = f.iterate(w.iters)
     A, B = f.factors()
+    sA, sB, pA, pB = f.whiten_split_state()
     f.close()
+    print(f"[{w.name}] split state: s(A) {sA:.3f} s(B) {sB:.3f}, passes {pA} / {pB}", flush=True)
+    assert (pA, pB) == ((2, 2) if key == "mlp_large" else (1, 1))
     _free()
     print(f"[{w.name}] loglik per iteration: {ll}", flush=True)
     assert len(ll) == w.iters and all(np.isfinite(ll))

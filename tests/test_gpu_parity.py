@@ -128,19 +128,52 @@ def test_bf16_config_shaped(gpu, key, m, n, N):
 
 def test_bf16_ill_conditioned_split(gpu):
     """Few samples per input channel (N m / n = 1.6) make the estimated A very
-    ill-conditioned (condition ~7e4); the bf16 rounding of L^-1 then costs
-    about 1e-2, and the hi/lo split of L^-1 (two passes) brings the error
-    back under the bar."""
+    ill-conditioned (condition ~7e4, rounding sensitivity s(A) = 10 after the
+    first iteration, 26 after the tenth); one bf16 pass of L^-1 then costs
+    about 8e-3, and the hi/lo split of L^-1 (two passes) brings the error
+    back under the bar.  The default (automatic) rule switches both
+    whitenings to two passes once s(A) > 16 and meets the bar."""
     w = small_workload("mlp_down", m=512, n=1280, N=4)
     d = synth.generate(w)
     ref = oracle.flipflop(d.G, w.iters)
     errs = {}
-    for split in (1, 2):
+    for split in (1, 2, 0):
         A, B, ll, done = run_gpu(d.G, w.iters, gpu, whiten_split=split)
         errs[split] = oracle.kron_rel_error(A, B, ref.A, ref.B)
-    print(f"bf16 512x1280 N=4: split1 {errs[1]:.3e}, split2 {errs[2]:.3e}")
-    assert errs[2] < TOL_BF16
+    print(f"bf16 512x1280 N=4: split1 {errs[1]:.3e}, split2 {errs[2]:.3e}, automatic {errs[0]:.3e}")
+    assert errs[2] < TOL_BF16 and errs[0] < TOL_BF16
     assert errs[2] < 0.5 * errs[1]
+
+
+def test_automatic_split_statistic(gpu):
+    """The device statistic s = (1/dim) sum_j F_jj (F^-1)_jj of the last
+    factorised A and B equals its fp64 evaluation from the returned factors
+    (s is invariant under the trace normalisation's scaling), and both
+    whitenings use two passes exactly when max(s(A), s(B)) > 16."""
+    import torch
+    import paper_2609_14706_amd as ffe
+    for key, kw in (("mlp_down", dict(m=512, n=1280, N=4)), ("attn", dict(m=512, n=768, N=8))):
+        w = small_workload(key, **kw)
+        d = synth.generate(w)
+        f = ffe.FlipFlop(to_device(d.G, gpu))
+        f.iterate(w.iters)
+        A, B = (X.double().cpu().numpy() for X in f.factors())
+        sA, sB, pA, pB = f.whiten_split_state()
+        f.close()
+        ref = [float(np.mean(np.diag(X) * np.diag(np.linalg.inv(X)))) for X in (A, B)]
+        print(f"{w.name}: device s(A) {sA:.6f} s(B) {sB:.6f}; fp64 {ref[0]:.6f} {ref[1]:.6f}; "
+              f"passes {pA} / {pB}")
+        assert abs(sA - ref[0]) < 1e-3 * ref[0] and abs(sB - ref[1]) < 1e-3 * ref[1]
+        assert pA == pB == (2 if max(sA, sB) > 16 else 1)
+    # forced settings report their pass counts and no statistic
+    w = small_workload("attn", m=256, n=256, N=4)
+    G = to_device(synth.generate(w).G, gpu)
+    for split in (1, 2):
+        f = ffe.FlipFlop(G, whiten_split=split)
+        f.iterate(2)
+        sA, sB, pA, pB = f.whiten_split_state()
+        f.close()
+        assert np.isnan(sA) and np.isnan(sB) and (pA, pB) == (split, split)
 
 
 # ------------------------------------------------------------- kron apply
