@@ -90,12 +90,12 @@ typedef enum { FF_SAMPLES_DENSE = 0, FF_SAMPLES_RANK1 = 1 } ff_sample_form;
  *   FF_EST_FROBENIUS: the same iteration with the factors in place of their
  *     inverses, B <- (1/(N n)) sum_i G_i A G_i^T, A <- (1/(N m)) sum_i G_i^T B G_i
  *     (rank-one form: weights x^T A x and g^T B g), a power iteration for
- *     min ||H - A (x) B||_F (Section 5).  The whitening operand is
- *     RevCholesky of the other factor (Y lower, Y^T Y = F, Section 2), from
- *     an fp32 factorisation: a factor beyond fp32's reach (condition number
- *     above ~1e7, which the undamped iteration reaches on few samples) is
- *     reported as FF_ERR_NOT_SPD; the paper damps every iteration
- *     (Appendix B).  Only FF_ORDER_B_FIRST: with A first, the trace
+ *     min ||H - A (x) B||_F (Section 5).  Nothing is factorised or
+ *     inverted: each half step forms P_i = G_i F (dense, twice the
+ *     triangular whitening's work; the bf16 path rounds F and P to bf16)
+ *     and sums the upper tiles of P_i G_i^T, so a factor of any condition
+ *     number (the undamped iteration's estimates lose rank on few samples)
+ *     is handled.  Only FF_ORDER_B_FIRST: with A first, the trace
  *     normalisation leaves B's scale growing doubly exponentially.
  *   FF_EST_MARGINAL: A = E[x x^T], B = E[g g^T] (means over the tokens).
  *   FF_EST_INPUT: A = E[x x^T], B = I_m.

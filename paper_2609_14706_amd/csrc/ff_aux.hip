@@ -99,6 +99,26 @@ __global__ __launch_bounds__(256) void k_row_sums(const float* __restrict__ P, i
   if (lane == 0) w[r] = (float)s;
 }
 
+// w[r] = sum_j P[r][j] V[r][j] (rows x cols, row-major, elem T, fp64 sum per
+// row): the quadratic forms v_r^T F v_r from P = V F.
+template <typename T>
+__global__ __launch_bounds__(256) void k_row_dot(const T* __restrict__ P, const T* __restrict__ V,
+                                                 int64_t rows, int64_t cols, float* __restrict__ w,
+                                                 const int* st) {
+  if (ff_halted(st)) return;
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= rows) return;
+  const T* p = P + r * cols;
+  const T* v = V + r * cols;
+  double s = 0.0;
+  for (int64_t j = lane; j < cols; j += 64)
+    s += (double)Elem<T>::to_f32(p[j]) * (double)Elem<T>::to_f32(v[j]);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o);
+  if (lane == 0) w[r] = (float)s;
+}
+
 // sqrt(w[r]) * M[r][c] for the rows_p x cols_p matrix M: the rows of M
 // (tokens) weighted and turned into the k axis of a symmetric product, in
 // segments of seg tokens: element (c, r) goes to
@@ -180,7 +200,7 @@ __global__ __launch_bounds__(256) void k_scale_transpose_16(const bf16_t* __rest
 template <typename T>
 __global__ __launch_bounds__(256) void k_convert_inverse(const float* __restrict__ Li, int64_t dim,
                                                          T* __restrict__ Lw, T* __restrict__ Lw2,
-                                                         int64_t dim_p, int64_t rch,
+                                                         int64_t dim_p, int64_t rch, int full,
                                                          const float* __restrict__ F,
                                                          double* __restrict__ part, const int* st) {
   if (ff_halted(st)) return;
@@ -195,7 +215,7 @@ __global__ __launch_bounds__(256) void k_convert_inverse(const float* __restrict
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int64_t r = i + u;
-        v[u] = (r < i1 && r < dim && j <= r) ? Li[r * dim + j] : 0.0f;
+        v[u] = (r < i1 && r < dim && j < dim && (full || j <= r)) ? Li[r * dim + j] : 0.0f;
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
@@ -461,17 +481,6 @@ __global__ __launch_bounds__(256) void k_copy2d_f32(const float* __restrict__ sr
   }
 }
 
-// Y = J C^T J from the lower Cholesky factor C of J M J (RevCholesky, Section 2).
-__global__ __launch_bounds__(256) void k_rev_transpose(const float* __restrict__ C, int64_t d,
-                                                       float* __restrict__ Y, const int* st) {
-  if (ff_halted(st)) return;
-  const int64_t stride = (int64_t)gridDim.x * 256;
-  for (int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x; k < d * d; k += stride) {
-    const int64_t i = k / d, j = k % d;
-    Y[k] = i >= j ? C[(d - 1 - j) * d + (d - 1 - i)] : 0.0f;
-  }
-}
-
 __global__ __launch_bounds__(256) void k_fill_f32(float* dst, int64_t count, float v) {
   const int64_t stride = (int64_t)gridDim.x * 256;
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count; i += stride) dst[i] = v;
@@ -529,6 +538,20 @@ hipError_t launch_row_sums(const float* P, int64_t rows, int64_t cols, int squar
   return hipGetLastError();
 }
 
+hipError_t launch_row_dot(const void* P, const void* V, int64_t rows, int64_t cols, int elem_bytes,
+                          float* w, const int* st, hipStream_t s) {
+  const int64_t blocks = (rows + 3) / 4;
+  if (elem_bytes == 2)
+    hipLaunchKernelGGL(k_row_dot<bf16_t>, dim3((uint32_t)blocks), dim3(256), 0, s, (const bf16_t*)P,
+                       (const bf16_t*)V, rows, cols, w, st);
+  else if (elem_bytes == 4)
+    hipLaunchKernelGGL(k_row_dot<float>, dim3((uint32_t)blocks), dim3(256), 0, s, (const float*)P,
+                       (const float*)V, rows, cols, w, st);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
 hipError_t launch_scale_transpose(const void* M, const float* w, int64_t rows_p, int64_t cols_p,
                                   int64_t seg, void* out, int elem_bytes, const int* st,
                                   hipStream_t s) {
@@ -559,17 +582,17 @@ int64_t convert_parts(int64_t dim_p) {
 
 hipError_t launch_convert_inverse(const float* Li, int64_t dim, void* Lw, void* Lw2, int64_t dim_p,
                                   int elem_bytes, const float* F, double* part, const int* st,
-                                  hipStream_t s) {
+                                  hipStream_t s, int full) {
   if (dim < 1 || dim_p < dim) return hipErrorInvalidValue;
   const int64_t nchunk = dim_p < kConvertChunks ? dim_p : kConvertChunks;
   const int64_t rch = (dim_p + nchunk - 1) / nchunk;
   const dim3 grid((uint32_t)((dim_p + 255) / 256), (uint32_t)((dim_p + rch - 1) / rch));
   if (elem_bytes == 2)
     hipLaunchKernelGGL(k_convert_inverse<bf16_t>, grid, dim3(256), 0, s, Li, dim, (bf16_t*)Lw,
-                       (bf16_t*)Lw2, dim_p, rch, F, part, st);
+                       (bf16_t*)Lw2, dim_p, rch, full, F, part, st);
   else if (elem_bytes == 4)
     hipLaunchKernelGGL(k_convert_inverse<float>, grid, dim3(256), 0, s, Li, dim, (float*)Lw,
-                       (float*)Lw2, dim_p, rch, F, part, st);
+                       (float*)Lw2, dim_p, rch, full, F, part, st);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
@@ -643,12 +666,6 @@ hipError_t launch_copy2d_f32(const float* src, int64_t lds, float* dst, int64_t 
   if (rows == 0 || cols == 0) return hipSuccess;
   hipLaunchKernelGGL(k_copy2d_f32, dim3(grid_for(rows * cols)), dim3(256), 0, s, src, lds, dst, ldd,
                      rows, cols, st);
-  return hipGetLastError();
-}
-
-hipError_t launch_rev_transpose(const float* C, int64_t d, float* Y, const int* st, hipStream_t s) {
-  if (d < 1) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_rev_transpose, dim3(grid_for(d * d)), dim3(256), 0, s, C, d, Y, st);
   return hipGetLastError();
 }
 

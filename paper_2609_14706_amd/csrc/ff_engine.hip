@@ -520,24 +520,23 @@ ff_status cholinv(ff_handle_s* h, Side& s, int slot, int iteration) {
   return cholinv_from(h, s, s.F[slot], iteration);
 }
 
-// Frobenius estimator: the whitening operand is Y = RevCholesky(F) = J C^T J
-// with C = Cholesky(J F J): Y is lower triangular with Y^T Y = F, so the
-// whitened samples X Y^T give X F X^T in the symmetric product.  Y goes where
-// L^-1 goes (s.Li, zeros above the diagonal) and into s.Lw; log|F| into s.slots.
-ff_status revchol_operand(ff_handle_s* h, Side& s, const float* src, int iteration) {
-  Timed t(h, 3, (double)s.dim * s.dim * s.dim / 3.0);
-  FF_HIP(launch_wk_reverse(src, s.dim, s.L, h->st, h->stream));
-  ff_status rc = chol_blocked(h, s, iteration);
-  if (rc != FF_OK) return rc;
-  FF_HIP(launch_rev_transpose(s.L, s.dim, s.Li, h->st, h->stream));
-  FF_HIP(launch_convert_inverse(s.Li, s.dim, s.Lw, s.Lw2, s.dim_p, h->elem, nullptr, nullptr,
-                                h->st, h->stream));
+// Frobenius estimator: the half steps B = (1/(N n)) sum_i G_i A G_i^T and
+// A = (1/(N m)) sum_i G_i^T B G_i use the factor itself, so the operand is F
+// rounded to the samples' type (dense, both triangles; hi + lo parts with
+// whiten_split = 2): the products P_i = G_i F and then the symmetric
+// sum_i P_i G_i^T need no factorisation, so a factor of any condition
+// number (the undamped power iteration's estimates lose rank quickly) is
+// handled as the oracle handles it.
+ff_status frob_operand(ff_handle_s* h, Side& s, const float* src) {
+  Timed t(h, 3, 0.0);
+  FF_HIP(launch_convert_inverse(src, s.dim, s.Lw, s.Lw2, s.dim_p, h->elem, nullptr, nullptr, h->st,
+                                h->stream, 1));
   return FF_OK;
 }
 
 // The whitening operand of the estimator for factor s.F[slot].
 ff_status operand(ff_handle_s* h, Side& s, int slot, int iteration) {
-  if (h->cfg.estimator == FF_EST_FROBENIUS) return revchol_operand(h, s, s.F[slot], iteration);
+  if (h->cfg.estimator == FF_EST_FROBENIUS) return frob_operand(h, s, s.F[slot]);
   return cholinv(h, s, slot, iteration);
 }
 
@@ -562,12 +561,37 @@ const bf16_t* second_part(const ff_handle_s* h, const Side& p, const int** use2,
 }
 
 // Rank-one form: token weights wbuf[t] = ||L_p^-1 v_t||^2 for the token
-// vectors v_t of side p's dimension (x_t when p = A, g_t when p = B).
+// vectors v_t of side p's dimension (x_t when p = A, g_t when p = B); for
+// the Frobenius estimator v_t^T F_p v_t, from P = V F_p and a row-wise dot
+// product with V.
 ff_status token_weights(ff_handle_s* h, Side& p, float* wbuf) {
   const void* V = (&p == &h->A) ? h->Gx : h->Gt;
   const int64_t T_p = h->lay.T_p, Kp = p.dim_p;
-  const double wflop = (double)h->N * p.dim * p.dim;
+  const bool frob = h->cfg.estimator == FF_EST_FROBENIUS;
+  const double wflop = (frob ? 2.0 : 1.0) * (double)h->N * p.dim * p.dim;
   Timed t(h, 0, wflop);
+  if (frob) {
+    // P goes into the weighted-token buffer, which is free until the weights exist
+    void* P = h->bf16 ? h->S : h->W;
+    if (h->bf16) {
+      const bf16_t* Y2 = h->cfg.whiten_split == 2 ? (const bf16_t*)p.Lw2 : nullptr;
+      FF_HIP(launch_whiten_bf16((const bf16_t*)V, (const bf16_t*)p.Lw, Y2, nullptr, nullptr,
+                                (bf16_t*)P, T_p, Kp, h->st, h->stream, true));
+    } else {
+      GemmF32 g{};
+      g.st = h->st;
+      g.ksplit = 1;
+      g.kseg = Kp;
+      g.A = (const float*)V; g.lda = Kp; g.transA = 0;
+      g.B = (const float*)p.Lw; g.ldb = Kp; g.transB = 1;
+      g.C = (float*)P; g.ldc = Kp;
+      g.M = T_p; g.N = Kp; g.K = Kp;
+      g.alpha = 1.f; g.beta = 0.f; g.flags = 0;
+      FF_HIP(launch_gemm_f32(g, 1, h->stream));
+    }
+    FF_HIP(launch_row_dot(P, V, T_p, Kp, h->elem, wbuf, h->st, h->stream));
+    return FF_OK;
+  }
   if (h->bf16) {
     const int *use2 = nullptr, *use2b = nullptr;
     const bf16_t* Y2 = second_part(h, p, &use2, &use2b);
@@ -648,7 +672,9 @@ ff_status update_rank1(ff_handle_s* h, Side& s, Side& p, int slot, bool finish,
 // s.tr; with finish = false, without damping and trace.  p_identity: p's
 // factor is exactly I (the default start), so Li_p = I and the whitened
 // samples are the samples themselves (bitwise: a product with I is exact);
-// the symmetric product then reads X directly.
+// the symmetric product then reads X directly.  Frobenius estimator:
+// (1/(N p.dim)) sum_i (X_i F_p) X_i^T, the dense product P = X F_p first
+// (twice the whitening's work), then the upper tiles of P X^T.
 ff_status update(ff_handle_s* h, Side& s, Side& p, int slot, bool finish = true,
                  bool p_identity = false, float* dst = nullptr) {
   if (h->lay.rank1) return update_rank1(h, s, p, slot, finish, false, dst);
@@ -656,7 +682,8 @@ ff_status update(ff_handle_s* h, Side& s, Side& p, int slot, bool finish = true,
   const void* X = (&s == &h->B) ? h->Gx : h->Gt;
   const int64_t N = h->N, rows = N * s.dim_p, Kp = p.dim_p;
   const double scale = 1.0 / ((double)N * (double)p.dim);
-  const double wflop = (double)N * s.dim * p.dim * p.dim;
+  const bool frob = h->cfg.estimator == FF_EST_FROBENIUS && !p_identity;
+  const double wflop = (frob ? 2.0 : 1.0) * (double)N * s.dim * p.dim * p.dim;
   const double sflop = (double)N * p.dim * s.dim * s.dim;
   const void* Wsrc = p_identity ? X : (const void*)h->W;
   if (h->bf16) {
@@ -665,12 +692,12 @@ ff_status update(ff_handle_s* h, Side& s, Side& p, int slot, bool finish = true,
       const int *use2 = nullptr, *use2b = nullptr;
       const bf16_t* Y2 = second_part(h, p, &use2, &use2b);
       FF_HIP(launch_whiten_bf16((const bf16_t*)X, (const bf16_t*)p.Lw, Y2, use2, use2b,
-                                (bf16_t*)h->W, rows, Kp, h->st, h->stream));
+                                (bf16_t*)h->W, rows, Kp, h->st, h->stream, frob));
     }
     {
       Timed t(h, 1, sflop);
       FF_HIP(launch_syrk_bf16((const bf16_t*)Wsrc, s.dim_p, Kp, s.dim_p * Kp, N, s.splits, h->P,
-                              h->st, h->stream));
+                              h->st, h->stream, frob ? (const bf16_t*)X : nullptr));
     }
     {
       Timed t(h, 2, 0.0);
@@ -686,7 +713,7 @@ ff_status update(ff_handle_s* h, Side& s, Side& p, int slot, bool finish = true,
       g.B = (const float*)p.Lw; g.ldb = Kp; g.transB = 1;
       g.C = (float*)h->W; g.ldc = Kp;
       g.M = rows; g.N = Kp; g.K = Kp; g.kseg = Kp;
-      g.alpha = 1.f; g.beta = 0.f; g.flags = kKHiCol;
+      g.alpha = 1.f; g.beta = 0.f; g.flags = frob ? 0 : kKHiCol;
       FF_HIP(launch_gemm_f32(g, 1, h->stream));
     }
     {
@@ -694,7 +721,7 @@ ff_status update(ff_handle_s* h, Side& s, Side& p, int slot, bool finish = true,
       GemmF32 q{};
       q.st = h->st;
       q.A = (const float*)Wsrc; q.lda = Kp; q.transA = 0;
-      q.B = (const float*)Wsrc; q.ldb = Kp; q.transB = 1;
+      q.B = (const float*)(frob ? X : Wsrc); q.ldb = Kp; q.transB = 1;
       q.C = h->P; q.ldc = s.dim_p; q.sC = s.dim_p * s.dim_p;
       q.M = s.dim_p; q.N = s.dim_p; q.K = N * Kp;
       q.kseg = Kp; q.segA = q.segB = s.dim_p * Kp;
@@ -1215,7 +1242,7 @@ ff_status ff_half_step(ff_handle h, ff_half which, const float* F, float* out) {
   const float* src = F != nullptr ? F : p.F[h->cur];
   // the whitening operands no longer belong to the current factors
   h->A.lw_valid = h->B.lw_valid = false;
-  ff_status rc = h->cfg.estimator == FF_EST_FROBENIUS ? revchol_operand(h, p, src, -1)
+  ff_status rc = h->cfg.estimator == FF_EST_FROBENIUS ? frob_operand(h, p, src)
                                                       : cholinv_from(h, p, src, -1);
   if (rc != FF_OK) return rc;
   if ((rc = update(h, s, p, 0, false, false, out)) != FF_OK) return rc;

@@ -211,8 +211,9 @@ __device__ __forceinline__ void zero_acc(f32x16 (&acc)[4][4]) {
 // row blocks) stay in step and share their operand slices in its L2.
 template <bool SW>
 __device__ __forceinline__ void whiten_tile(Ring& sm, const bf16_t* xa, const bf16_t* Y, const bf16_t* Y2,
-                                            uint32_t cj, bool rev, uint32_t Kp, f32x16 (&acc)[4][4]) {
-  const int np = (int)((cj + 1) * (TM / PK));
+                                            uint32_t cj, bool rev, uint32_t Kp, bool full,
+                                            f32x16 (&acc)[4][4]) {
+  const int np = (int)((full ? Kp / TM : cj + 1) * (TM / PK));
   zero_acc(acc);
   for (int pass = 0; pass < (Y2 != nullptr ? 2 : 1); ++pass) {
     const bf16_t* yb = (pass ? Y2 : Y) + (size_t)cj * TM * Kp;
@@ -254,7 +255,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_whiten_bf16(const bf16_t* __restric
                                                          const bf16_t* __restrict__ Y2,
                                                          const int* __restrict__ use2, const int* __restrict__ use2b,
                                                          bf16_t* __restrict__ C, uint32_t Kp,
-                                                         const int* st) {
+                                                         uint32_t full, const int* st) {
   if (ff_halted(st)) return;
   if (use2 != nullptr && *use2 == 0 && (use2b == nullptr || *use2b == 0)) Y2 = nullptr;  // one pass
   __shared__ Ring sm;
@@ -265,7 +266,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_whiten_bf16(const bf16_t* __restric
   f32x16 acc[4][4];
   for (uint32_t h = 0; h < (ncol - 1 - c != c ? 2u : 1u); ++h) {
     const uint32_t cj = h ? ncol - 1 - c : c;
-    whiten_tile<false>(sm, xa, Y, Y2, cj, h != 0, Kp, acc);
+    whiten_tile<false>(sm, xa, Y, Y2, cj, h != 0, Kp, full != 0, acc);
     store_whitened(acc, C, rb, cj, Kp);
   }
 }
@@ -312,7 +313,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_whiten_norm_bf16(const bf16_t* __re
   f32x16 acc[4][4];
   for (uint32_t h = 0; h < (ncol - 1 - c != c ? 2u : 1u); ++h) {
     const uint32_t cj = h ? ncol - 1 - c : c;
-    whiten_tile<true>(sm, xa, Y, Y2, cj, h != 0, Kp, acc);
+    whiten_tile<true>(sm, xa, Y, Y2, cj, h != 0, Kp, false, acc);
     store_norms(acc, part, rb, cj, ncol);
   }
 }
@@ -361,7 +362,8 @@ __device__ __forceinline__ void grouped_tile(uint32_t idx, uint32_t T, uint32_t&
   ti = tj = 0;
 }
 
-__global__ __launch_bounds__(NTHR, 1) void k_syrk_bf16(const bf16_t* __restrict__ X, uint32_t ld,
+__global__ __launch_bounds__(NTHR, 1) void k_syrk_bf16(const bf16_t* __restrict__ X,
+                                                       const bf16_t* __restrict__ Xb, uint32_t ld,
                                                        uint64_t seg_stride, uint32_t nseg,
                                                        uint32_t T, uint32_t ntiles, uint32_t splits,
                                                        float* __restrict__ P, const int* st) {
@@ -375,7 +377,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_syrk_bf16(const bf16_t* __restrict_
   const uint64_t ptot = (uint64_t)pps * nseg;
   const int p0 = (int)(ptot * z / splits), p1 = (int)(ptot * (z + 1) / splits);
   const bf16_t* xa = X + (size_t)ti * TM * ld;
-  const bf16_t* xb = X + (size_t)tj * TM * ld;
+  const bf16_t* xb = (Xb != nullptr ? Xb : X) + (size_t)tj * TM * ld;
   f32x16 acc[4][4];
   zero_acc(acc);
   auto addr = [&](int p, const bf16_t*& pa, const bf16_t*& pb) {
@@ -433,12 +435,12 @@ __global__ __launch_bounds__(256) void k_reduce_frag(const float* __restrict__ P
 
 hipError_t launch_whiten_bf16(const bf16_t* X, const bf16_t* Y, const bf16_t* Y2, const int* use2,
                               const int* use2b, bf16_t* C, int64_t rows, int64_t Kp, const int* st,
-                              hipStream_t s) {
+                              hipStream_t s, bool full) {
   if (rows <= 0 || Kp <= 0 || rows % TM || Kp % TM || Kp > (1 << 20)) return hipErrorInvalidValue;
   const int64_t tiles = (rows / TM) * ((Kp / TM + 1) / 2);  // one workgroup per tile pair
   if (tiles > 0x7fffffff) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_whiten_bf16, dim3((uint32_t)tiles), dim3(NTHR), 0, s, X, Y, Y2, use2, use2b, C,
-                     (uint32_t)Kp, st);
+                     (uint32_t)Kp, (uint32_t)full, st);
   return hipGetLastError();
 }
 
@@ -455,13 +457,14 @@ hipError_t launch_whiten_norm_bf16(const bf16_t* X, const bf16_t* Y, const bf16_
 }
 
 hipError_t launch_syrk_bf16(const bf16_t* X, int64_t dim_p, int64_t ld, int64_t seg_stride,
-                            int64_t nseg, int splits, float* P, const int* st, hipStream_t s) {
+                            int64_t nseg, int splits, float* P, const int* st, hipStream_t s,
+                            const bf16_t* Xb) {
   if (dim_p <= 0 || dim_p % TM || ld <= 0 || ld % PK || nseg <= 0 || splits <= 0)
     return hipErrorInvalidValue;
   const int64_t T = dim_p / TM, ntiles = T * (T + 1) / 2;
   if ((int64_t)splits > (ld / PK) * nseg) return hipErrorInvalidValue;
   if (ntiles * splits > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_syrk_bf16, dim3((uint32_t)(ntiles * splits)), dim3(NTHR), 0, s, X,
+  hipLaunchKernelGGL(k_syrk_bf16, dim3((uint32_t)(ntiles * splits)), dim3(NTHR), 0, s, X, Xb,
                      (uint32_t)ld, (uint64_t)seg_stride, (uint32_t)nseg, (uint32_t)T,
                      (uint32_t)ntiles, (uint32_t)splits, P, st);
   return hipGetLastError();

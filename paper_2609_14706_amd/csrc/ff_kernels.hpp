@@ -20,10 +20,11 @@ constexpr int kTileBF16 = 256;
 //   and, if use2 is non-null, *use2 != 0 or *use2b != 0 (use2b may be null):
 //   flags read on the device at launch)
 // X: rows x Kp, Y/Y2: Kp x Kp lower triangular, C: rows x Kp, all row-major
-// bf16 with leading dimension Kp.  rows and Kp are multiples of 256.
+// bf16 with leading dimension Kp.  rows and Kp are multiples of 256.  With
+// full = true, Y/Y2 are dense and k runs over all of Kp (C = X Y^T).
 hipError_t launch_whiten_bf16(const bf16_t* X, const bf16_t* Y, const bf16_t* Y2, const int* use2,
                               const int* use2b, bf16_t* C, int64_t rows, int64_t Kp, const int* st,
-                              hipStream_t s);
+                              hipStream_t s, bool full = false);
 
 // Row norms of the whitened rows without storing them: part[r][2 cj + h]
 // (2 Kp / 256 floats per row) = sum of squares of (X Y^T (+ X Y2^T))[r][.]
@@ -37,9 +38,12 @@ hipError_t launch_whiten_norm_bf16(const bf16_t* X, const bf16_t* Y, const bf16_
 // where row r of X is the concatenation over segments s < nseg of
 // X[s * seg_stride + r * ld .. + ld).  dim_p (rows) and ld are multiples of
 // 256 and 64.  P holds splits * T(T+1)/2 tiles of 256 x 256 fp32 in the
-// matrix-core fragment order (decoded by launch_reduce_frag).
+// matrix-core fragment order (decoded by launch_reduce_frag).  With Xb
+// non-null (same layout), the upper tiles of X Xb^T instead (for a product
+// the caller knows to be symmetric).
 hipError_t launch_syrk_bf16(const bf16_t* X, int64_t dim_p, int64_t ld, int64_t seg_stride,
-                            int64_t nseg, int splits, float* P, const int* st, hipStream_t s);
+                            int64_t nseg, int splits, float* P, const int* st, hipStream_t s,
+                            const bf16_t* Xb = nullptr);
 
 // F (dim x dim, fp32, row-major) = scale * sum_z P[z]  (upper tiles mirrored).
 hipError_t launch_reduce_frag(const float* P, int splits, int64_t dim_p, float* F, int64_t dim,
@@ -109,8 +113,9 @@ hipError_t launch_chol_step(float* L, float* Li, int64_t dim, int64_t d0, int64_
 hipError_t launch_pack(const void* G, void* out, int64_t N, int64_t m, int64_t n, int64_t rows_p,
                        int64_t cols_p, int transpose, int elem_bytes, hipStream_t s);
 
-// Lw (dim_p x dim_p, elem) = lower(Li) rounded (bf16: hi part; Lw2: lo part
-// if non-null), zero elsewhere.  elem_bytes = 2 or 4.  With part non-null,
+// Lw (dim_p x dim_p, elem) = lower(Li) (all of Li with full = 1) rounded
+// (bf16: hi part; Lw2: lo part if non-null), zero elsewhere.  elem_bytes = 2
+// or 4.  With part non-null (and full = 0),
 // convert_parts(dim_p) partial sums of sum_j F_jj ||column j of lower(Li)||^2
 // go to part (F: the dim x dim factor whose inverse factor Li is; the input
 // of launch_split_decide).
@@ -118,7 +123,7 @@ constexpr int64_t kConvertChunks = 64;
 int64_t convert_parts(int64_t dim_p);
 hipError_t launch_convert_inverse(const float* Li, int64_t dim, void* Lw, void* Lw2, int64_t dim_p,
                                   int elem_bytes, const float* F, double* part, const int* st,
-                                  hipStream_t s);
+                                  hipStream_t s, int full = 0);
 
 // From those partials: out[0] = s = (1/dim) sum_j F_jj (F^-1)_jj and
 // flag[0] = (s > threshold).
@@ -157,6 +162,10 @@ hipError_t launch_delta(const float* A, const float* Ap, int64_t nA, const float
                         const float* Bp, int64_t nB, double* part, double* delta_out, double tol,
                         int iteration, int* st, hipStream_t s);
 
+// w[r] = sum_j P[r][j] V[r][j], rows x cols, elem_bytes 2 (bf16) or 4.
+hipError_t launch_row_dot(const void* P, const void* V, int64_t rows, int64_t cols, int elem_bytes,
+                          float* w, const int* st, hipStream_t s);
+
 // w[r] = sum_j P[r][j] (square = 0) or sum_j P[r][j]^2 (square = 1), rows x cols.
 hipError_t launch_row_sums(const float* P, int64_t rows, int64_t cols, int square, float* w,
                            const int* st, hipStream_t s);
@@ -179,9 +188,6 @@ hipError_t launch_copy_f32(const float* src, float* dst, int64_t count, const in
 // dst[r][c] = src[r][c] for r < rows, c < cols (leading dimensions lds, ldd).
 hipError_t launch_copy2d_f32(const float* src, int64_t lds, float* dst, int64_t ldd, int64_t rows,
                              int64_t cols, const int* st, hipStream_t s);
-// Y[i][j] = C[d-1-j][d-1-i] for i >= j, 0 above: with C = Cholesky(J M J),
-// Y = J C^T J is lower triangular with Y^T Y = M (RevCholesky(M), Section 2).
-hipError_t launch_rev_transpose(const float* C, int64_t d, float* Y, const int* st, hipStream_t s);
 hipError_t launch_fill_f32(float* dst, int64_t count, float v, hipStream_t s);
 hipError_t launch_identity_f32(float* dst, int64_t dim, hipStream_t s);
 hipError_t launch_set_int(int* dst, int64_t count, int v, hipStream_t s);
