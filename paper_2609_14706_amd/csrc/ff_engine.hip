@@ -414,15 +414,6 @@ ff_status inverse_p1_split(ff_handle_s* h, Side& s, int64_t o, int64_t sz, int64
 // after the last leaf is the factorisation's tail.  The upper triangle of
 // s.L is scratch.
 constexpr int64_t kInvEvery = 8;
-// Automatic split (whiten_split = 0): whiten with the hi + lo bf16 parts of
-// L^-1 while s = (1/dim) sum_j F_jj (F^-1)_jj of either factor exceeds this,
-// i.e. when the rms distortion 2^-9 sqrt(s/3) of the whitened metric by the
-// bf16 rounding of that factor's L^-1 would exceed about 4.5e-3.  Measured (bf16 against fp32 / split 2 after the
-// workloads' iteration counts): the 4096 x 4096 layer (s(A) = 6.1) 2.5e-4,
-// 11008 x 4096 (7.4) 4.2e-4, 4096 x 11008 (13) 3.5e-4 with one pass; the
-// 8192 x 28672 layer (s(A) = 21) 2.4e-3 and a 512 x 1280 layer from 4 samples
-// (s(A) up to 26) 7.9e-3 with one pass, which the second pass removes.
-constexpr double kSplitThreshold = 16.0;
 constexpr int64_t kTwoLevel = 6144;
 constexpr int64_t kOuter = 2048;
 
@@ -498,6 +489,17 @@ ff_status chol_blocked(ff_handle_s* h, Side& s, int iteration) {
   }
   return FF_OK;
 }
+
+// Automatic split (whiten_split = 0): whiten with the hi + lo bf16 parts of
+// L^-1 while s = (1/dim) sum_j F_jj (F^-1)_jj of either factor exceeds this,
+// i.e. when the rms distortion 2^-9 sqrt(s/3) of the whitened metric by the
+// bf16 rounding of that factor's L^-1 would exceed about 4.5e-3.  Measured
+// (bf16 against fp32 / split 2 after the workloads' iteration counts): the
+// 4096 x 4096 layer (s(A) = 6.1) 2.5e-4, 11008 x 4096 (7.4) 4.2e-4,
+// 4096 x 11008 (13) 3.5e-4 with one pass; the 8192 x 28672 layer
+// (s(A) = 21) 2.4e-3 and a 512 x 1280 layer from 4 samples (s(A) up to 26)
+// 7.9e-3 with one pass, which the second pass removes.
+constexpr double kSplitThreshold = 16.0;
 
 // L^-1 of the dim x dim factor at src into s.Li and the whitening operand
 // s.Lw; sum log L_jj per leaf into s.slots.

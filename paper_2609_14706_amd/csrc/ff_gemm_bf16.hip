@@ -146,7 +146,25 @@ __device__ __forceinline__ void step(Ring& sm, const Frags& cur, Frags& nxt, int
 // wave has finished reading this pair's slot and sees the next pair), then
 // multiplies the second half while reading the next pair's first half and
 // copying the pair after next into the slot just freed.
-template <bool SW = false, class Addr>
+// The first two pairs' copies of mainloop (p0 and p0 + 1 into slots 0, 1).
+template <class Addr>
+__device__ __forceinline__ void issue_prologue(Ring& sm, int p0, int p1, uint32_t lda, uint32_t ldb,
+                                               const Addr& addr) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const uint32_t oa = chunk_offset(wave, lane, lda), ob = chunk_offset(wave, lane, ldb);
+  const bf16_t *pa, *pb;
+  addr(p0, pa, pb);
+  issue_pair(sm, 0, pa, pb, oa, ob, lda, ldb, wave);
+  if (p1 - p0 > 1) {
+    addr(p0 + 1, pa, pb);
+    issue_pair(sm, 1, pa, pb, oa, ob, lda, ldb, wave);
+  }
+}
+
+// PRE: the caller has issued the prologue's copies (issue_prologue) after
+// its last other vector-memory instruction.
+template <bool SW = false, bool PRE = false, class Addr>
 __device__ __forceinline__ void mainloop(Ring& sm, int p0, int p1, uint32_t lda, uint32_t ldb,
                                          const Addr& addr, f32x16 (&acc)[4][4]) {
   const int tid = threadIdx.x, lane = tid & 63;
@@ -155,11 +173,8 @@ __device__ __forceinline__ void mainloop(Ring& sm, int p0, int p1, uint32_t lda,
   if (n <= 0) return;
   const uint32_t oa = chunk_offset(wave, lane, lda), ob = chunk_offset(wave, lane, ldb);
   const bf16_t *pa, *pb;
-  addr(p0, pa, pb);
-  issue_pair(sm, 0, pa, pb, oa, ob, lda, ldb, wave);
+  if (!PRE) issue_prologue(sm, p0, p1, lda, ldb, addr);
   if (n > 1) {
-    addr(p0 + 1, pa, pb);
-    issue_pair(sm, 1, pa, pb, oa, ob, lda, ldb, wave);
     wait_vmem<16>();
   } else {
     wait_vmem<0>();
@@ -209,20 +224,37 @@ __device__ __forceinline__ void zero_acc(f32x16 (&acc)[4][4]) {
 // workgroup all pairs of a row block sit at k slice t or 8 (ncol + 1) - 1 - t,
 // so the workgroups that run together on an XCD (consecutive pairs of a few
 // row blocks) stay in step and share their operand slices in its L2.
-template <bool SW>
+// Operand addresses of pair p of tile column cj (pass 0: Y, pass 1: Y2).
+struct WhitenAddr {
+  const bf16_t* xa;
+  const bf16_t* yb;
+  int np;
+  bool rev;
+  __device__ __forceinline__ void operator()(int p, const bf16_t*& pa, const bf16_t*& pb) const {
+    const int k = rev ? np - 1 - p : p;
+    pa = xa + k * PK;
+    pb = yb + k * PK;
+  }
+};
+
+__device__ __forceinline__ WhitenAddr whiten_addr(const bf16_t* xa, const bf16_t* Y, uint32_t cj,
+                                                  bool rev, uint32_t Kp, bool full) {
+  const int np = (int)((full ? Kp / TM : cj + 1) * (TM / PK));
+  return WhitenAddr{xa, Y + (size_t)cj * TM * Kp, np, rev};
+}
+
+// acc = X Y^T (+ X Y2^T) over tile column cj; PRE: the first pass's prologue
+// copies are issued and acc is zero already.
+template <bool SW, bool PRE>
 __device__ __forceinline__ void whiten_tile(Ring& sm, const bf16_t* xa, const bf16_t* Y, const bf16_t* Y2,
                                             uint32_t cj, bool rev, uint32_t Kp, bool full,
                                             f32x16 (&acc)[4][4]) {
-  const int np = (int)((full ? Kp / TM : cj + 1) * (TM / PK));
-  zero_acc(acc);
-  for (int pass = 0; pass < (Y2 != nullptr ? 2 : 1); ++pass) {
-    const bf16_t* yb = (pass ? Y2 : Y) + (size_t)cj * TM * Kp;
-    auto addr = [&](int p, const bf16_t*& pa, const bf16_t*& pb) {
-      const int k = rev ? np - 1 - p : p;
-      pa = xa + k * PK;
-      pb = yb + k * PK;
-    };
-    mainloop<SW>(sm, 0, np, Kp, Kp, addr, acc);
+  if (!PRE) zero_acc(acc);
+  const WhitenAddr a0 = whiten_addr(xa, Y, cj, rev, Kp, full);
+  mainloop<SW, PRE>(sm, 0, a0.np, Kp, Kp, a0, acc);
+  if (Y2 != nullptr) {
+    const WhitenAddr a1 = whiten_addr(xa, Y2, cj, rev, Kp, full);
+    mainloop<SW>(sm, 0, a1.np, Kp, Kp, a1, acc);
   }
 }
 
@@ -264,9 +296,16 @@ __global__ __launch_bounds__(NTHR, 1) void k_whiten_bf16(const bf16_t* __restric
   const uint32_t rb = t / npair, c = t % npair;
   const bf16_t* xa = X + (size_t)rb * TM * Kp;
   f32x16 acc[4][4];
-  for (uint32_t h = 0; h < (ncol - 1 - c != c ? 2u : 1u); ++h) {
-    const uint32_t cj = h ? ncol - 1 - c : c;
-    whiten_tile<false>(sm, xa, Y, Y2, cj, h != 0, Kp, full != 0, acc);
+  // the second tile's first copies go out right behind the first tile's
+  // stores, so that their latency overlaps the stores' drain
+  whiten_tile<false, false>(sm, xa, Y, Y2, c, false, Kp, full != 0, acc);
+  store_whitened(acc, C, rb, c, Kp);
+  if (ncol - 1 - c != c) {
+    const uint32_t cj = ncol - 1 - c;
+    const WhitenAddr a0 = whiten_addr(xa, Y, cj, true, Kp, full != 0);
+    issue_prologue(sm, 0, a0.np, Kp, Kp, a0);
+    zero_acc(acc);
+    whiten_tile<false, true>(sm, xa, Y, Y2, cj, true, Kp, full != 0, acc);
     store_whitened(acc, C, rb, cj, Kp);
   }
 }
@@ -313,7 +352,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_whiten_norm_bf16(const bf16_t* __re
   f32x16 acc[4][4];
   for (uint32_t h = 0; h < (ncol - 1 - c != c ? 2u : 1u); ++h) {
     const uint32_t cj = h ? ncol - 1 - c : c;
-    whiten_tile<true>(sm, xa, Y, Y2, cj, h != 0, Kp, false, acc);
+    whiten_tile<true, false>(sm, xa, Y, Y2, cj, h != 0, Kp, false, acc);
     store_norms(acc, part, rb, cj, ncol);
   }
 }
