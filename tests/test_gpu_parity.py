@@ -95,7 +95,7 @@ def test_fp32_start_factor(gpu):
 
 # -------------------------------------------------------------- bf16 path
 
-@pytest.mark.parametrize("split", [1, 2])
+@pytest.mark.parametrize("split", [0, 1, 2])
 def test_bf16_ragged_multi_tile(gpu, split):
     """Attention-layer generator (power-law spectra, 10% rank-32 noise) at a
     size the oracle finishes in seconds: 3 x 3 tiles with ragged tails."""
@@ -165,6 +165,18 @@ def test_automatic_split_statistic(gpu):
               f"passes {pA} / {pB}")
         assert abs(sA - ref[0]) < 1e-3 * ref[0] and abs(sB - ref[1]) < 1e-3 * ref[1]
         assert pA == pB == (2 if max(sA, sB) > 16 else 1)
+    # the rank-one (per-token) form computes the same statistic from its factorisations
+    wt = synth.token_workload("tokens_attn").scaled(T=3000, m=320, n=384, iters=4)
+    dt = synth.generate_tokens(wt)
+    f = ffe.FlipFlop(tokens=(to_device(dt.x, gpu), to_device(dt.g, gpu)))
+    f.iterate(wt.iters)
+    A, B = (X.double().cpu().numpy() for X in f.factors())
+    sA, sB, pA, pB = f.whiten_split_state()
+    f.close()
+    ref = [float(np.mean(np.diag(X) * np.diag(np.linalg.inv(X)))) for X in (A, B)]
+    print(f"{wt.name}: device s(A) {sA:.6f} s(B) {sB:.6f}; fp64 {ref[0]:.6f} {ref[1]:.6f}")
+    assert abs(sA - ref[0]) < 1e-3 * ref[0] and abs(sB - ref[1]) < 1e-3 * ref[1]
+    assert pA == pB == (2 if max(sA, sB) > 16 else 1)
     # forced settings report their pass counts and no statistic
     w = small_workload("attn", m=256, n=256, N=4)
     G = to_device(synth.generate(w).G, gpu)
