@@ -130,7 +130,10 @@ typedef struct {
                              (from the column norms of L^-1; rms whitening
                              distortion 2^-9 sqrt(s/3)); the whitenings use
                              two passes while the latest s of A or of B
-                             exceeds 16, one pass otherwise;
+                             exceeds 16, and always when fewer than 16
+                             samples per dimension determine a factor
+                             (min(N m / n, N n / m); rank-one form:
+                             N / max(m, n)), one pass otherwise;
                              1 = L^-1 rounded to bf16 once;
                              2 = L^-1 split as hi + lo bf16 parts (two passes,
                              smaller whitening error).  The Frobenius

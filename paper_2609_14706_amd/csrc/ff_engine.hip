@@ -500,6 +500,24 @@ ff_status chol_blocked(ff_handle_s* h, Side& s, int iteration) {
 // (s(A) = 21) 2.4e-3 and a 512 x 1280 layer from 4 samples (s(A) up to 26)
 // 7.9e-3 with one pass, which the second pass removes.
 constexpr double kSplitThreshold = 16.0;
+// Automatic split, shape rule: the whitening's rounding perturbs every
+// sample's term alike, and the iteration amplifies that perturbation the
+// more, the fewer samples determine each factor.  Across the measured cases
+// the one-pass error follows r = min(N m / n, N n / m) (rank-one form:
+// T / max(m, n)), samples per dimension of the less determined factor,
+// rather than s: r = 128, 48, 24 (the three widest-sampled layers) gave
+// 2.4e-4 to 4.2e-4, while r = 11 (768 x 512, 16 samples; s <= 4.6) gave
+// 1.1e-3, r = 6 (11008 x 4096, 16 samples; s <= 15.5) 3.4e-3 against 2.8e-4
+// with two passes, r = 1.6 (512 x 1280, 4 samples) 7.9e-3.  Below this r
+// both whitenings always use two passes.
+constexpr double kMinSamplesPerDim = 16.0;
+
+// Samples per dimension of the less determined factor (see above).
+double samples_per_dim(const ff_handle_s* h) {
+  const double m = (double)h->m, n = (double)h->n, N = (double)h->N;
+  if (h->lay.rank1) return N / std::max(m, n);
+  return N * std::min(m, n) / std::max(m, n);
+}
 
 // L^-1 of the dim x dim factor at src into s.Li and the whitening operand
 // s.Lw; sum log L_jj per leaf into s.slots.
@@ -549,14 +567,16 @@ ff_status operand(ff_handle_s* h, Side& s, int slot, int iteration) {
 // whitening by p's operand goes into the update of the other factor, whose
 // own conditioning then amplifies it in its small eigenvalues (an
 // 8192 x 28672 layer with s(A) = 21 and s(B) = 2.3 keeps a flat likelihood
-// only with both whitenings split).  The Frobenius operand is not an inverse,
-// so the statistic does not apply to it: one pass.
+// only with both whitenings split); and always two when few samples
+// determine the factors (kMinSamplesPerDim).  The Frobenius operand is not
+// an inverse, so the statistic does not apply to it: one pass.
 const bf16_t* second_part(const ff_handle_s* h, const Side& p, const int** use2,
                           const int** use2b) {
   *use2 = *use2b = nullptr;
   if (p.Lw2 == nullptr) return nullptr;
   if (h->cfg.whiten_split == 2) return (const bf16_t*)p.Lw2;
   if (h->cfg.estimator == FF_EST_FROBENIUS) return nullptr;
+  if (samples_per_dim(h) < kMinSamplesPerDim) return (const bf16_t*)p.Lw2;
   *use2 = h->A.split_flag;
   *use2b = h->B.split_flag;
   return (const bf16_t*)p.Lw2;
@@ -1578,6 +1598,7 @@ ff_status ff_whiten_split_state(ff_handle h, double* s_A, double* s_B, int* pass
     if (h->cfg.whiten_split == 2) {
       passes = 2;
     } else if (h->cfg.estimator != FF_EST_FROBENIUS && h->A.split_flag != nullptr) {
+      if (samples_per_dim(h) < kMinSamplesPerDim) passes = 2;
       int flag[2] = {0, 0};
       const Side* sides[2] = {&h->A, &h->B};
       for (int k = 0; k < 2; ++k) {
@@ -1588,7 +1609,7 @@ ff_status ff_whiten_split_state(ff_handle h, double* s_A, double* s_B, int* pass
                                 hipMemcpyDeviceToHost, h->stream));
       }
       FF_HIP(hipStreamSynchronize(h->stream));
-      passes = (flag[0] || flag[1]) ? 2 : 1;
+      if (flag[0] || flag[1]) passes = 2;
     }
   }
   if (s_A) *s_A = sv[0];

@@ -37,13 +37,14 @@ def test_mlp_fullsize(gpu, key):
     G = synth.generate_device(w, device=gpu)
 
     # (b) the configured number of iterations on a fresh handle, with the
-    # library's default (automatic) whitening precision.  The widest layer's
-    # input factor has condition ~3e5 and rounding sensitivity s(A) ~ 21:
-    # the rule whitens with the hi/lo split of L^-1 there (one pass stays
-    # inside the 5e-3 bar, 2.4e-3 against an fp64 flip-flop on the same
-    # samples, but its likelihood drifts by ~2e-4 N m n over the last
-    # iterations, also when only the A-side operand is split); the two other
-    # layers (s <= 13) get one pass.
+    # library's default (automatic) whitening precision.  The widest layer
+    # has 9.1 samples per dimension of its input factor (N m / n) and
+    # rounding sensitivity s(A) ~ 21: the rule whitens with the hi/lo split of
+    # L^-1 there (one pass stays inside the 5e-3 bar, 2.4e-3 against an fp64
+    # flip-flop on the same samples, but its likelihood drifts by ~2e-4 N m n
+    # over the last iterations, also when only the A-side operand is split);
+    # the two other layers (48 and 24 samples per dimension, s <= 13) get one
+    # pass.
     print(f"[{w.name}] {w.iters} iterations, automatic whitening split", flush=True)
     f = ffe.FlipFlop(G)
     ll = f.iterate(w.iters)

@@ -98,7 +98,9 @@ def test_iterations_match_the_oracle(gpu, key):
     A1, B1 = (X.double().cpu().numpy() for X in f.factors())
     f.iterate(w.iters - 1)
     A, B = (X.double().cpu().numpy() for X in f.factors())
+    sA, sB, pA, pB = f.whiten_split_state()
     f.close()
+    print(f"[{key}] automatic whitening split: s(A) {sA:.2f}, s(B) {sB:.2f}, passes {pA}", flush=True)
     del G
     _free()
     out = {}

@@ -149,10 +149,17 @@ def test_automatic_split_statistic(gpu):
     """The device statistic s = (1/dim) sum_j F_jj (F^-1)_jj of the last
     factorised A and B equals its fp64 evaluation from the returned factors
     (s is invariant under the trace normalisation's scaling), and both
-    whitenings use two passes exactly when max(s(A), s(B)) > 16."""
+    whitenings use two passes exactly when max(s(A), s(B)) > 16 or fewer than
+    16 samples per dimension determine a factor (min(N m / n, N n / m); the
+    rank-one form: T / max(m, n))."""
     import torch
     import paper_2609_14706_amd as ffe
-    for key, kw in (("mlp_down", dict(m=512, n=1280, N=4)), ("attn", dict(m=512, n=768, N=8))):
+
+    def expected_passes(sA, sB, r):
+        return 2 if (max(sA, sB) > 16 or r < 16) else 1
+
+    for key, kw in (("mlp_down", dict(m=512, n=1280, N=4)), ("attn", dict(m=512, n=768, N=8)),
+                    ("attn", dict(m=512, n=512, N=32))):
         w = small_workload(key, **kw)
         d = synth.generate(w)
         f = ffe.FlipFlop(to_device(d.G, gpu))
@@ -161,10 +168,11 @@ def test_automatic_split_statistic(gpu):
         sA, sB, pA, pB = f.whiten_split_state()
         f.close()
         ref = [float(np.mean(np.diag(X) * np.diag(np.linalg.inv(X)))) for X in (A, B)]
+        r = w.N * min(w.m, w.n) / max(w.m, w.n)
         print(f"{w.name}: device s(A) {sA:.6f} s(B) {sB:.6f}; fp64 {ref[0]:.6f} {ref[1]:.6f}; "
-              f"passes {pA} / {pB}")
+              f"{r:.1f} samples per dimension; passes {pA} / {pB}")
         assert abs(sA - ref[0]) < 1e-3 * ref[0] and abs(sB - ref[1]) < 1e-3 * ref[1]
-        assert pA == pB == (2 if max(sA, sB) > 16 else 1)
+        assert pA == pB == expected_passes(sA, sB, r)
     # the rank-one (per-token) form computes the same statistic from its factorisations
     wt = synth.token_workload("tokens_attn").scaled(T=3000, m=320, n=384, iters=4)
     dt = synth.generate_tokens(wt)
@@ -176,7 +184,7 @@ def test_automatic_split_statistic(gpu):
     ref = [float(np.mean(np.diag(X) * np.diag(np.linalg.inv(X)))) for X in (A, B)]
     print(f"{wt.name}: device s(A) {sA:.6f} s(B) {sB:.6f}; fp64 {ref[0]:.6f} {ref[1]:.6f}")
     assert abs(sA - ref[0]) < 1e-3 * ref[0] and abs(sB - ref[1]) < 1e-3 * ref[1]
-    assert pA == pB == (2 if max(sA, sB) > 16 else 1)
+    assert pA == pB == expected_passes(sA, sB, wt.T / max(wt.m, wt.n))
     # forced settings report their pass counts and no statistic
     w = small_workload("attn", m=256, n=256, N=4)
     G = to_device(synth.generate(w).G, gpu)

@@ -19,7 +19,7 @@ def _config(G, dtype):
     cfg.dtype = ffe.FF_BF16 if dtype == "bf16" else ffe.FF_F32
     cfg.G = G.data_ptr()
     cfg.stream = torch.cuda.current_stream(G.device).cuda_stream
-    cfg.whiten_split = 1
+    cfg.whiten_split = 0  # the library's default (automatic), as in the workspace path below
     return cfg
 
 
@@ -36,7 +36,7 @@ def _noalloc(G, iters, dtype):
 
 def _workspace_path(G, iters):
     import paper_2609_14706_amd as ffe
-    f = ffe.FlipFlop(G)
+    f = ffe.FlipFlop(G, whiten_split=0)
     ll = f.iterate(iters)
     A, B = f.factors()
     f.close()
