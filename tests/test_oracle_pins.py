@@ -430,6 +430,11 @@ def test_rev_cholesky_definition_and_inverse():
     assert np.allclose(np.triu(L, 1), 0) and np.all(np.diag(L) > 0)
     assert np.allclose(L.T @ L, M, atol=1e-12)
     assert np.allclose(np.linalg.inv(L), np.linalg.cholesky(np.linalg.inv(M)), atol=1e-10)
+    # the normalised inverse (Algorithm 2's error-spreading matrix) is unit
+    # lower triangular and L times it is diagonal with L's own diagonal
+    Lt = oracle.normalised_inverse(M)
+    assert np.allclose(np.triu(Lt, 1), 0) and np.allclose(np.diag(Lt), 1.0)
+    assert np.allclose(L @ Lt, np.diag(np.diag(L)), atol=1e-10)
 
 
 def test_waterfilling_scales_of_the_babai_figure():
