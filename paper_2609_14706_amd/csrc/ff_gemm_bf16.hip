@@ -12,13 +12,17 @@
 //    i of the Section 5 updates), upper tiles only, split over k into
 //    deterministic partial sums that a second kernel adds in fixed order.
 //
-// Operands move global -> LDS with the direct-to-LDS loads of gfx950
-// (global_load_lds_dwordx4, no register staging) in 64-wide k pairs, so that
-// every copy request is a whole 128-byte line (half-line requests cost about
-// 15% of the symmetric product's time in L2 traffic), through two pair slots
-// (128 KB), one pair in flight ahead of the matrix cores.  The 16-byte chunks
-// of each 128-byte row are XOR-swizzled so that fragment reads of
-// consecutive rows hit distinct banks.
+// Operands move global -> LDS with the direct-to-LDS buffer loads of gfx950
+// (buffer_load_dwordx4 ... lds, no register staging) in 64-wide k pairs, so
+// that every copy request is a whole 128-byte line (half-line requests cost
+// about 15% of the symmetric product's time in L2 traffic), through two pair
+// slots (128 KB), one pair in flight ahead of the matrix cores.  The 16-byte
+// chunks of each 128-byte row are XOR-swizzled so that fragment reads of
+// consecutive rows hit distinct banks.  Copy and fragment-read addresses are
+// fixed per lane and set up once: inside the loop only scalar bases and
+// instruction offsets change (about 7 vector instructions per 64 products
+// instead of 30-50; worth about 1% under sustained load, where the clock is
+// power limited).
 #include "ff_common.hpp"
 #include "ff_kernels.hpp"
 
@@ -50,7 +54,6 @@ struct __align__(16) Ring {
 };
 
 __device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
-__device__ __forceinline__ int chunk_pos(int row, int c) { return row * 8 + (c ^ swz(row)); }
 
 // vmcnt(N) with the other counters left alone (gfx9 encoding).
 template <int N>
@@ -61,14 +64,22 @@ __device__ __forceinline__ void wait_vmem() {
 // lgkmcnt(0) with the other counters left alone.
 __device__ __forceinline__ void wait_lds() { __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4)); }
 
-// Element offset of the chunk this lane copies with instruction 0 of a pair;
+// Byte offset of the chunk this lane copies with instruction 0 of a pair;
 // instruction q (0..7) of wave w fills positions (4 q + w) 64 + lane, which
 // lie 32 q rows further down with the same swizzle, so its offset is
-// off + 32 q ld.
+// off + 64 q ld bytes (a scalar offset of the instruction).
 __device__ __forceinline__ uint32_t chunk_offset(int wave, int lane, uint32_t ld) {
   const int P = wave * 64 + lane;
   const int row = P >> 3, c = (P & 7) ^ swz(row);
-  return (uint32_t)row * ld + (uint32_t)c * 8u;
+  return ((uint32_t)row * ld + (uint32_t)c * 8u) * 2u;  // bytes
+}
+
+// Buffer resource of a pair's operand (gfx9 descriptor: base, stride 0, no
+// effective range limit, raw dword data format).  The copies then address
+// base (scalar) + the lane's fixed byte offset (vector) + the instruction's
+// row-group offset (scalar): no per-lane address arithmetic in the loop.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t pair_rsrc(const bf16_t* p) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(p), (short)0, (int)0x7fffffff, 0x00020000);
 }
 
 // Copy q (0..15) of a pair: operand q % 2, instruction q / 2.
@@ -77,11 +88,11 @@ __device__ __forceinline__ void issue_one(Ring& sm, int slot, const bf16_t* pa, 
                                           int wave, int q) {
   const int g = q >> 1;
   if (q & 1)
-    __builtin_amdgcn_global_load_lds((const void*)(pb + ob + (size_t)g * 32 * ldb),
-                                     (lds_void*)&sm.b[slot][(g * 4 + wave) * 64], 16, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(pair_rsrc(pb), (lds_void*)&sm.b[slot][(g * 4 + wave) * 64],
+                                             16, (int)ob, (int)((uint32_t)g * 64u * ldb), 0, 0);
   else
-    __builtin_amdgcn_global_load_lds((const void*)(pa + oa + (size_t)g * 32 * lda),
-                                     (lds_void*)&sm.a[slot][(g * 4 + wave) * 64], 16, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(pair_rsrc(pa), (lds_void*)&sm.a[slot][(g * 4 + wave) * 64],
+                                             16, (int)oa, (int)((uint32_t)g * 64u * lda), 0, 0);
 }
 
 __device__ __forceinline__ void issue_pair(Ring& sm, int slot, const bf16_t* pa, const bf16_t* pb,
@@ -96,14 +107,38 @@ __device__ __forceinline__ void issue_pair(Ring& sm, int slot, const bf16_t* pa,
 // quadrant, 8 consecutive k per lane.  f[kk][0..3] = A, f[kk][4..7] = B.
 typedef bf16x8 Frags[2][8];
 
+// Byte offsets (from the start of the Ring) of this lane's fragment chunks
+// in slot 0 for tile 0 of each operand, k half and 16-wide k step.  The
+// swizzle of a fragment row depends on the lane only (the tile's first row
+// is a multiple of 32), so every read is one of these eight registers plus
+// a constant: the slot (32 KB) and the tile (4 KB).
+struct FragBase {
+  uint32_t v[2][2][2];  // [operand B][half][kk]
+};
+
+__device__ __forceinline__ FragBase frag_base(int wave, int lane) {
+  FragBase fb;
+  const uint32_t s = (uint32_t)swz(lane & 31), hl = (uint32_t)(lane >> 5);
+#pragma unroll
+  for (int o = 0; o < 2; ++o)
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const uint32_t c = (uint32_t)(h * 4 + kk * 2) + hl;
+        const uint32_t row = (uint32_t)(o ? (wave & 1) : (wave >> 1)) * 128u + (uint32_t)(lane & 31);
+        fb.v[o][h][kk] = (o ? (uint32_t)sizeof(Ring::a) : 0u) + row * 128u + 16u * (c ^ s);
+      }
+  return fb;
+}
+
 // Fragment read q (0..15) of step `half` (0, 1) of the pair in `slot`:
 // k half q / 8, A tiles for q % 8 < 4, B tiles above.
-__device__ __forceinline__ void read_frag_one(const Ring& sm, int slot, int half, int wave, int lane,
+__device__ __forceinline__ void read_frag_one(const Ring& sm, int slot, int half, const FragBase& fb,
                                               Frags& f, int q) {
   const int kk = q >> 3, t = q & 7;
-  const int c = half * 4 + kk * 2 + (lane >> 5);
-  const int row = (t < 4 ? (wave >> 1) : (wave & 1)) * 128 + (t & 3) * 32 + (lane & 31);
-  f[kk][t] = __builtin_bit_cast(bf16x8, t < 4 ? sm.a[slot][chunk_pos(row, c)] : sm.b[slot][chunk_pos(row, c)]);
+  const uint32_t off = fb.v[t >= 4][half][kk] + (uint32_t)slot * (uint32_t)(PCH * 16) + (uint32_t)(t & 3) * 4096u;
+  f[kk][t] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(&sm) + off));
 }
 
 // Product m (0..31) of a step: k half m / 16, tile pair ((m / 4) % 4, m % 4).
@@ -126,13 +161,13 @@ __device__ __forceinline__ void mfma_one(const Frags& f, f32x16 (&acc)[4][4], in
 template <bool SW, bool READ, bool LOADS>
 __device__ __forceinline__ void step(Ring& sm, const Frags& cur, Frags& nxt, int rslot, int rhalf,
                                      int lslot, const bf16_t* pa, const bf16_t* pb, uint32_t oa,
-                                     uint32_t ob, uint32_t lda, uint32_t ldb, int wave, int lane,
+                                     uint32_t ob, uint32_t lda, uint32_t ldb, int wave, const FragBase& fb,
                                      f32x16 (&acc)[4][4]) {
 #pragma unroll
   for (int m = 0; m < 32; ++m) {
     mfma_one<SW>(cur, acc, m);
     if (READ && m < 24 && m % 3 != 2)
-      read_frag_one(sm, rslot, rhalf, wave, lane, nxt, (2 * m + (m % 3)) / 3);
+      read_frag_one(sm, rslot, rhalf, fb, nxt, (2 * m + (m % 3)) / 3);
     if (LOADS && m % 2 == 0) issue_one(sm, lslot, pa, pb, oa, ob, lda, ldb, wave, m / 2);
     __builtin_amdgcn_sched_barrier(0);
   }
@@ -172,6 +207,7 @@ __device__ __forceinline__ void mainloop(Ring& sm, int p0, int p1, uint32_t lda,
   const int n = p1 - p0;
   if (n <= 0) return;
   const uint32_t oa = chunk_offset(wave, lane, lda), ob = chunk_offset(wave, lane, ldb);
+  const FragBase fb = frag_base(wave, lane);
   const bf16_t *pa, *pb;
   if (!PRE) issue_prologue(sm, p0, p1, lda, ldb, addr);
   if (n > 1) {
@@ -182,28 +218,28 @@ __device__ __forceinline__ void mainloop(Ring& sm, int p0, int p1, uint32_t lda,
   __builtin_amdgcn_s_barrier();
   Frags F[2];
 #pragma unroll
-  for (int q = 0; q < 16; ++q) read_frag_one(sm, 0, 0, wave, lane, F[0], q);
+  for (int q = 0; q < 16; ++q) read_frag_one(sm, 0, 0, fb, F[0], q);
   int j = 0;
   for (; j + 2 < n; ++j) {  // steady: step B also copies pair j + 2
     const int slot = j & 1;
-    step<SW, true, false>(sm, F[0], F[1], slot, 1, 0, nullptr, nullptr, 0, 0, lda, ldb, wave, lane, acc);
+    step<SW, true, false>(sm, F[0], F[1], slot, 1, 0, nullptr, nullptr, 0, 0, lda, ldb, wave, fb, acc);
     wait_vmem<0>();  // pair j + 1 (the only pair in flight)
     wait_lds();      // this wave's reads of pair j are complete
     __builtin_amdgcn_s_barrier();
     addr(p0 + j + 2, pa, pb);
-    step<SW, true, true>(sm, F[1], F[0], slot ^ 1, 0, slot, pa, pb, oa, ob, lda, ldb, wave, lane, acc);
+    step<SW, true, true>(sm, F[1], F[0], slot ^ 1, 0, slot, pa, pb, oa, ob, lda, ldb, wave, fb, acc);
   }
   if (j + 1 < n) {
     const int slot = j & 1;
-    step<SW, true, false>(sm, F[0], F[1], slot, 1, 0, nullptr, nullptr, 0, 0, lda, ldb, wave, lane, acc);
+    step<SW, true, false>(sm, F[0], F[1], slot, 1, 0, nullptr, nullptr, 0, 0, lda, ldb, wave, fb, acc);
     wait_vmem<0>();
     wait_lds();
     __builtin_amdgcn_s_barrier();
-    step<SW, true, false>(sm, F[1], F[0], slot ^ 1, 0, 0, nullptr, nullptr, 0, 0, lda, ldb, wave, lane, acc);
+    step<SW, true, false>(sm, F[1], F[0], slot ^ 1, 0, 0, nullptr, nullptr, 0, 0, lda, ldb, wave, fb, acc);
     ++j;
   }
-  step<SW, true, false>(sm, F[0], F[1], j & 1, 1, 0, nullptr, nullptr, 0, 0, lda, ldb, wave, lane, acc);
-  step<SW, false, false>(sm, F[1], F[0], 0, 0, 0, nullptr, nullptr, 0, 0, lda, ldb, wave, lane, acc);
+  step<SW, true, false>(sm, F[0], F[1], j & 1, 1, 0, nullptr, nullptr, 0, 0, lda, ldb, wave, fb, acc);
+  step<SW, false, false>(sm, F[1], F[0], 0, 0, 0, nullptr, nullptr, 0, 0, lda, ldb, wave, fb, acc);
   __syncthreads();
 }
 
@@ -475,6 +511,7 @@ __global__ __launch_bounds__(256) void k_reduce_frag(const float* __restrict__ P
 hipError_t launch_whiten_bf16(const bf16_t* X, const bf16_t* Y, const bf16_t* Y2, const int* use2,
                               const int* use2b, bf16_t* C, int64_t rows, int64_t Kp, const int* st,
                               hipStream_t s, bool full) {
+  // Kp <= 2^20 keeps every copy's byte offset from its pair base below 2^31
   if (rows <= 0 || Kp <= 0 || rows % TM || Kp % TM || Kp > (1 << 20)) return hipErrorInvalidValue;
   const int64_t tiles = (rows / TM) * ((Kp / TM + 1) / 2);  // one workgroup per tile pair
   if (tiles > 0x7fffffff) return hipErrorInvalidValue;
@@ -498,7 +535,8 @@ hipError_t launch_whiten_norm_bf16(const bf16_t* X, const bf16_t* Y, const bf16_
 hipError_t launch_syrk_bf16(const bf16_t* X, int64_t dim_p, int64_t ld, int64_t seg_stride,
                             int64_t nseg, int splits, float* P, const int* st, hipStream_t s,
                             const bf16_t* Xb) {
-  if (dim_p <= 0 || dim_p % TM || ld <= 0 || ld % PK || nseg <= 0 || splits <= 0)
+  // ld <= 2^20 keeps every copy's byte offset from its pair base below 2^31
+  if (dim_p <= 0 || dim_p % TM || ld <= 0 || ld % PK || ld > (1 << 20) || nseg <= 0 || splits <= 0)
     return hipErrorInvalidValue;
   const int64_t T = dim_p / TM, ntiles = T * (T + 1) / 2;
   if ((int64_t)splits > (ld / PK) * nseg) return hipErrorInvalidValue;
