@@ -277,12 +277,14 @@ struct Timed {
     if (h->timing && h->ev_used + 2 <= h->events.size()) {
       ev = h->ev_used;
       h->ev_used += 2;
-      hipEventRecord(h->events[ev], h->stream);
+      // a failed record only loses this measurement; a broken stream shows
+      // at the call's next checked launch
+      (void)hipEventRecord(h->events[ev], h->stream);
     }
   }
   ~Timed() {
     if (ev != SIZE_MAX) {
-      hipEventRecord(h->events[ev + 1], h->stream);
+      (void)hipEventRecord(h->events[ev + 1], h->stream);
       h->pending.push_back({kernel, ev, flop});
     }
   }
@@ -1554,22 +1556,24 @@ ff_status ff_quantize(ff_handle h, const float* W, const float* A, const float* 
 
 ff_status ff_destroy(ff_handle h) {
   if (h == nullptr) return FF_OK;
-  hipStreamSynchronize(h->stream);
+  // best-effort teardown: every object is released even if an earlier
+  // release reports an error (there is nothing left to report it to)
+  (void)hipStreamSynchronize(h->stream);
   if (h->aux != nullptr) {
-    hipStreamSynchronize(h->aux);
-    hipStreamDestroy(h->aux);
-    hipEventDestroy(h->fork);
-    hipEventDestroy(h->join);
+    (void)hipStreamSynchronize(h->aux);
+    (void)hipStreamDestroy(h->aux);
+    (void)hipEventDestroy(h->fork);
+    (void)hipEventDestroy(h->join);
   }
   for (Side* sd : {&h->A, &h->B}) {
     if (sd->istream != nullptr) {
-      hipStreamSynchronize(sd->istream);
-      hipStreamDestroy(sd->istream);
-      hipEventDestroy(sd->ev_leaf);
-      hipEventDestroy(sd->ev_inv);
+      (void)hipStreamSynchronize(sd->istream);
+      (void)hipStreamDestroy(sd->istream);
+      (void)hipEventDestroy(sd->ev_leaf);
+      (void)hipEventDestroy(sd->ev_inv);
     }
   }
-  for (hipEvent_t e : h->events) hipEventDestroy(e);
+  for (hipEvent_t e : h->events) (void)hipEventDestroy(e);
   delete h;
   return FF_OK;
 }

@@ -437,6 +437,24 @@ __device__ __forceinline__ void grouped_tile(uint32_t idx, uint32_t T, uint32_t&
   ti = tj = 0;
 }
 
+// Work item of workgroup b when the dispatcher places b on XCD b % 8 and
+// each XCD runs its workgroups in order, 32 at a time: round r of XCD x
+// takes items 256 r + 32 x .. + 31, so that the eight XCDs work on
+// neighbouring items (the same k split) at the same time and each XCD's
+// 32 co-resident workgroups take consecutive items (a compact group of
+// tiles).  The workgroups past the last full round take the remaining
+// items XCD by XCD.  A bijection of [0, total).
+__device__ __forceinline__ uint32_t round_item(uint32_t b, uint32_t total) {
+  const uint32_t q = total >> 3, rem = total & 7u;
+  const uint32_t x = b & 7u, li = b >> 3;
+  const uint32_t full = (q / 32u) * 32u;  // local indices in full rounds (every XCD has them)
+  if (li < full) return (li / 32u) * 256u + x * 32u + (li % 32u);
+  // tail: XCD x holds wx - full items, wx = q + (x < rem)
+  const uint32_t tail = q - full;
+  const uint32_t before = x * tail + min(x, rem);
+  return full * 8u + before + (li - full);
+}
+
 __global__ __launch_bounds__(NTHR, 1) void k_syrk_bf16(const bf16_t* __restrict__ X,
                                                        const bf16_t* __restrict__ Xb, uint32_t ld,
                                                        uint64_t seg_stride, uint32_t nseg,
@@ -444,7 +462,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_syrk_bf16(const bf16_t* __restrict_
                                                        float* __restrict__ P, const int* st) {
   if (ff_halted(st)) return;
   __shared__ Ring sm;
-  const uint32_t t = xcd_remap(blockIdx.x, gridDim.x);
+  const uint32_t t = round_item(blockIdx.x, gridDim.x);
   const uint32_t z = t / ntiles, tile = t % ntiles;
   uint32_t ti, tj;
   grouped_tile(tile, T, ti, tj);
