@@ -10,7 +10,7 @@ leaves a choice open, the reading taken is stated in the docstring.
 """
 from .flipflop import (FlipFlopResult, NotSPDError, as_f64_samples, half_step_B, half_step_B_rows,
                        half_step_A, half_step_A_rows, normalise, damp, flipflop, loglik, objective)
-from .metrics import kron_rel_error, trace_identity
+from .metrics import kron_rel_error, kron_rel_error_scale_free, trace_identity
 from .kron import kron_apply, mismatch_factor
 from .waterkron import (rev_cholesky, normalised_inverse, waterfilling_scales, gptq,
                         two_sided_gptq, distortion)
@@ -21,7 +21,7 @@ from .tokens import (half_step_A_tokens, half_step_B_tokens, half_step_B_tokens_
 
 __all__ = ["FlipFlopResult", "NotSPDError", "as_f64_samples", "half_step_B", "half_step_B_rows",
            "half_step_A", "half_step_A_rows", "normalise", "damp", "flipflop", "loglik", "objective",
-           "kron_rel_error", "trace_identity",
+           "kron_rel_error", "kron_rel_error_scale_free", "trace_identity",
            "kron_apply", "mismatch_factor", "half_step_A_tokens", "half_step_B_tokens", "half_step_B_tokens_rows",
            "flipflop_tokens", "loglik_tokens", "objective_tokens", "materialise", "token_weights",
            "rev_cholesky", "normalised_inverse", "waterfilling_scales", "gptq", "two_sided_gptq",

@@ -35,6 +35,16 @@ def kron_rel_error(A, B, A_ref, B_ref) -> float:
     return float(np.sqrt(max(sq, 0.0)) / den)
 
 
+def kron_rel_error_scale_free(A, B, A_ref, B_ref) -> float:
+    """|| A(x)B / ||A(x)B|| - A_ref(x)B_ref / ||A_ref(x)B_ref|| ||_F: the error
+    of the products' directions, blind to an overall scale (the error
+    metric's scale-free companion).  Each factor is scaled to unit norm (the
+    product then has unit norm) and the stable form above is applied."""
+    A, B, A_ref, B_ref = map(_f64, (A, B, A_ref, B_ref))
+    unit = lambda X: X / np.sqrt(np.sum(X * X))
+    return kron_rel_error(unit(A), unit(B), unit(A_ref), unit(B_ref))
+
+
 def trace_identity(G, A, B) -> float:
     """(1/(N m n)) sum_i tr(B^-1 G_i A^-1 G_i^T)  (Section 5 trace identity).
 

@@ -56,9 +56,10 @@ def test_tiny_workload_full_parity(gpu):
     A, B, ll, done = run_gpu(d.G, w.iters, gpu)
     ref = oracle.flipflop(d.G, w.iters)
     err = oracle.kron_rel_error(A, B, ref.A, ref.B)
-    print(f"tiny fp32 20 iterations: rel err {err:.3e}")
+    esf = oracle.kron_rel_error_scale_free(A, B, ref.A, ref.B)
+    print(f"tiny fp32 20 iterations: rel err {err:.3e} (scale-free {esf:.3e})")
     assert done == w.iters
-    assert err < TOL_F32
+    assert err < TOL_F32 and esf < TOL_F32
     # per-iteration log-likelihood against the oracle's, for the last iterate
     assert abs(ll[-1] - oracle.loglik(d.G, ref.A, ref.B)) < 1e-6 * abs(ll[-1])
     assert all(b >= a - 1e-6 * abs(a) for a, b in zip(ll, ll[1:]))
@@ -118,12 +119,14 @@ def test_bf16_config_shaped(gpu, key, m, n, N):
     A, B, ll, done = run_gpu(d.G, w.iters, gpu)
     ref = oracle.flipflop(d.G, w.iters)
     err = oracle.kron_rel_error(A, B, ref.A, ref.B)
+    esf = oracle.kron_rel_error_scale_free(A, B, ref.A, ref.B)
     A1, B1, _, _ = run_gpu(d.G, 1, gpu)
     r1 = oracle.flipflop(d.G, 1)
     err1 = oracle.kron_rel_error(A1, B1, r1.A, r1.B)
-    print(f"bf16 {key} {m}x{n} N={N}: rel err {err:.3e} after {w.iters}, {err1:.3e} after 1")
+    print(f"bf16 {key} {m}x{n} N={N}: rel err {err:.3e} after {w.iters} (scale-free {esf:.3e}), "
+          f"{err1:.3e} after 1")
     assert done == w.iters
-    assert err < TOL_BF16 and err1 < TOL_BF16
+    assert err < TOL_BF16 and err1 < TOL_BF16 and esf < TOL_BF16
 
 
 def test_bf16_ill_conditioned_split(gpu):

@@ -292,6 +292,28 @@ def test_kron_rel_error_matches_explicit_kronecker():
     assert abs(e - np.linalg.norm(dA) / np.linalg.norm(Ar)) < 1e-6 * e
 
 
+def test_scale_free_error_matches_explicit_kronecker():
+    """The scale-free error against its definition on the explicit products,
+    its blindness to scale, and its small-error limit."""
+    rng = np.random.default_rng(12)
+    A, Ar = rand_spd(4, rng), rand_spd(4, rng)
+    B, Br = rand_spd(3, rng), rand_spd(3, rng)
+    K, Kr = np.kron(A, B), np.kron(Ar, Br)
+    ref = np.linalg.norm(K / np.linalg.norm(K) - Kr / np.linalg.norm(Kr))
+    assert abs(oracle.kron_rel_error_scale_free(A, B, Ar, Br) - ref) < 1e-14
+    # a common scale, and a scale moved between the factors, are invisible
+    assert abs(oracle.kron_rel_error_scale_free(3.0 * A, 0.5 * B, Ar, 7.0 * Br) - ref) < 1e-14
+    assert oracle.kron_rel_error_scale_free(2.0 * Ar, Br / 2.0, Ar, Br) < 1e-15
+    # while the plain error sees a scale of the whole product
+    assert abs(oracle.kron_rel_error(1.01 * Ar, Br, Ar, Br) - 0.01) < 1e-12
+    # small direction errors agree with the plain error to first order
+    dA = 1e-7 * rng.standard_normal((4, 4))
+    dA -= np.sum(dA * Ar) / np.sum(Ar * Ar) * Ar  # orthogonal to Ar: no change of scale
+    e1 = oracle.kron_rel_error_scale_free(Ar + dA, Br, Ar, Br)
+    e2 = oracle.kron_rel_error(Ar + dA, Br, Ar, Br)
+    assert abs(e1 - e2) < 1e-6 * e2
+
+
 def test_kron_apply_matches_explicit_kronecker():
     rng = np.random.default_rng(12)
     m, n = 3, 5
