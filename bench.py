@@ -50,6 +50,22 @@ def recorded_traffic(kernel: str, workload: str):
 PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 
 
+def host_description() -> str:
+    """The host the oracle ran on: CPU model, logical CPUs, BLAS library."""
+    from threadpoolctl import threadpool_info
+    model = "unknown CPU"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    blas = sorted({f"{i.get('internal_api')} {i.get('version') or ''}".strip()
+                   for i in threadpool_info() if i.get("user_api") == "blas"}) or ["unknown BLAS"]
+    return f"{model}, {os.cpu_count()} logical CPUs, {', '.join(blas)}"
+
+
 def cpu_baseline(G, w, budget_s: float, estimator: str = "flipflop"):
     """Oracle time of one iteration, from a bounded number of samples.
 
@@ -383,8 +399,12 @@ def main():
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the fp64 oracle on host cores", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = (cpu_baseline_tokens(x, g, w, args.cpu_budget, args.estimator)
-                               if tokens else cpu_baseline(G, w, args.cpu_budget, args.estimator))
+        cb = (cpu_baseline_tokens(x, g, w, args.cpu_budget, args.estimator)
+              if tokens else cpu_baseline(G, w, args.cpu_budget, args.estimator))
+        # algorithmic rate of the oracle (its direct form executes about twice F_alg)
+        cb["alg_gflops"] = round(cb["value"] * flop_iter / 1e9, 2)
+        cb["host"] = host_description()
+        out["cpu_baseline"] = cb
     print(json.dumps(out), flush=True)
 
 
