@@ -17,7 +17,7 @@ m x n with the first N_p samples (16 for the two 11008-wide layers, 8 for the
 N_p n >= 2 m, which is 6, 6 and 7, so both factors are well determined):
 the fp64 oracle at the full N would take most of a day on a CPU.
 
-Usage: python tests/golden/make_fullsize_expected.py [attn] [mlp_up] [mlp_down] [mlp_large]
+Usage: python tests/golden/make_fullsize_expected.py [attn] [mlp_up[:N]] [mlp_down[:N]] [mlp_large[:N]]
 """
 from __future__ import annotations
 
@@ -62,8 +62,8 @@ def summary(A, B, rowsA, rowsB):
     }
 
 
-def run(key: str) -> str:
-    w = synth.workload(key).scaled(N=PARITY_N[key])
+def run(key: str, N: int | None = None) -> str:
+    w = synth.workload(key).scaled(N=N or PARITY_N[key])
     t0 = time.time()
     d = synth.generate(w)
     digests = synth.sample_digests(d.G)
@@ -103,6 +103,7 @@ def run(key: str) -> str:
 
 
 if __name__ == "__main__":
-    keys = sys.argv[1:] or list(PARITY_N)
-    for k in keys:
-        run(k)
+    # key or key:N (N samples instead of the default above)
+    for arg in sys.argv[1:] or list(PARITY_N):
+        k, _, n = arg.partition(":")
+        run(k, int(n) if n else None)
