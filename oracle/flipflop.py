@@ -14,7 +14,7 @@ Paper passages followed (Section 5, "The FlipFlop Hessian Approximation"):
   and both factors may be damped by a multiple of their mean diagonal,
   including between iterations.
 
-Readings taken where the paper only writes "proportional to":
+Readings taken where the paper gives the updates only up to a constant factor:
 
 * the expectation is the empirical mean over the N samples;
 * B is scaled by 1/(N n) and A by 1/(N m): the maximum-likelihood

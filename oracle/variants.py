@@ -10,7 +10,7 @@ lists
              iteration with A^-1, B^-1 replaced by A, B: a power iteration
              for min ||H - A (x) B||_F.
 
-Readings where the paper writes "proportional to":
+Readings where the paper gives the updates only up to a constant factor:
 * Frobenius keeps every convention of ``flipflop``: B first from A = I_n,
   scalings 1/(N n) for B and 1/(N m) for A, optional damping right after each
   update, trace normalisation tr(A) = n after each iteration.  The two
