@@ -11,11 +11,12 @@ each) and ``synth`` (the seeded inputs).  For every workload it stores, in
   and a seeded uniform sample of rows of A and B (fp32), the squared
   Frobenius norms, traces and log-determinants of both factors (fp64).
 
-The attention layer runs at its full N = 128.  The MLP layers run the full
-m x n with the first N_p samples (16 for the two 11008-wide layers, 8 for the
-28672-wide one; each above the smallest N_p with N_p m >= 2 n and
-N_p n >= 2 m, which is 6, 6 and 7, so both factors are well determined):
-the fp64 oracle at the full N would take most of a day on a CPU.
+The attention layer and the 4096 x 11008 layer run at their full N (128 and
+64).  The two other MLP layers run the full m x n with the first N_p samples
+(48 of 128 for the 11008 x 4096 layer, 8 of 32 for the 28672-wide one; each
+above the smallest N_p with N_p m >= 2 n and N_p n >= 2 m, which is 6 and 7,
+so both factors are well determined): the fp64 oracle at their full N would
+take 5 and 7 hours on 8 cores.
 
 Usage: python tests/golden/make_fullsize_expected.py [attn] [mlp_up[:N]] [mlp_down[:N]] [mlp_large[:N]]
 """
@@ -38,7 +39,7 @@ import oracle  # noqa: E402
 import synth   # noqa: E402
 
 OUT = os.path.join(os.path.dirname(os.path.abspath(__file__)), "fullsize")
-PARITY_N = {"attn": 128, "mlp_up": 16, "mlp_down": 16, "mlp_large": 8}
+PARITY_N = {"attn": 128, "mlp_up": 48, "mlp_down": 64, "mlp_large": 8}
 ROWS = 32
 
 
