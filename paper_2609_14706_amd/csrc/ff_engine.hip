@@ -363,6 +363,10 @@ ff_status inverse_p2(ff_handle_s* h, Side& s, int64_t o, int64_t sz, hipStream_t
   GemmF32 g = tree_gemm(h, s, t);
   // Li21 = -Li22 T
   g.A = t.Li22; g.B = t.Tt; g.C = t.Li21; g.M = t.r; g.N = t.hh; g.K = t.r;
+  // up to 2048 columns 64 x 64 tiles here too: the root's second product of
+  // a 4096 factor runs alone after the last leaf, and with 128 x 128 tiles
+  // its workgroups of the last row block (k = 2048) finish long after the rest
+  if (t.hh <= 2048) g.tile = 64;
   g.transA = 0; g.transB = 1; g.alpha = -1.f; g.beta = 0.f; g.flags = kKHiRow;
   FF_HIP(launch_gemm_f32(g, 1, st));
   return FF_OK;
